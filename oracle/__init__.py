@@ -1,0 +1,33 @@
+"""Reference oracle for the IsoLoCo outer aggregation step.
+
+TEST INFRASTRUCTURE ONLY.  This package is a plain, slow, float64 CPU
+implementation of the IsoLoCo outer step (Algorithm 2 of "Can Model Merging
+Improve Aggregation in DiLoCo?"), written from the paper so that the HIP path
+can be checked against it.  Only the test suite, the smoke check of
+``__graft_entry__`` and the ``cpu_baseline`` leg of ``bench.py`` may import it.
+The product path (``paper_2607_03011_amd``) never imports, links or calls it,
+and this package imports nothing from the product path.
+
+Contents
+--------
+``jacobi``       one-sided (Hestenes) Jacobi SVD with round-robin pair ordering
+``isoloco_step`` the outer step: pseudo-gradient mean (Algorithm 1's
+                 pseudo-gradient, averaged as in Algorithm 2), the isotropic
+                 correction of every exactly-2-D tensor (Algorithm 2's SVD
+                 branch, i.e. Iso-C of Section 2.2), and Nesterov momentum
+                 (Algorithm 2's last three assignments).
+
+Every function is pinned by ``tests/test_oracle_pins.py`` against values fixed
+by the mathematics (closed forms, invariants, library routines, brute force)
+rather than against itself.  One function is not pinned beyond itself: the
+behaviour on inputs whose smallest singular value is below float64 resolution
+(parity unpinned; the pseudo-gradients of the benchmark are full rank).
+"""
+from .jacobi import jacobi_svd, polar_factor  # noqa: F401
+from .isoloco_step import (  # noqa: F401
+    decode_bf16,
+    pseudo_gradient_mean,
+    iso_correct,
+    nesterov_update,
+    outer_step,
+)
