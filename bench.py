@@ -1,0 +1,200 @@
+"""Benchmark of the IsoLoCo outer step on one MI355X.
+
+One step = one full outer aggregation (K-way pseudo-gradient mean, polar
+iteration of every 2-D tensor, sigma_bar, fused Nesterov write-back) through
+the C ABI, on the 109.5M-parameter LLaMA-style workload (12 blocks d = 768,
+FFN 2048, tied 32000 x 768 embedding) with K = 16 float32 replicas resident in
+HBM.  Prints one JSON line.
+
+    python bench.py [--steps 20] [--warmup 3] [--workload 2] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+PEAK_FP32_MFMA_TFS = 157.3   # MI355X dense fp32 matrix, TFLOP/s
+
+
+def gemm_flops_per_step(layout, n_steps, check):
+    """Algorithmic flops of the batched products of one outer step: per polar
+    step and m x n matrix (m >= n), Gram X^T X (2 m n^2), polynomial A A
+    (2 n^3) and update X P (2 m n^2); plus one Gram for the check."""
+    f = 0
+    for (_, r, c, kind) in layout:
+        if kind != 0:
+            continue
+        m, n = max(r, c), min(r, c)
+        f += n_steps * (4 * m * n * n + 2 * n ** 3)
+        if check:
+            f += 2 * m * n * n
+    return f
+
+
+def reduce_bytes(layout, n_elems, K, wbytes):
+    """Algorithmic HBM bytes of the reduction kernel: every replica element
+    read once, theta read once, Delta written for 2-D tensors, and for the
+    other tensors the momentum read and theta + momentum written."""
+    b = 0
+    for (_, r, c, kind) in layout:
+        n = r * c
+        b += K * wbytes * n + 4 * n
+        b += 4 * n if kind == 0 else 12 * n
+    return b
+
+
+def finish_bytes(layout):
+    """Fused Nesterov write-back: reads Q, B, theta and writes B, theta (2-D tensors)."""
+    return sum(20 * r * c for (_, r, c, kind) in layout if kind == 0)
+
+
+def cpu_baseline(cfg, theta, workers, mom, budget_s):
+    """The float64 oracle timed on the host on a bounded sample of the step:
+    all 1-D tensors plus one tensor of each 2-D shape, extrapolated to the whole
+    step by the count of each shape."""
+    import numpy as np
+
+    import oracle
+    import oracle.jacobi as J
+    from collections import OrderedDict
+    shapes = OrderedDict()
+    for i, (off, r, c, kind) in enumerate(cfg.layout):
+        key = (r, c, kind) if kind == 0 else ("1d",)
+        shapes.setdefault(key, []).append(i)
+    th = theta.cpu().numpy()
+    mo = mom.cpu().numpy()
+    total = 0.0
+    timed = []
+    t_start = time.time()
+    for key, idx in shapes.items():
+        sel = idx if key == ("1d",) else idx[:1]
+        t0 = time.time()
+        for i in sel:
+            off, r, c, kind = cfg.layout[i]
+            sl = slice(off, off + r * c)
+            ws = [w for w in workers[:, sl].cpu().numpy()]
+            oracle.outer_step([(0, r, c, kind)], th[sl], ws, mo[sl], cfg.alpha, cfg.outer_lr, cfg.mu)
+        dt = time.time() - t0
+        total += dt * (len(idx) / len(sel))
+        timed.append("%s x%d" % ("1-D" if key == ("1d",) else "%dx%d" % key[:2], len(sel)))
+        if time.time() - t_start > budget_s:
+            break
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    return {"value": total * 1e3, "unit": "ms per outer step (extrapolated)",
+            "cores": threads if J.BACKEND == "c" else 1, "kind": "oracle",
+            "sample": "float64 oracle (one-sided Jacobi SVD, %s sweeps) on %s of the workload's "
+                      "tensors, each shape's time scaled by its count; host has %d cores" %
+                      (J.BACKEND, ", ".join(timed), len(os.sched_getaffinity(0)))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build measures one GPU; the IsoLoCo step here runs unsharded on a "
+              "single MI355X (--gpus %d is not supported)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_03011_amd as iso
+    from workload import CONFIGS, ReplicaGenerator
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    gen = ReplicaGenerator(cfg, seed=args.seed, device=dev)
+    theta, mom = gen.init_state()
+    workers = gen.workers(theta, step=1)
+    wdt = iso.ISOLOCO_F32 if cfg.worker_dtype == "f32" else iso.ISOLOCO_BF16
+    wbytes = 4 if cfg.worker_dtype == "f32" else 2
+    theta0 = theta.clone()
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, device=dev)
+    n_polar = len(plan.schedule())
+    stream = torch.cuda.current_stream(dev)
+    print("bench: workload %s, %d params, K=%d, %d polar steps, workspace %.2f GB" %
+          (cfg.name, cfg.n_params, cfg.K, n_polar, plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        plan.aggregate(theta, workers, mom, cfg.alpha, cfg.outer_lr, cfg.mu)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` outer steps, with per-launch HIP events on the
+    # step's stream (read back after each step)
+    plan.enable_timing(True)
+    acc = {k: 0.0 for k in ("total_ms", "reduce_ms", "gram_ms", "poly_ms", "update_ms", "finish_ms", "other_ms")}
+    launches = {"gemm": 0}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        plan.aggregate(theta, workers, mom, cfg.alpha, cfg.outer_lr, cfg.mu)
+        tm = plan.timing()
+        for k in acc:
+            acc[k] += getattr(tm, k)
+        launches["gemm"] += tm.gram_launches + tm.poly_launches + tm.update_launches
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    plan.enable_timing(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    per = {k: v / args.steps for k, v in acc.items()}
+    st = plan.stats()
+    resid = max(s.orth_resid for s, t in zip(st, cfg.layout) if t[3] == 0)
+
+    flops = gemm_flops_per_step(cfg.layout, n_polar, True)
+    gemm_ms = per["gram_ms"] + per["poly_ms"] + per["update_ms"]
+    gemm_tfs = flops / (gemm_ms * 1e-3) / 1e12
+    rbytes = reduce_bytes(cfg.layout, cfg.n_elems, cfg.K, wbytes)
+    red_gbs = rbytes / (per["reduce_ms"] * 1e-3) / 1e9
+    fbytes = finish_bytes(cfg.layout)
+    fin_gbs = fbytes / (per["finish_ms"] * 1e-3) / 1e9
+
+    out = {
+        "metric": "ms per IsoLoCo outer step",
+        "value": round(ms_per_step, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic: seeded low-rank + Gaussian-noise pseudo-gradients, replicas resident in HBM",
+        "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
+                   "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
+                   "polar_steps": n_polar, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel (Gram, polynomial and update products)",
+                     "achieved": round(gemm_tfs, 3), "peak": PEAK_FP32_MFMA_TFS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tfs / PEAK_FP32_MFMA_TFS, 4), "traffic": None,
+                     "flops_per_step": flops, "ms_per_step": round(gemm_ms, 4),
+                     "launches_per_step": launches["gemm"] // args.steps},
+        "roofline_reduce": {"bound": "hbm", "kernel": "reduce_kernel", "achieved": round(red_gbs, 1),
+                            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(red_gbs / PEAK_HBM_GBS, 4),
+                            "traffic": None, "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4)},
+        "roofline_finish": {"bound": "hbm", "kernel": "finish_kernel", "achieved": round(fin_gbs, 1),
+                            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(fin_gbs / PEAK_HBM_GBS, 4),
+                            "bytes_per_launch": fbytes, "ms": round(per["finish_ms"], 4)},
+        "phases_ms": {k: round(v, 4) for k, v in per.items()},
+        "max_orth_resid": resid,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget)
+    plan.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,178 @@
+/*
+ * isoloco.h -- C ABI of the IsoLoCo outer aggregation step for AMD MI355X (gfx950).
+ *
+ * The operation (Algorithm 2 of "Can Model Merging Improve Aggregation in
+ * DiLoCo?", arXiv 2607.03011) takes the global parameters theta, K worker
+ * replicas theta_k and the outer momentum buffer B, and performs one outer
+ * step in place:
+ *
+ *   Delta   = (1/K) sum_k (theta - theta_k)            averaged pseudo-gradient
+ *                                                       (sign as in Algorithm 1)
+ *   D_l     = alpha * sigma_bar_l * U_l V_l^T           every tensor l of kind ISO
+ *             with Delta_l = U_l S_l V_l^T and sigma_bar_l = trace(S_l) / min(rows, cols)
+ *             (Iso-C spectrum flattening, Section 2.2; the SVD branch of Algorithm 2)
+ *   D_l     = Delta_l                                   every tensor of kind AVG
+ *             (1-D tensors: "left unchanged", Section 4)
+ *   B      <- mu * B + D;   P = D + mu * B;   theta <- theta - outer_lr * P
+ *                                                       (Nesterov, Algorithm 2)
+ *
+ * alpha is an extra isotropic scale; alpha = 1 is the paper.  U V^T is not
+ * obtained from an SVD: it is the orthogonal polar factor of Delta_l, computed
+ * by a fixed polynomial (Newton-Schulz-type) iteration on matrix products
+ * (Section 4.3 motivates the iteration; this library runs it to convergence
+ * rather than for a fixed 5 steps), and sigma_bar_l = <Q_l, Delta_l>_F / r.
+ *
+ * Memory.  The caller owns every buffer.  theta, B and the K replicas are flat
+ * device arrays of n_elems elements that share one layout, described by a
+ * table of tensors.  The library never allocates device memory: the caller
+ * provides a workspace of isoloco_workspace_size() bytes.
+ *
+ * Asynchrony.  isoloco_aggregate() only enqueues work on the caller's HIP
+ * stream and returns; buffers must stay valid until the stream passes that
+ * point.  One plan must not be used by two streams at once; distinct plans
+ * are independent.
+ *
+ * Errors.  Every function returns an isoloco_status; no C++ exception crosses
+ * this boundary.  A call that fails validation enqueues nothing.  The last
+ * error message of the calling thread is available from isoloco_last_error().
+ */
+#ifndef ISOLOCO_H
+#define ISOLOCO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ISOLOCO_MAX_WORKERS 128
+
+typedef enum {
+  ISOLOCO_OK = 0,
+  ISOLOCO_ERR_INVALID_ARG = -1, /* null pointer, K out of range, non-finite scalar, bad option  */
+  ISOLOCO_ERR_LAYOUT = -2,      /* tensor out of range, overlapping, rows/cols < 1, bad kind     */
+  ISOLOCO_ERR_ALIGN = -3,       /* a device base pointer is not 16-byte aligned                  */
+  ISOLOCO_ERR_ALIAS = -4,       /* theta, momentum, a worker or the workspace overlap            */
+  ISOLOCO_ERR_WORKSPACE = -5,   /* workspace missing, too small or misaligned                    */
+  ISOLOCO_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed                    */
+  ISOLOCO_ERR_UNSUPPORTED = -7  /* a valid request this build does not implement                 */
+} isoloco_status;
+
+typedef enum { ISOLOCO_F32 = 0, ISOLOCO_BF16 = 1 } isoloco_dtype;
+
+typedef enum {
+  ISOLOCO_KIND_ISO = 0, /* a rows x cols matrix: spectrum flattened (Algorithm 2, dim = 2) */
+  ISOLOCO_KIND_AVG = 1  /* plain mean pseudo-gradient (1-D tensors, or 2-D kept plain)     */
+} isoloco_kind;
+
+/* One tensor of the flat layout: elements [offset, offset + rows*cols) of every
+ * buffer, row-major.  A 1-D tensor of length n is {offset, n, 1, AVG}.
+ * Elements covered by no tensor are left untouched. */
+typedef struct {
+  int64_t offset;
+  int64_t rows;
+  int64_t cols;
+  int32_t kind;     /* isoloco_kind */
+  int32_t reserved; /* must be 0 */
+} isoloco_tensor;
+
+/* Plan options; pass NULL for the defaults (every field 0 also selects the default). */
+typedef struct {
+  int32_t max_steps; /* cap on the polar iteration's steps (default 40)                          */
+  float ell0;        /* assumed lower bound of sigma_min / ||Delta^T Delta||_F^(1/2), the start
+                        of the polynomial schedule (default 1e-10)                               */
+  float tol;         /* the schedule stops when every singular value is within tol of 1
+                        (default 1e-6)                                                           */
+  int32_t check;     /* 1: after the last step also form Q^T Q to report the orthonormality
+                        residual per matrix in isoloco_get_stats (default 1); -1: skip it        */
+} isoloco_options;
+
+/* Per-tensor results of the last isoloco_aggregate() on a plan. */
+typedef struct {
+  float sigma_bar;  /* mean singular value of Delta_l (ISO tensors; 0 for AVG)            */
+  float fro_norm;   /* ||Delta_l||_F                                                        */
+  float orth_resid; /* ||Q^T Q - I||_F / sqrt(r) on the short side (ISO, if checked; else -1) */
+  int32_t steps;    /* polar iteration steps taken (ISO tensors)                             */
+  int32_t flags;    /* bit 0: Delta_l had a non-finite value; bit 1: Delta_l == 0;
+                       bit 2: residual above 1e-3 (not converged)                            */
+  int32_t reserved;
+} isoloco_tensor_stats;
+
+#define ISOLOCO_FLAG_NONFINITE 1
+#define ISOLOCO_FLAG_ZERO 2
+#define ISOLOCO_FLAG_NOT_CONVERGED 4
+
+typedef struct isoloco_plan_s* isoloco_plan_t;
+
+/* Build a plan for one layout.  Host only: validates the table (every tensor
+ * inside [0, n_elems), no two overlapping, rows and cols >= 1, kind valid),
+ * orders the matrices for batched launches, builds the polynomial schedule
+ * and sizes the workspace.  1 <= K <= ISOLOCO_MAX_WORKERS.  On success
+ * *out_plan owns host memory released by isoloco_plan_destroy(). */
+isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int64_t n_elems,
+                            int32_t K, isoloco_dtype worker_dtype, const isoloco_options* opts,
+                            isoloco_plan_t* out_plan);
+
+/* Workspace bytes the plan needs (device memory, 256-byte aligned). */
+isoloco_status isoloco_workspace_size(isoloco_plan_t plan, size_t* bytes);
+
+/* Hand the plan a device workspace of at least isoloco_workspace_size() bytes,
+ * 256-byte aligned, on the current HIP device.  The caller keeps ownership.
+ * Copies the plan's device tables into it (synchronous); call once before
+ * the first aggregate, and again whenever the workspace moves. */
+isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t bytes);
+
+/* Enqueue one IsoLoCo outer step on `hip_stream` (a hipStream_t; NULL = the
+ * default stream).  global and momentum: float32 device arrays of n_elems,
+ * updated in place.  workers: HOST array of K device pointers, each to
+ * n_elems elements of worker_dtype (read only; copied into the launch, so
+ * the host array may be freed on return).  All device pointers 16-byte
+ * aligned; workers must not overlap global, momentum or the workspace.
+ * alpha, outer_lr and mu must be finite. */
+isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void* const* workers,
+                                 float* momentum, float alpha, float outer_lr, float mu,
+                                 void* hip_stream);
+
+/* Copy the per-tensor statistics of the last aggregate to the host
+ * (n_tensors entries, in layout order).  Waits for that aggregate's stream. */
+isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out, int32_t n_tensors);
+
+/* The polynomial schedule of the plan: for step k, p_k(x) = c[3k] x + c[3k+1] x^3 + c[3k+2] x^5
+ * (on singular values normalised by ||Delta^T Delta||_F^(1/2)).  Writes at most
+ * max_steps triples; *n_steps receives the schedule length.  Host only. */
+isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps,
+                                int32_t* n_steps);
+
+/* Per-kernel timing of the last aggregate, measured with HIP events recorded
+ * on the aggregate's stream around every launch (enable first; the events
+ * add a few microseconds per launch).  Not part of the operation itself. */
+typedef struct {
+  float total_ms;   /* first launch start to last launch end                       */
+  float reduce_ms;  /* K-way reduction (+ Nesterov of the uncorrected tensors)     */
+  float gram_ms;    /* batched Gram products X^T X, all steps (+ the check)        */
+  float poly_ms;    /* batched polynomial products b A + c A^2, all steps          */
+  float update_ms;  /* batched updates X <- a X + X P, all steps                   */
+  float finish_ms;  /* fused Nesterov write-back of the corrected tensors          */
+  float other_ms;   /* norms, split-K sums, trace and sigma_bar                    */
+  int32_t gram_launches, poly_launches, update_launches, launches;
+} isoloco_timing;
+
+/* enable = 1 turns per-launch event timing on for later aggregates, 0 off. */
+isoloco_status isoloco_enable_timing(isoloco_plan_t plan, int32_t enable);
+
+/* Timing of the last aggregate (waits for its stream). */
+isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out);
+
+isoloco_status isoloco_plan_destroy(isoloco_plan_t plan);
+
+const char* isoloco_status_string(isoloco_status s);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* isoloco_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISOLOCO_H */

@@ -11,9 +11,34 @@ operation.  Tall matrices are first reduced by a Householder QR (a library
 primitive): if M = Q_r R then M and R share singular values and V, and
 U = Q_r U_R.  Nothing here is blocked, fused or reordered beyond that.
 """
+import ctypes
+import os
+
 import numpy as np
 
 _EPS = np.finfo(np.float64).eps
+
+_CLIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libjacobi_sweeps.so")
+_clib = None
+if os.path.exists(_CLIB_PATH):
+    _clib = ctypes.CDLL(_CLIB_PATH)
+    _clib.jacobi_columns.restype = ctypes.c_int
+    _clib.jacobi_columns.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                     ctypes.c_double, ctypes.c_int]
+
+# "c": the compiled twin of _jacobi_columns (jacobi_sweeps.c), same pair order,
+# rotation and stopping rule; "numpy": the vectorised loop below.
+BACKEND = "c" if _clib is not None else "numpy"
+
+
+def _jacobi_columns_c(Wt, tol, max_sweeps):
+    n, m = Wt.shape
+    Vt = np.ascontiguousarray(np.eye(n))
+    assert Wt.flags["C_CONTIGUOUS"] and Wt.dtype == np.float64
+    sweeps = _clib.jacobi_columns(Wt.ctypes.data, n, m, Vt.ctypes.data, float(tol), int(max_sweeps))
+    if sweeps < 0:
+        raise RuntimeError("one-sided Jacobi did not converge in %d sweeps" % max_sweeps)
+    return Vt, sweeps
 
 
 def _tournament_rounds(n):
@@ -110,7 +135,10 @@ def jacobi_svd(M, tol=None, max_sweeps=60):
     if tol is None:
         tol = 1e-15 * np.sqrt(Wt.shape[1])
     if Wt.shape[0] >= 2:
-        Vt_acc, _ = _jacobi_columns(Wt, tol, max_sweeps)
+        if BACKEND == "c" and _clib is not None:
+            Vt_acc, _ = _jacobi_columns_c(Wt, tol, max_sweeps)
+        else:
+            Vt_acc, _ = _jacobi_columns(Wt, tol, max_sweeps)
     else:
         Vt_acc = np.eye(Wt.shape[0])
     W = Wt[:n].T

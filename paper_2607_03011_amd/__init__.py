@@ -1,0 +1,237 @@
+"""IsoLoCo outer aggregation step on AMD MI355X (gfx950).
+
+Thin ctypes binding of ``libisoloco.so`` (C ABI declared in
+``include/isoloco.h``).  Every function below has the name and the argument
+order of the C function it marshals; ``IsoLoCoPlan`` bundles them with a
+torch-allocated workspace.  All arithmetic runs in the HIP kernels of the
+library: if the library is missing, importing the binding raises.
+"""
+import ctypes
+import os
+
+__all__ = [
+    "ISOLOCO_F32", "ISOLOCO_BF16", "ISOLOCO_KIND_ISO", "ISOLOCO_KIND_AVG",
+    "IsoLoCoError", "isoloco_tensor", "isoloco_options", "isoloco_tensor_stats",
+    "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
+    "isoloco_get_stats", "isoloco_schedule", "isoloco_plan_destroy", "isoloco_status_string",
+    "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing", "isoloco_timing",
+    "IsoLoCoPlan", "LIB_PATH", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libisoloco.so")
+
+ISOLOCO_F32 = 0
+ISOLOCO_BF16 = 1
+ISOLOCO_KIND_ISO = 0
+ISOLOCO_KIND_AVG = 1
+ISOLOCO_FLAG_NONFINITE = 1
+ISOLOCO_FLAG_ZERO = 2
+ISOLOCO_FLAG_NOT_CONVERGED = 4
+
+EXPORTED_SYMBOLS = (
+    "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
+    "isoloco_get_stats", "isoloco_schedule", "isoloco_plan_destroy", "isoloco_status_string",
+    "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
+)
+
+
+class isoloco_tensor(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_int64), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("kind", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class isoloco_options(ctypes.Structure):
+    _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
+                ("check", ctypes.c_int32)]
+
+
+class isoloco_tensor_stats(ctypes.Structure):
+    _fields_ = [("sigma_bar", ctypes.c_float), ("fro_norm", ctypes.c_float),
+                ("orth_resid", ctypes.c_float), ("steps", ctypes.c_int32),
+                ("flags", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class isoloco_timing(ctypes.Structure):
+    _fields_ = [("total_ms", ctypes.c_float), ("reduce_ms", ctypes.c_float), ("gram_ms", ctypes.c_float),
+                ("poly_ms", ctypes.c_float), ("update_ms", ctypes.c_float), ("finish_ms", ctypes.c_float),
+                ("other_ms", ctypes.c_float), ("gram_launches", ctypes.c_int32),
+                ("poly_launches", ctypes.c_int32), ("update_launches", ctypes.c_int32),
+                ("launches", ctypes.c_int32)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libisoloco.so is not built: run `python -m paper_2607_03011_amd.build` "
+                      "(or __graft_entry__.build()) first")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_P = ctypes.c_void_p
+_sig = {
+    "isoloco_plan": (ctypes.c_int, [ctypes.POINTER(isoloco_tensor), ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_int32, ctypes.c_int, ctypes.POINTER(isoloco_options),
+                                    ctypes.POINTER(_P)]),
+    "isoloco_workspace_size": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
+    "isoloco_set_workspace": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
+    "isoloco_aggregate": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), _P, ctypes.c_float,
+                                         ctypes.c_float, ctypes.c_float, _P]),
+    "isoloco_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_tensor_stats), ctypes.c_int32]),
+    "isoloco_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
+                                        ctypes.POINTER(ctypes.c_int32)]),
+    "isoloco_plan_destroy": (ctypes.c_int, [_P]),
+    "isoloco_enable_timing": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "isoloco_get_timing": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_timing)]),
+    "isoloco_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "isoloco_last_error": (ctypes.c_char_p, []),
+}
+for _name, (_res, _args) in _sig.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+class IsoLoCoError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = _lib.isoloco_last_error().decode()
+        super().__init__("%s: %s (%d)%s" % (where, _lib.isoloco_status_string(status).decode(), status,
+                                            (": " + msg) if msg else ""))
+
+
+def _check(status, where):
+    if status != 0:
+        raise IsoLoCoError(status, where)
+
+
+def isoloco_status_string(status):
+    return _lib.isoloco_status_string(status).decode()
+
+
+def isoloco_last_error():
+    return _lib.isoloco_last_error().decode()
+
+
+def isoloco_plan(layout, n_elems, K, worker_dtype=ISOLOCO_F32, opts=None):
+    """layout: sequence of (offset, rows, cols, kind).  Returns an opaque plan handle."""
+    arr = (isoloco_tensor * max(len(layout), 1))()
+    for i, (off, rows, cols, kind) in enumerate(layout):
+        arr[i] = isoloco_tensor(int(off), int(rows), int(cols), int(kind), 0)
+    o = None
+    if opts is not None:
+        o = ctypes.byref(opts if isinstance(opts, isoloco_options) else isoloco_options(**opts))
+    h = _P()
+    _check(_lib.isoloco_plan(arr, len(layout), int(n_elems), int(K), int(worker_dtype), o,
+                             ctypes.byref(h)), "isoloco_plan")
+    return h
+
+
+def isoloco_workspace_size(plan):
+    n = ctypes.c_size_t()
+    _check(_lib.isoloco_workspace_size(plan, ctypes.byref(n)), "isoloco_workspace_size")
+    return n.value
+
+
+def isoloco_set_workspace(plan, dev_ptr, nbytes):
+    _check(_lib.isoloco_set_workspace(plan, _P(int(dev_ptr)), int(nbytes)), "isoloco_set_workspace")
+
+
+def isoloco_aggregate(plan, global_ptr, worker_ptrs, momentum_ptr, alpha, outer_lr, mu, stream=0):
+    arr = (_P * max(len(worker_ptrs), 1))(*[_P(int(p)) for p in worker_ptrs])
+    _check(_lib.isoloco_aggregate(plan, _P(int(global_ptr)), arr, _P(int(momentum_ptr)),
+                                  float(alpha), float(outer_lr), float(mu), _P(int(stream))),
+           "isoloco_aggregate")
+
+
+def isoloco_get_stats(plan, n_tensors):
+    arr = (isoloco_tensor_stats * max(n_tensors, 1))()
+    _check(_lib.isoloco_get_stats(plan, arr, n_tensors), "isoloco_get_stats")
+    return [arr[i] for i in range(n_tensors)]
+
+
+def isoloco_schedule(plan, max_steps=256):
+    buf = (ctypes.c_double * (3 * max_steps))()
+    n = ctypes.c_int32()
+    _check(_lib.isoloco_schedule(plan, buf, max_steps, ctypes.byref(n)), "isoloco_schedule")
+    return [tuple(buf[3 * k: 3 * k + 3]) for k in range(min(n.value, max_steps))]
+
+
+def isoloco_enable_timing(plan, enable=True):
+    _check(_lib.isoloco_enable_timing(plan, 1 if enable else 0), "isoloco_enable_timing")
+
+
+def isoloco_get_timing(plan):
+    t = isoloco_timing()
+    _check(_lib.isoloco_get_timing(plan, ctypes.byref(t)), "isoloco_get_timing")
+    return t
+
+
+def isoloco_plan_destroy(plan):
+    _check(_lib.isoloco_plan_destroy(plan), "isoloco_plan_destroy")
+
+
+class IsoLoCoPlan:
+    """A plan plus its workspace, allocated as a torch uint8 tensor on the
+    current device.  ``aggregate`` marshals torch tensors to the C call and
+    enqueues on the current torch stream (or ``stream``)."""
+
+    def __init__(self, layout, n_elems, K, worker_dtype=ISOLOCO_F32, opts=None, device=None):
+        import torch
+        self.layout = [tuple(int(v) for v in t) for t in layout]
+        self.n_elems = int(n_elems)
+        self.K = int(K)
+        self.worker_dtype = worker_dtype
+        self.handle = isoloco_plan(self.layout, n_elems, K, worker_dtype, opts)
+        self.ws_bytes = isoloco_workspace_size(self.handle)
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        with torch.cuda.device(dev):
+            self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+            base = self.workspace.data_ptr()
+            self._ws_ptr = (base + 255) // 256 * 256
+            isoloco_set_workspace(self.handle, self._ws_ptr, self.ws_bytes)
+
+    def aggregate(self, theta, workers, momentum, alpha=1.0, outer_lr=0.7, mu=0.9, stream=None):
+        import torch
+        for t in (theta, momentum):
+            if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != self.n_elems:
+                raise ValueError("theta and momentum must be contiguous float32 of n_elems")
+        wdt = torch.float32 if self.worker_dtype == ISOLOCO_F32 else torch.bfloat16
+        if isinstance(workers, torch.Tensor):
+            if workers.dim() != 2 or workers.shape[0] != self.K or workers.shape[1] != self.n_elems:
+                raise ValueError("workers tensor must be [K, n_elems]")
+            if workers.dtype != wdt or not workers.is_contiguous():
+                raise ValueError("workers must be contiguous %s" % wdt)
+            ptrs = [workers[k].data_ptr() for k in range(self.K)]
+        else:
+            ws = list(workers)
+            if len(ws) != self.K:
+                raise ValueError("expected %d workers" % self.K)
+            for w in ws:
+                if w.dtype != wdt or not w.is_contiguous() or w.numel() != self.n_elems:
+                    raise ValueError("each worker must be contiguous %s of n_elems" % wdt)
+            ptrs = [w.data_ptr() for w in ws]
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device).cuda_stream
+        isoloco_aggregate(self.handle, theta.data_ptr(), ptrs, momentum.data_ptr(), alpha, outer_lr,
+                          mu, stream)
+
+    def stats(self):
+        return isoloco_get_stats(self.handle, len(self.layout))
+
+    def enable_timing(self, enable=True):
+        isoloco_enable_timing(self.handle, enable)
+
+    def timing(self):
+        return isoloco_get_timing(self.handle)
+
+    def schedule(self):
+        return isoloco_schedule(self.handle)
+
+    def close(self):
+        if self.handle is not None:
+            isoloco_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

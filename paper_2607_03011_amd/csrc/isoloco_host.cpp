@@ -1,0 +1,705 @@
+// Host side of the IsoLoCo C ABI: validation, planning, polynomial schedule,
+// workspace layout and the launch sequence of one outer step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "isoloco.h"
+#include "isoloco_kernels.h"
+#include "isoloco_types.h"
+
+using namespace isoloco;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+isoloco_status fail(isoloco_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+isoloco_status hip_fail(hipError_t e, const char* what) {
+  return fail(ISOLOCO_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+
+enum Phase { kPhReduce = 0, kPhGram, kPhPoly, kPhUpdate, kPhFinish, kPhOther };
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Polynomial schedule
+// ---------------------------------------------------------------------------
+//
+// The polar factor Q = U V^T of X is the limit of X_{k+1} = p_k(X_k), where
+// p_k(x) = a x + b x^3 + c x^5 acts on every singular value independently.
+// With all singular values of X_0 in [l, u], each p_k is chosen greedily as
+// the odd quintic closest to 1 in the max norm on [max(l, rho u), s u]
+// (minimax, found by the Remez exchange: for an odd quintic the error
+// 1 - p equioscillates on the two end points and the two interior critical
+// points, which are the positive roots of p'(x) = a + 3 b x^2 + 5 c x^4).
+// The cushion rho keeps the interior minimum of p far from 0, and s (slightly
+// above 1 while the interval is wide) absorbs rounding that pushes singular
+// values past u.  The image of [l, u] under p_k is the next interval; the
+// schedule ends when it is within tol of 1.  Once the interval is narrow the
+// minimax polynomial tends to x (15 - 10 x^2 + 3 x^4) / 8, which is used
+// directly for intervals narrower than 1e-3.
+
+constexpr double kCushion = 0.1;
+constexpr double kSafety = 1.02;
+
+bool solve4(double M[4][5], double out[4]) {
+  for (int col = 0; col < 4; ++col) {
+    int piv = col;
+    for (int r = col + 1; r < 4; ++r)
+      if (std::fabs(M[r][col]) > std::fabs(M[piv][col])) piv = r;
+    if (M[piv][col] == 0.0) return false;
+    if (piv != col)
+      for (int c = 0; c < 5; ++c) std::swap(M[piv][c], M[col][c]);
+    for (int r = 0; r < 4; ++r) {
+      if (r == col) continue;
+      const double f = M[r][col] / M[col][col];
+      for (int c = col; c < 5; ++c) M[r][c] -= f * M[col][c];
+    }
+  }
+  for (int i = 0; i < 4; ++i) out[i] = M[i][4] / M[i][i];
+  return true;
+}
+
+// Positive critical points of p (roots of a + 3 b y + 5 c y^2 with y = x^2).
+int critical_points(const double co[3], double xs[2]) {
+  const double a = co[0], b = co[1], c = co[2];
+  int n = 0;
+  if (c == 0.0) {
+    if (b != 0.0) {
+      const double y = -a / (3.0 * b);
+      if (y > 0) xs[n++] = std::sqrt(y);
+    }
+    return n;
+  }
+  const double disc = 9.0 * b * b - 20.0 * a * c;
+  if (disc < 0) return 0;
+  const double r = std::sqrt(disc);
+  double y1 = (-3.0 * b - r) / (10.0 * c), y2 = (-3.0 * b + r) / (10.0 * c);
+  if (y1 > y2) std::swap(y1, y2);
+  if (y1 > 0) xs[n++] = std::sqrt(y1);
+  if (y2 > 0) xs[n++] = std::sqrt(y2);
+  return n;
+}
+
+// Minimax odd quintic approximation of 1 on [lam, 1], 0 < lam < 1.
+bool remez_quintic(double lam, double co[3]) {
+  const double kPi = 3.14159265358979323846;
+  double x[4];
+  for (int i = 0; i < 4; ++i) x[i] = lam + (1.0 - lam) * (1.0 - std::cos(kPi * i / 3.0)) / 2.0;
+  bool ok = false;
+  for (int it = 0; it < 100; ++it) {
+    double M[4][5];
+    for (int i = 0; i < 4; ++i) {
+      const double xi = x[i], x3 = xi * xi * xi;
+      M[i][0] = xi;
+      M[i][1] = x3;
+      M[i][2] = x3 * xi * xi;
+      M[i][3] = (i % 2) ? -1.0 : 1.0;
+      M[i][4] = 1.0;
+    }
+    double sol[4];
+    if (!solve4(M, sol)) break;
+    co[0] = sol[0];
+    co[1] = sol[1];
+    co[2] = sol[2];
+    ok = true;
+    double cp[2];
+    if (critical_points(co, cp) != 2) break;
+    if (!(cp[0] > lam && cp[1] < 1.0 && cp[0] < cp[1])) break;
+    const double xn[4] = {lam, cp[0], cp[1], 1.0};
+    double dmax = 0;
+    for (int i = 0; i < 4; ++i) dmax = std::max(dmax, std::fabs(xn[i] - x[i]));
+    std::memcpy(x, xn, sizeof x);
+    if (dmax < 1e-15) break;
+  }
+  return ok;
+}
+
+double peval(const double co[3], double x) {
+  const double x2 = x * x;
+  return x * (co[0] + x2 * (co[1] + x2 * co[2]));
+}
+
+void interval_image(const double co[3], double l, double u, double* nl, double* nu) {
+  double lo = std::min(peval(co, l), peval(co, u)), hi = std::max(peval(co, l), peval(co, u));
+  double cp[2];
+  const int n = critical_points(co, cp);
+  for (int i = 0; i < n; ++i)
+    if (cp[i] > l && cp[i] < u) {
+      const double v = peval(co, cp[i]);
+      lo = std::min(lo, v);
+      hi = std::max(hi, v);
+    }
+  *nl = lo;
+  *nu = hi;
+}
+
+std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
+  std::vector<double> out;
+  double l = ell0, u = 1.0;
+  for (int k = 0; k < max_steps; ++k) {
+    double co[3];
+    if (1.0 - l / u < 1e-3) {
+      co[0] = 15.0 / 8.0 / u;
+      co[1] = -10.0 / 8.0 / (u * u * u);
+      co[2] = 3.0 / 8.0 / (u * u * u * u * u);
+    } else {
+      const double ud = u * ((l / u < 0.5) ? kSafety : 1.0);
+      const double ld = std::max(l, kCushion * u);
+      if (!remez_quintic(ld / ud, co)) {
+        co[0] = 15.0 / 8.0;
+        co[1] = -10.0 / 8.0;
+        co[2] = 3.0 / 8.0;
+      }
+      co[0] /= ud;
+      co[1] /= ud * ud * ud;
+      co[2] /= ud * ud * ud * ud * ud;
+    }
+    out.push_back(co[0]);
+    out.push_back(co[1]);
+    out.push_back(co[2]);
+    double nl, nu;
+    interval_image(co, l, u, &nl, &nu);
+    l = nl;
+    u = nu;
+    if (1.0 - l < tol && u - 1.0 < tol) break;
+  }
+  return out;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Plan
+// ---------------------------------------------------------------------------
+
+struct isoloco_plan_s {
+  std::vector<isoloco_tensor> layout;
+  int64_t n_elems = 0;
+  int K = 0;
+  int dtype = 0;
+  isoloco_options opts{};
+  std::vector<int> mat_of_tensor;
+  std::vector<MatInfo> mats;
+  std::vector<Chunk> chunks;
+  int n_iso_chunks = 0;
+  std::vector<Task> gram_tasks, poly_tasks, update_tasks;
+  std::vector<int> split_mats, split_n;
+  std::vector<double> sched;
+  int64_t n2d = 0;   // elements of one Delta / X buffer
+  int64_t nsq = 0;   // elements of one Gram / polynomial buffer
+  int64_t npart = 0; // elements of the split-K partial buffer
+  size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
+  size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
+  size_t off_poly = 0, off_gpart = 0, total = 0;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  int device = -1;
+  hipStream_t last_stream = nullptr;
+  bool has_run = false;
+  // per-launch timing
+  bool timing = false;
+  std::vector<hipEvent_t> events;  // 2 per timed launch
+  std::vector<int> ev_phase;
+  int ev_used = 0;
+};
+
+namespace {
+
+void plan_matrices(isoloco_plan_s* p) {
+  const int V = p->dtype == ISOLOCO_BF16 ? 8 : 4;
+  int64_t ws = 0, sq = 0, part = 0;
+  p->mat_of_tensor.assign(p->layout.size(), -1);
+  // corrected matrices and their chunks first
+  for (size_t t = 0; t < p->layout.size(); ++t) {
+    const isoloco_tensor& T = p->layout[t];
+    if (T.kind != ISOLOCO_KIND_ISO) continue;
+    MatInfo mi{};
+    mi.trans = T.rows < T.cols ? 1 : 0;
+    mi.m = (int32_t)std::max(T.rows, T.cols);
+    mi.n = (int32_t)std::min(T.rows, T.cols);
+    mi.src_off = T.offset;
+    mi.ws_off = ws;
+    mi.sq_off = sq;
+    mi.vec = (mi.m % 4 == 0 && mi.n % 4 == 0) ? 1 : 0;
+    mi.tensor = (int32_t)t;
+    const int64_t tiles = (mi.n + kBM - 1) / kBM;
+    // Split the Gram's K dimension when the matrix has few output tiles and
+    // a long K, so that no single tile dominates the launch.
+    int ks = 1;
+    if (mi.m >= 4 * mi.n && mi.m > 4096) {
+      ks = (int)std::min<int64_t>((1024 + tiles * tiles - 1) / (tiles * tiles), (mi.m + 1023) / 1024);
+      ks = std::max(ks, 1);
+    }
+    int64_t kchunk = (mi.m + ks - 1) / ks;
+    kchunk = (kchunk + kBK - 1) / kBK * kBK;
+    ks = (int)((mi.m + kchunk - 1) / kchunk);
+    mi.ksplit = ks;
+    mi.kchunk = (int32_t)kchunk;
+    mi.part_off = 0;
+    if (ks > 1) {
+      mi.part_off = part;
+      part += (int64_t)ks * mi.n * mi.n;
+      part = (part + 63) / 64 * 64;
+    }
+    const int64_t cnt = (int64_t)mi.m * mi.n;
+    mi.chunk_begin = (int32_t)p->chunks.size();
+    for (int64_t s = 0; s < cnt; s += kChunk) {
+      Chunk c{};
+      c.src = T.offset + s;
+      c.ws = ws + s;
+      c.count = (int32_t)std::min<int64_t>(kChunk, cnt - s);
+      c.mat = (int32_t)p->mats.size();
+      c.vec = (T.offset % V == 0) ? 1 : 0;
+      p->chunks.push_back(c);
+    }
+    mi.chunk_end = (int32_t)p->chunks.size();
+    p->mat_of_tensor[t] = (int)p->mats.size();
+    p->mats.push_back(mi);
+    ws += (cnt + 63) / 64 * 64;
+    sq += ((int64_t)mi.n * mi.n + 63) / 64 * 64;
+  }
+  p->n_iso_chunks = (int)p->chunks.size();
+  for (size_t t = 0; t < p->layout.size(); ++t) {
+    const isoloco_tensor& T = p->layout[t];
+    if (T.kind == ISOLOCO_KIND_ISO) continue;
+    const int64_t cnt = T.rows * T.cols;
+    for (int64_t s = 0; s < cnt; s += kChunk) {
+      Chunk c{};
+      c.src = T.offset + s;
+      c.ws = -1;
+      c.count = (int32_t)std::min<int64_t>(kChunk, cnt - s);
+      c.mat = -1;
+      c.vec = (T.offset % V == 0) ? 1 : 0;
+      p->chunks.push_back(c);
+    }
+  }
+  p->n2d = ws;
+  p->nsq = sq;
+  p->npart = part;
+
+  // Work lists, longest tasks first.
+  std::vector<int> order(p->mats.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    return (int64_t)p->mats[a].kchunk > (int64_t)p->mats[b].kchunk;
+  });
+  for (int mi : order) {
+    const MatInfo& M = p->mats[mi];
+    const int T = (M.n + kBM - 1) / kBM;
+    for (int ks = 0; ks < M.ksplit; ++ks)
+      for (int a = 0; a < T; ++a)
+        for (int b = 0; b < T; ++b) p->gram_tasks.push_back(Task{mi, a, b, ks});
+  }
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
+  for (int mi : order) {
+    const MatInfo& M = p->mats[mi];
+    const int T = (M.n + kBM - 1) / kBM;
+    for (int a = 0; a < T; ++a)
+      for (int b = 0; b < T; ++b) p->poly_tasks.push_back(Task{mi, a, b, 0});
+  }
+  for (int mi : order) {
+    const MatInfo& M = p->mats[mi];
+    const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
+    for (int a = 0; a < TM; ++a)
+      for (int b = 0; b < TN; ++b) p->update_tasks.push_back(Task{mi, a, b, 0});
+  }
+  for (size_t i = 0; i < p->mats.size(); ++i)
+    if (p->mats[i].ksplit > 1) {
+      p->split_mats.push_back((int)i);
+      p->split_n.push_back(p->mats[i].n);
+    }
+}
+
+void plan_workspace(isoloco_plan_s* p) {
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + std::max<size_t>(bytes, 1), kAlign);
+    return at;
+  };
+  p->off_mats = take(p->mats.size() * sizeof(MatInfo));
+  p->off_chunks = take(p->chunks.size() * sizeof(Chunk));
+  p->off_gt = take(p->gram_tasks.size() * sizeof(Task));
+  p->off_pt = take(p->poly_tasks.size() * sizeof(Task));
+  p->off_ut = take(p->update_tasks.size() * sizeof(Task));
+  p->off_sc = take(p->mats.size() * sizeof(MatScalars));
+  p->off_psq = take(p->chunks.size() * sizeof(double));
+  p->off_ptr = take(p->chunks.size() * sizeof(double));
+  p->off_delta = take((size_t)p->n2d * sizeof(float));
+  p->off_x0 = take((size_t)p->n2d * sizeof(float));
+  p->off_x1 = take((size_t)p->n2d * sizeof(float));
+  p->off_gram = take((size_t)p->nsq * sizeof(float));
+  p->off_poly = take((size_t)p->nsq * sizeof(float));
+  p->off_gpart = take((size_t)p->npart * sizeof(float));
+  p->total = o;
+}
+
+DevTables dev_tables(const isoloco_plan_s* p) {
+  DevTables t{};
+  char* w = p->ws;
+  t.mats = reinterpret_cast<const MatInfo*>(w + p->off_mats);
+  t.chunks = reinterpret_cast<const Chunk*>(w + p->off_chunks);
+  t.gram_tasks = reinterpret_cast<const Task*>(w + p->off_gt);
+  t.poly_tasks = reinterpret_cast<const Task*>(w + p->off_pt);
+  t.update_tasks = reinterpret_cast<const Task*>(w + p->off_ut);
+  t.scalars = reinterpret_cast<MatScalars*>(w + p->off_sc);
+  t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
+  t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
+  t.delta = reinterpret_cast<float*>(w + p->off_delta);
+  t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
+  t.x[1] = reinterpret_cast<float*>(w + p->off_x1);
+  t.gram = reinterpret_cast<float*>(w + p->off_gram);
+  t.poly = reinterpret_cast<float*>(w + p->off_poly);
+  t.gpart = reinterpret_cast<float*>(w + p->off_gpart);
+  t.n_mat = (int)p->mats.size();
+  t.n_chunks = (int)p->chunks.size();
+  t.n_iso_chunks = p->n_iso_chunks;
+  t.n_gram_tasks = (int)p->gram_tasks.size();
+  t.n_poly_tasks = (int)p->poly_tasks.size();
+  t.n_update_tasks = (int)p->update_tasks.size();
+  t.n_split = (int)p->split_mats.size();
+  t.split_mats_host = p->split_mats.data();
+  t.split_n_host = p->split_n.data();
+  return t;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int64_t n_elems,
+                            int32_t K, isoloco_dtype worker_dtype, const isoloco_options* opts,
+                            isoloco_plan_t* out_plan) {
+  g_last_error.clear();
+  if (!out_plan) return fail(ISOLOCO_ERR_INVALID_ARG, "out_plan is NULL");
+  *out_plan = nullptr;
+  if (n_tensors < 0) return fail(ISOLOCO_ERR_INVALID_ARG, "n_tensors < 0");
+  if (n_tensors > 0 && !layout) return fail(ISOLOCO_ERR_INVALID_ARG, "layout is NULL");
+  if (n_elems < 0) return fail(ISOLOCO_ERR_INVALID_ARG, "n_elems < 0");
+  if (K < 1 || K > ISOLOCO_MAX_WORKERS)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "K = %d outside [1, %d]", K, ISOLOCO_MAX_WORKERS);
+  if (worker_dtype != ISOLOCO_F32 && worker_dtype != ISOLOCO_BF16)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown worker dtype %d", (int)worker_dtype);
+  isoloco_options o{};
+  if (opts) o = *opts;
+  if (o.max_steps == 0) o.max_steps = 40;
+  if (o.ell0 == 0.f) o.ell0 = 1e-10f;
+  if (o.tol == 0.f) o.tol = 1e-6f;
+  if (o.check == 0) o.check = 1;
+  if (o.max_steps < 1 || o.max_steps > 200)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
+  if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
+  if (!(o.tol > 0.f && o.tol < 0.5f)) return fail(ISOLOCO_ERR_INVALID_ARG, "tol must be in (0, 0.5)");
+  if (o.check != 1 && o.check != -1) return fail(ISOLOCO_ERR_INVALID_ARG, "check must be 1 or -1");
+
+  std::vector<std::pair<int64_t, int64_t>> spans;
+  for (int32_t i = 0; i < n_tensors; ++i) {
+    const isoloco_tensor& T = layout[i];
+    if (T.rows < 1 || T.cols < 1)
+      return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: rows and cols must be >= 1", i);
+    if (T.rows > INT32_MAX || T.cols > INT32_MAX)
+      return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: dimension above 2^31-1", i);
+    if (T.kind != ISOLOCO_KIND_ISO && T.kind != ISOLOCO_KIND_AVG)
+      return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: unknown kind %d", i, T.kind);
+    if (T.reserved != 0) return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: reserved field must be 0", i);
+    if (T.offset < 0) return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: negative offset", i);
+    if (T.rows > n_elems / T.cols || T.offset > n_elems - T.rows * T.cols)
+      return fail(ISOLOCO_ERR_LAYOUT, "tensor %d: extends past n_elems", i);
+    spans.push_back({T.offset, T.offset + T.rows * T.cols});
+  }
+  std::sort(spans.begin(), spans.end());
+  for (size_t i = 1; i < spans.size(); ++i)
+    if (spans[i].first < spans[i - 1].second)
+      return fail(ISOLOCO_ERR_LAYOUT, "tensors overlap at element %lld", (long long)spans[i].first);
+
+  isoloco_plan_s* p = new (std::nothrow) isoloco_plan_s();
+  if (!p) return fail(ISOLOCO_ERR_INVALID_ARG, "out of host memory");
+  try {
+    p->layout.assign(layout, layout + n_tensors);
+    p->n_elems = n_elems;
+    p->K = K;
+    p->dtype = worker_dtype;
+    p->opts = o;
+    plan_matrices(p);
+    p->sched = build_schedule(o.ell0, o.tol, o.max_steps);
+    plan_workspace(p);
+  } catch (...) {
+    delete p;
+    return fail(ISOLOCO_ERR_INVALID_ARG, "out of host memory while planning");
+  }
+  *out_plan = p;
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_workspace_size(isoloco_plan_t plan, size_t* bytes) {
+  if (!plan || !bytes) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  *bytes = plan->total;
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t bytes) {
+  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
+  if (!dev_ptr) return fail(ISOLOCO_ERR_WORKSPACE, "workspace pointer is NULL");
+  if (bytes < plan->total)
+    return fail(ISOLOCO_ERR_WORKSPACE, "workspace of %zu bytes, plan needs %zu", bytes, plan->total);
+  if ((uintptr_t)dev_ptr % kAlign)
+    return fail(ISOLOCO_ERR_WORKSPACE, "workspace must be %zu-byte aligned", kAlign);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  char* w = static_cast<char*>(dev_ptr);
+  auto up = [&](size_t off, const void* src, size_t n) -> hipError_t {
+    if (n == 0) return hipSuccess;
+    return hipMemcpy(w + off, src, n, hipMemcpyHostToDevice);
+  };
+  if ((e = up(plan->off_mats, plan->mats.data(), plan->mats.size() * sizeof(MatInfo))) != hipSuccess ||
+      (e = up(plan->off_chunks, plan->chunks.data(), plan->chunks.size() * sizeof(Chunk))) != hipSuccess ||
+      (e = up(plan->off_gt, plan->gram_tasks.data(), plan->gram_tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_pt, plan->poly_tasks.data(), plan->poly_tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_ut, plan->update_tasks.data(), plan->update_tasks.size() * sizeof(Task))) != hipSuccess)
+    return hip_fail(e, "copying plan tables to the workspace");
+  if (!plan->mats.empty()) {
+    e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
+    if (e != hipSuccess) return hip_fail(e, "clearing per-matrix scalars");
+  }
+  plan->ws = w;
+  plan->ws_bytes = bytes;
+  plan->device = dev;
+  plan->has_run = false;
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void* const* workers,
+                                 float* momentum, float alpha, float outer_lr, float mu,
+                                 void* hip_stream) {
+  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
+  if (!plan->ws) return fail(ISOLOCO_ERR_WORKSPACE, "no workspace set (isoloco_set_workspace)");
+  if (!std::isfinite(alpha) || !std::isfinite(outer_lr) || !std::isfinite(mu))
+    return fail(ISOLOCO_ERR_INVALID_ARG, "alpha, outer_lr and mu must be finite");
+  const size_t nb = (size_t)plan->n_elems * sizeof(float);
+  const size_t wb = (size_t)plan->n_elems * (plan->dtype == ISOLOCO_BF16 ? 2 : 4);
+  if (plan->n_elems > 0) {
+    if (!global || !momentum || !workers)
+      return fail(ISOLOCO_ERR_INVALID_ARG, "global, momentum and workers must not be NULL");
+    if ((uintptr_t)global % 16 || (uintptr_t)momentum % 16)
+      return fail(ISOLOCO_ERR_ALIGN, "global and momentum must be 16-byte aligned");
+    if (overlaps(global, nb, momentum, nb)) return fail(ISOLOCO_ERR_ALIAS, "global and momentum overlap");
+    if (overlaps(global, nb, plan->ws, plan->total) || overlaps(momentum, nb, plan->ws, plan->total))
+      return fail(ISOLOCO_ERR_ALIAS, "global or momentum overlaps the workspace");
+    for (int k = 0; k < plan->K; ++k) {
+      const void* w = workers[k];
+      if (!w) return fail(ISOLOCO_ERR_INVALID_ARG, "worker %d pointer is NULL", k);
+      if ((uintptr_t)w % 16) return fail(ISOLOCO_ERR_ALIGN, "worker %d is not 16-byte aligned", k);
+      if (overlaps(w, wb, global, nb) || overlaps(w, wb, momentum, nb) ||
+          overlaps(w, wb, plan->ws, plan->total))
+        return fail(ISOLOCO_ERR_ALIAS, "worker %d overlaps global, momentum or the workspace", k);
+    }
+  }
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != plan->device)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "current device %d differs from the workspace's device %d", dev,
+                plan->device);
+
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  const DevTables t = dev_tables(plan);
+  StepArgs a{};
+  a.theta = global;
+  a.mom = momentum;
+  for (int k = 0; k < plan->K; ++k) a.workers.p[k] = workers[k];
+  a.K = plan->K;
+  a.worker_dtype = plan->dtype;
+  a.alpha = alpha;
+  a.lr = outer_lr;
+  a.mu = mu;
+
+  plan->ev_used = 0;
+  auto timed = [&](int phase, auto&& launch) -> hipError_t {
+    if (!plan->timing) return launch();
+    const size_t i = (size_t)plan->ev_used;
+    if (2 * i + 1 >= plan->events.size()) return launch();
+    hipError_t r = hipEventRecord(plan->events[2 * i], st);
+    if (r != hipSuccess) return r;
+    if ((r = launch()) != hipSuccess) return r;
+    r = hipEventRecord(plan->events[2 * i + 1], st);
+    plan->ev_phase[i] = phase;
+    plan->ev_used++;
+    return r;
+  };
+  e = timed(kPhReduce, [&] { return launch_reduce(t, a, st); });
+  if (e != hipSuccess) return hip_fail(e, "reduce launch");
+  if (t.n_mat > 0) {
+    if ((e = timed(kPhOther, [&] { return launch_fro(t, st); })) != hipSuccess)
+      return hip_fail(e, "fro launch");
+    const int S = (int)plan->sched.size() / 3;
+    const float* xin = t.delta;
+    for (int k = 0; k < S; ++k) {
+      PolarStep ps{};
+      ps.xin = xin;
+      ps.xout = t.x[k & 1];
+      ps.ca = (float)plan->sched[3 * k];
+      ps.cb = (float)plan->sched[3 * k + 1];
+      ps.cc = (float)plan->sched[3 * k + 2];
+      ps.first = (k == 0);
+      if ((e = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); })) != hipSuccess ||
+          (t.n_split && (e = timed(kPhOther, [&] { return launch_split_sums(t, st); })) != hipSuccess) ||
+          (k == 0 && (e = timed(kPhOther, [&] { return launch_gram_norm(t, 0, S, st); })) != hipSuccess) ||
+          (e = timed(kPhPoly, [&] { return launch_gemm(t, 1, ps, st); })) != hipSuccess ||
+          (e = timed(kPhUpdate, [&] { return launch_gemm(t, 2, ps, st); })) != hipSuccess)
+        return hip_fail(e, "polar step launch");
+      xin = ps.xout;
+    }
+    if (plan->opts.check == 1) {
+      PolarStep ps{};
+      ps.xin = xin;
+      if ((e = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); })) != hipSuccess ||
+          (t.n_split && (e = timed(kPhOther, [&] { return launch_split_sums(t, st); })) != hipSuccess) ||
+          (e = timed(kPhOther, [&] { return launch_gram_norm(t, 1, S, st); })) != hipSuccess)
+        return hip_fail(e, "check launch");
+    }
+    if ((e = timed(kPhOther, [&] { return launch_trace(t, xin, st); })) != hipSuccess ||
+        (e = timed(kPhFinish, [&] { return launch_finish(t, xin, a, st); })) != hipSuccess)
+      return hip_fail(e, "finish launch");
+  }
+  plan->last_stream = st;
+  plan->has_run = true;
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out, int32_t n_tensors) {
+  if (!plan || !out) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  if (n_tensors != (int32_t)plan->layout.size())
+    return fail(ISOLOCO_ERR_INVALID_ARG, "n_tensors = %d, plan has %zu tensors", n_tensors,
+                plan->layout.size());
+  std::vector<MatScalars> sc(plan->mats.size());
+  if (plan->has_run && !sc.empty()) {
+    hipError_t e = hipStreamSynchronize(plan->last_stream);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    e = hipMemcpy(sc.data(), plan->ws + plan->off_sc, sc.size() * sizeof(MatScalars),
+                  hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "copying statistics");
+  }
+  for (int32_t i = 0; i < n_tensors; ++i) {
+    isoloco_tensor_stats s{};
+    const int m = plan->mat_of_tensor[i];
+    if (m >= 0 && plan->has_run) {
+      s.sigma_bar = sc[m].sigma_bar;
+      s.fro_norm = sc[m].fro;
+      s.orth_resid = sc[m].resid;
+      s.steps = sc[m].steps;
+      s.flags = sc[m].flags;
+    } else {
+      s.fro_norm = -1.f;
+      s.orth_resid = -1.f;
+    }
+    out[i] = s;
+  }
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps, int32_t* n_steps) {
+  if (!plan || !n_steps) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  const int S = (int)plan->sched.size() / 3;
+  *n_steps = S;
+  if (coeffs)
+    for (int i = 0; i < 3 * std::min<int>(S, std::max(max_steps, 0)); ++i) coeffs[i] = plan->sched[i];
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_enable_timing(isoloco_plan_t plan, int32_t enable) {
+  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
+  if (enable && plan->events.empty()) {
+    const int n = 2 * 1024;
+    plan->events.resize(n);
+    plan->ev_phase.assign(n / 2, 0);
+    for (int i = 0; i < n; ++i) {
+      hipError_t e = hipEventCreate(&plan->events[i]);
+      if (e != hipSuccess) {
+        for (int j = 0; j < i; ++j) (void)hipEventDestroy(plan->events[j]);
+        plan->events.clear();
+        return hip_fail(e, "hipEventCreate");
+      }
+    }
+  }
+  plan->timing = enable != 0;
+  plan->ev_used = 0;
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out) {
+  if (!plan || !out) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  *out = isoloco_timing{};
+  if (!plan->timing || plan->ev_used == 0) return ISOLOCO_OK;
+  const int n = plan->ev_used;
+  hipError_t e = hipEventSynchronize(plan->events[2 * n - 1]);
+  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  float ms = 0;
+  if ((e = hipEventElapsedTime(&ms, plan->events[0], plan->events[2 * n - 1])) != hipSuccess)
+    return hip_fail(e, "hipEventElapsedTime");
+  out->total_ms = ms;
+  for (int i = 0; i < n; ++i) {
+    if ((e = hipEventElapsedTime(&ms, plan->events[2 * i], plan->events[2 * i + 1])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    out->launches++;
+    switch (plan->ev_phase[i]) {
+      case kPhReduce: out->reduce_ms += ms; break;
+      case kPhGram: out->gram_ms += ms; out->gram_launches++; break;
+      case kPhPoly: out->poly_ms += ms; out->poly_launches++; break;
+      case kPhUpdate: out->update_ms += ms; out->update_launches++; break;
+      case kPhFinish: out->finish_ms += ms; break;
+      default: out->other_ms += ms; break;
+    }
+  }
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_plan_destroy(isoloco_plan_t plan) {
+  if (plan)
+    for (hipEvent_t ev : plan->events) (void)hipEventDestroy(ev);
+  delete plan;
+  return ISOLOCO_OK;
+}
+
+const char* isoloco_status_string(isoloco_status s) {
+  switch (s) {
+    case ISOLOCO_OK: return "ok";
+    case ISOLOCO_ERR_INVALID_ARG: return "invalid argument";
+    case ISOLOCO_ERR_LAYOUT: return "invalid layout";
+    case ISOLOCO_ERR_ALIGN: return "misaligned pointer";
+    case ISOLOCO_ERR_ALIAS: return "overlapping buffers";
+    case ISOLOCO_ERR_WORKSPACE: return "workspace missing or too small";
+    case ISOLOCO_ERR_HIP: return "HIP runtime error";
+    case ISOLOCO_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* isoloco_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,644 @@
+// HIP kernels of the IsoLoCo outer step for gfx950 (MI355X).
+//
+//   reduce        K-way pseudo-gradient mean (Algorithm 1's sign, averaged as in
+//                 Algorithm 2), 16-byte loads, ||Delta||_F^2 partials per chunk
+//                 for the 2-D tensors, and the whole Nesterov step (Algorithm 2)
+//                 for tensors that are not corrected.
+//   fro           per-matrix Frobenius norm from the partials (pre-scaling).
+//   gemm          batched, grouped fp32 MFMA products for the polar iteration:
+//                 Gram A = X^T X, polynomial P = b A + c A^2, update X <- a X + X P.
+//   gram_norm     ||A||_F (first step: normalisation) or ||A - I||_F (check).
+//   trace/sigma   sigma_bar = <Q, Delta>_F / r (mean singular value, Algorithm 2).
+//   finish        fused Nesterov update and write-back of theta and B for the
+//                 corrected tensors (Algorithm 2).
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "isoloco_kernels.h"
+
+namespace isoloco {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum of one value per thread over a 256-thread block, in a fixed order.
+// Result valid in thread 0.
+__device__ __forceinline__ double block_sum256(double v, double* lds4) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) lds4[wave] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0) r = ((lds4[0] + lds4[1]) + lds4[2]) + lds4[3];
+  return r;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// ---------------------------------------------------------------------------
+// K-way reduction
+// ---------------------------------------------------------------------------
+
+template <int WDT>  // 0: float32 workers, 1: bfloat16 workers
+struct WorkerLoad;
+
+template <>
+struct WorkerLoad<0> {
+  static constexpr int kVec = 4;  // elements per 16-byte access
+  __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(static_cast<const float*>(p) + i);
+    out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
+  }
+  __device__ static __forceinline__ float one(const void* p, int64_t i) {
+    return static_cast<const float*>(p)[i];
+  }
+};
+
+template <>
+struct WorkerLoad<1> {
+  static constexpr int kVec = 8;
+  __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      out[2 * q] = __uint_as_float(w[q] << 16);
+      out[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  }
+  __device__ static __forceinline__ float one(const void* p, int64_t i) {
+    return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+  }
+};
+
+// Per element: Delta = (1/K) sum_k (theta - theta_k).  2-D (ISO) chunks store
+// Delta in the workspace and add Delta^2 to the chunk's partial; AVG chunks run
+// Nesterov in place: B <- mu B + Delta; theta <- theta - lr (Delta + mu B).
+template <int WDT>
+__global__ void __launch_bounds__(kStreamThreads)
+reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
+              float* __restrict__ mom, float* __restrict__ delta, double* __restrict__ part_sq,
+              WorkerPtrs w, int K, float inv_k, float lr, float mu) {
+  using WL = WorkerLoad<WDT>;
+  constexpr int V = WL::kVec;
+  __shared__ double red[4];
+  const Chunk c = chunks[blockIdx.x];
+  const bool iso = c.mat >= 0;
+  double sq = 0.0;
+  int done = 0;
+  if (c.vec) {
+    const int nv = c.count / V;
+    for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
+      const int64_t e = c.src + (int64_t)v * V;
+      float th[V], acc[V];
+#pragma unroll
+      for (int q = 0; q < V; q += 4) {
+        const floatx4 t4 = *reinterpret_cast<const floatx4*>(theta + e + q);
+        th[q] = t4[0]; th[q + 1] = t4[1]; th[q + 2] = t4[2]; th[q + 3] = t4[3];
+      }
+#pragma unroll
+      for (int q = 0; q < V; ++q) acc[q] = 0.f;
+#pragma unroll 4
+      for (int k = 0; k < K; ++k) {
+        float wv[V];
+        WL::vec(w.p[k], e, wv);
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc[q] += th[q] - wv[q];
+      }
+#pragma unroll
+      for (int q = 0; q < V; ++q) acc[q] *= inv_k;
+      if (iso) {
+        float* dst = delta + c.ws + (int64_t)v * V;
+#pragma unroll
+        for (int q = 0; q < V; q += 4) {
+          floatx4 o = {acc[q], acc[q + 1], acc[q + 2], acc[q + 3]};
+          *reinterpret_cast<floatx4*>(dst + q) = o;
+          sq += (double)acc[q] * acc[q] + (double)acc[q + 1] * acc[q + 1] +
+                (double)acc[q + 2] * acc[q + 2] + (double)acc[q + 3] * acc[q + 3];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < V; q += 4) {
+          floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + q);
+          floatx4 t4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float d = acc[q + r];
+            const float bn = mu * b4[r] + d;
+            b4[r] = bn;
+            t4[r] = th[q + r] - lr * (d + mu * bn);
+          }
+          *reinterpret_cast<floatx4*>(mom + e + q) = b4;
+          *reinterpret_cast<floatx4*>(theta + e + q) = t4;
+        }
+      }
+    }
+    done = nv * V;
+  }
+  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
+    const int64_t e = c.src + i;
+    const float th = theta[e];
+    float acc = 0.f;
+    for (int k = 0; k < K; ++k) acc += th - WL::one(w.p[k], e);
+    acc *= inv_k;
+    if (iso) {
+      delta[c.ws + i] = acc;
+      sq += (double)acc * acc;
+    } else {
+      const float bn = mu * mom[e] + acc;
+      mom[e] = bn;
+      theta[e] = th - lr * (acc + mu * bn);
+    }
+  }
+  if (iso) {
+    const double s = block_sum256(sq, red);
+    if (threadIdx.x == 0) part_sq[blockIdx.x] = s;
+  }
+}
+
+// ||Delta||_F per matrix, from the chunk partials in chunk order.
+__global__ void fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
+                           MatScalars* __restrict__ sc, int n_mat) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= n_mat) return;
+  const MatInfo mi = mats[m];
+  double s = 0.0;
+  for (int c = mi.chunk_begin; c < mi.chunk_end; ++c) s += part_sq[c];
+  MatScalars o;
+  o.fro = (float)sqrt(s);
+  o.flags = 0;
+  if (!isfinite(s)) o.flags |= 1;
+  else if (s == 0.0) o.flags |= 2;
+  o.inv_fro = (o.flags == 0) ? (float)(1.0 / sqrt(s)) : 0.f;
+  o.gscale = 0.f;
+  o.sigma_bar = 0.f;
+  o.resid = -1.f;
+  o.steps = 0;
+  o.pad = 0;
+  sc[m] = o;
+}
+
+// ---------------------------------------------------------------------------
+// Batched fp32 MFMA products of the polar iteration
+// ---------------------------------------------------------------------------
+//
+// Output tile 128 x 128 per 256-thread workgroup; wave w owns the 64 x 64
+// quarter (w >> 1, w & 1) as 2 x 2 blocks of v_mfma_f32_32x32x2f32.  K is
+// staged through LDS in slabs of 16, with the next slab's global loads in
+// flight while the current one is multiplied.  LDS holds both operands
+// k-major ([k][i], i contiguous) so that a wavefront's operand read is two
+// rows of 32 consecutive floats.
+
+constexpr int kLdsW = kBM + 4;
+
+// A 16 x 128 operand slab: element (k, i) at base + k * s_k + i * s_i, with
+// either s_i == 1 ("i-contiguous") or s_k == 1 ("k-contiguous").
+struct Operand {
+  const float* base;
+  int64_t s_k, s_i;
+  int K, I;       // bounds: k in [0, K), i in [0, I)
+  bool icontig;
+  bool vec;
+  float scale;
+};
+
+struct SlabRegs {
+  floatx4 v[2];
+};
+
+__device__ __forceinline__ void slab_load(const Operand& op, int k0, int i0, SlabRegs& r) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    floatx4 x = {0.f, 0.f, 0.f, 0.f};
+    if (op.icontig) {
+      const int k = k0 + (t >> 5) + 8 * rep;
+      const int i = i0 + 4 * (t & 31);
+      if (k < op.K) {
+        const float* p = op.base + (int64_t)k * op.s_k + i;
+        if (op.vec && i + 3 < op.I) {
+          x = *reinterpret_cast<const floatx4*>(p);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (i + e < op.I) x[e] = p[e];
+        }
+      }
+    } else {
+      const int i = i0 + (t >> 2) + 64 * rep;
+      const int k = k0 + 4 * (t & 3);
+      if (i < op.I) {
+        const float* p = op.base + (int64_t)i * op.s_i + k;
+        if (op.vec && k + 3 < op.K) {
+          x = *reinterpret_cast<const floatx4*>(p);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (k + e < op.K) x[e] = p[e];
+        }
+      }
+    }
+    r.v[rep] = x * op.scale;
+  }
+}
+
+__device__ __forceinline__ void slab_store(const Operand& op, const SlabRegs& r, float (*lds)[kLdsW]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    if (op.icontig) {
+      const int k = (t >> 5) + 8 * rep;
+      const int i = 4 * (t & 31);
+      *reinterpret_cast<floatx4*>(&lds[k][i]) = r.v[rep];
+    } else {
+      const int i = (t >> 2) + 64 * rep;
+      const int k = 4 * (t & 3);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) lds[k + e][i] = r.v[rep][e];
+    }
+  }
+}
+
+enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2 };
+
+struct GemmArgs {
+  const MatInfo* mats;
+  const Task* tasks;
+  const MatScalars* sc;
+  const float* xin;   // Gram/Update: X input buffer (Delta at step 0)
+  float* xout;        // Update: X output buffer
+  float* gram;        // n x n Gram buffers (Gram output, Poly input)
+  float* poly;        // n x n polynomial buffers (Poly output, Update input)
+  float* gpart;       // split-K Gram partials
+  float ca, cb, cc;   // step coefficients p(x) = ca x + cb x^3 + cc x^5
+  int first;          // 1 on the first step (inputs pre-scaled by 1/||Delta||_F, g applied)
+};
+
+template <int MODE>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs g) {
+  __shared__ float As[kBK][kLdsW];
+  __shared__ float Bs[kBK][kLdsW];
+
+  const Task task = g.tasks[blockIdx.x];
+  const MatInfo mi = g.mats[task.mat];
+  const int m = mi.m, n = mi.n;
+  const int64_t sr = mi.trans ? 1 : n;
+  const int64_t sc = mi.trans ? m : 1;
+  const bool vec = mi.vec != 0;
+  float xscale = 1.f;   // applied to X operands as they are loaded
+  float gs = 1.f;       // normalisation g of the first step
+  if (g.first) {
+    const MatScalars s = g.sc[task.mat];
+    xscale = s.inv_fro;
+    gs = s.gscale;
+  }
+
+  Operand A, B;
+  int M, N, k_begin, k_end;
+  if (MODE == kGram) {
+    // C(i, j) = sum_k X[k][i] X[k][j], k over the K slice
+    const float* x = g.xin + mi.ws_off;
+    A = {x, sr, sc, m, n, !mi.trans, vec, xscale};
+    B = A;
+    M = n; N = n;
+    k_begin = task.ks * mi.kchunk;
+    k_end = min(m, k_begin + mi.kchunk);
+  } else if (MODE == kPoly) {
+    // C = A A (A symmetric, read as A[k][i])
+    const float* a = g.gram + mi.sq_off;
+    A = {a, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
+    B = A;
+    M = n; N = n;
+    k_begin = 0; k_end = n;
+  } else {
+    // C(i, j) = sum_k X[i][k] P[k][j]
+    const float* x = g.xin + mi.ws_off;
+    A = {x, sc, sr, n, m, mi.trans != 0, vec, xscale};
+    const float* p = g.poly + mi.sq_off;
+    B = {p, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
+    M = m; N = n;
+    k_begin = 0; k_end = n;
+  }
+  const int i0 = task.tm * kBM, j0 = task.tn * kBN;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  // k indices inside the operand are absolute (k_begin.. k_end); the bound is k_end.
+  A.K = k_end;
+  B.K = k_end;
+  SlabRegs ra, rb;
+  slab_load(A, k_begin, i0, ra);
+  slab_load(B, k_begin, j0, rb);
+  for (int k0 = k_begin; k0 < k_end; k0 += kBK) {
+    slab_store(A, ra, As);
+    slab_store(B, rb, Bs);
+    __syncthreads();
+    if (k0 + kBK < k_end) {
+      slab_load(A, k0 + kBK, i0, ra);
+      slab_load(B, k0 + kBK, j0, rb);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kBK; kk += 2) {
+      const int kr = kk + (lane >> 5);
+      const float a0 = As[kr][wm * 64 + (lane & 31)];
+      const float a1 = As[kr][wm * 64 + 32 + (lane & 31)];
+      const float b0 = Bs[kr][wn * 64 + (lane & 31)];
+      const float b1 = Bs[kr][wn * 64 + 32 + (lane & 31)];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue.  acc[a][b][r] holds C(i, j) with
+  //   i = i0 + wm*64 + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32.
+  const int jl = lane & 31;
+  const int ib = 4 * (lane >> 5);
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int j = j0 + wn * 64 + b * 32 + jl;
+      if (j >= N) continue;
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int ibase = i0 + wm * 64 + a * 32 + 8 * grp + ib;
+        if (MODE == kGram) {
+          float* out = (mi.ksplit > 1) ? g.gpart + mi.part_off + (int64_t)task.ks * n * n
+                                       : g.gram + mi.sq_off;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            if (i < M) out[(int64_t)i * n + j] = acc[a][b][4 * grp + r];
+          }
+        } else if (MODE == kPoly) {
+          // P = cb g^2 A + cc g^4 A^2  (g = 1 after the first step)
+          const float g2 = gs * gs;
+          const float beta = g.cb * g2, gamma = g.cc * g2 * g2;
+          const float* asrc = g.gram + mi.sq_off;
+          float* out = g.poly + mi.sq_off;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            if (i < M) {
+              const int64_t o = (int64_t)i * n + j;
+              out[o] = beta * asrc[o] + gamma * acc[a][b][4 * grp + r];
+            }
+          }
+        } else {
+          // X' = g (ca X + X P), X read with the same pre-scaling as the product
+          const float* xs = g.xin + mi.ws_off;
+          float* xo = g.xout + mi.ws_off;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            if (i < M) {
+              const int64_t o = (int64_t)i * sr + (int64_t)j * sc;
+              xo[o] = gs * (g.ca * (xscale * xs[o]) + acc[a][b][4 * grp + r]);
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+// Sum of the split-K Gram partials of one matrix, 4 elements per thread.
+__global__ void __launch_bounds__(256)
+gram_split_sum_kernel(const MatInfo* __restrict__ mats, int mat, const float* __restrict__ gpart,
+                      float* __restrict__ gram) {
+  const MatInfo mi = mats[mat];
+  const int64_t nn = (int64_t)mi.n * mi.n;
+  const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (e >= nn) return;
+  const float* p = gpart + mi.part_off;
+  float* out = gram + mi.sq_off;
+  if (e + 3 < nn && (nn & 3) == 0) {
+    floatx4 s = *reinterpret_cast<const floatx4*>(p + e);
+    for (int k = 1; k < mi.ksplit; ++k) s += *reinterpret_cast<const floatx4*>(p + k * nn + e);
+    *reinterpret_cast<floatx4*>(out + e) = s;
+  } else {
+    for (int q = 0; q < 4 && e + q < nn; ++q) {
+      float s = p[e + q];
+      for (int k = 1; k < mi.ksplit; ++k) s += p[k * nn + e + q];
+      out[e + q] = s;
+    }
+  }
+}
+
+// One workgroup per matrix.  mode 0: gscale = ||A||_F^(-1/2) (A = X0^T X0 of
+// the first step); mode 1: resid = ||A - I||_F / sqrt(n).
+__global__ void __launch_bounds__(256)
+gram_norm_kernel(const MatInfo* __restrict__ mats, const float* __restrict__ gram,
+                 MatScalars* __restrict__ sc, int mode, int steps) {
+  __shared__ double red[4];
+  const MatInfo mi = mats[blockIdx.x];
+  const int n = mi.n;
+  const int64_t nn = (int64_t)n * n;
+  const float* a = gram + mi.sq_off;
+  double s = 0.0;
+  for (int64_t e = threadIdx.x; e < nn; e += 256) {
+    double v = a[e];
+    if (mode == 1 && (e / n) == (e % n)) v -= 1.0;
+    s += v * v;
+  }
+  s = block_sum256(s, red);
+  if (threadIdx.x == 0) {
+    MatScalars& o = sc[blockIdx.x];
+    if (mode == 0) {
+      o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
+    } else {
+      o.resid = (float)sqrt(s / n);
+      if (!(o.resid <= 1e-3f) && o.flags == 0) o.flags |= 4;
+    }
+    o.steps = steps;
+  }
+}
+
+// <Q, Delta>_F partial per chunk of a corrected matrix.
+__global__ void __launch_bounds__(kStreamThreads)
+trace_kernel(const Chunk* __restrict__ chunks, const float* __restrict__ q,
+             const float* __restrict__ delta, double* __restrict__ part_tr) {
+  __shared__ double red[4];
+  const Chunk c = chunks[blockIdx.x];
+  double s = 0.0;
+  int done = 0;
+  if (c.vec) {
+    const int nv = c.count / 4;
+    for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
+      const floatx4 a = *reinterpret_cast<const floatx4*>(q + c.ws + 4 * v);
+      const floatx4 d = *reinterpret_cast<const floatx4*>(delta + c.ws + 4 * v);
+      s += (double)a[0] * d[0] + (double)a[1] * d[1] + (double)a[2] * d[2] + (double)a[3] * d[3];
+    }
+    done = nv * 4;
+  }
+  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads)
+    s += (double)q[c.ws + i] * delta[c.ws + i];
+  s = block_sum256(s, red);
+  if (threadIdx.x == 0) part_tr[blockIdx.x] = s;
+}
+
+__global__ void sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
+                             MatScalars* __restrict__ sc, int n_mat) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= n_mat) return;
+  const MatInfo mi = mats[m];
+  double s = 0.0;
+  for (int c = mi.chunk_begin; c < mi.chunk_end; ++c) s += part_tr[c];
+  MatScalars& o = sc[m];
+  if (o.flags & 1) o.sigma_bar = __builtin_nanf("");
+  else if (o.flags & 2) o.sigma_bar = 0.f;
+  else o.sigma_bar = (float)(s / mi.n);
+}
+
+// D = alpha sigma_bar Q;  B <- mu B + D;  theta <- theta - lr (D + mu B).
+__global__ void __launch_bounds__(kStreamThreads)
+finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
+              const float* __restrict__ q, float* __restrict__ theta, float* __restrict__ mom,
+              float alpha, float lr, float mu) {
+  const Chunk c = chunks[blockIdx.x];
+  const MatScalars s = sc[c.mat];
+  float f = alpha * s.sigma_bar;
+  if (s.flags & 2) f = 0.f;
+  int done = 0;
+  if (c.vec) {
+    const int nv = c.count / 4;
+    for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
+      const int64_t e = c.src + 4 * v;
+      const floatx4 qq = *reinterpret_cast<const floatx4*>(q + c.ws + 4 * v);
+      floatx4 b = *reinterpret_cast<const floatx4*>(mom + e);
+      floatx4 t = *reinterpret_cast<const floatx4*>(theta + e);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float d = f * qq[r];
+        const float bn = mu * b[r] + d;
+        b[r] = bn;
+        t[r] = t[r] - lr * (d + mu * bn);
+      }
+      *reinterpret_cast<floatx4*>(mom + e) = b;
+      *reinterpret_cast<floatx4*>(theta + e) = t;
+    }
+    done = nv * 4;
+  }
+  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
+    const int64_t e = c.src + i;
+    const float d = f * q[c.ws + i];
+    const float bn = mu * mom[e] + d;
+    mom[e] = bn;
+    theta[e] = theta[e] - lr * (d + mu * bn);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st) {
+  if (t.n_chunks == 0) return hipSuccess;
+  const float inv_k = 1.0f / (float)a.K;
+  if (a.worker_dtype == 0)
+    hipLaunchKernelGGL(reduce_kernel<0>, dim3(t.n_chunks), dim3(kStreamThreads), 0, st, t.chunks,
+                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu);
+  else
+    hipLaunchKernelGGL(reduce_kernel<1>, dim3(t.n_chunks), dim3(kStreamThreads), 0, st, t.chunks,
+                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu);
+  return hipGetLastError();
+}
+
+hipError_t launch_fro(const DevTables& t, hipStream_t st) {
+  if (t.n_mat == 0) return hipSuccess;
+  hipLaunchKernelGGL(fro_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_sq,
+                     t.scalars, t.n_mat);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st) {
+  GemmArgs g;
+  g.mats = t.mats;
+  g.sc = t.scalars;
+  g.xin = p.xin;
+  g.xout = p.xout;
+  g.gram = t.gram;
+  g.poly = t.poly;
+  g.gpart = t.gpart;
+  g.ca = p.ca;
+  g.cb = p.cb;
+  g.cc = p.cc;
+  g.first = p.first;
+  if (mode == kGram) {
+    if (t.n_gram_tasks == 0) return hipSuccess;
+    g.tasks = t.gram_tasks;
+    hipLaunchKernelGGL(gemm_kernel<kGram>, dim3(t.n_gram_tasks), dim3(kGemmThreads), 0, st, g);
+  } else if (mode == kPoly) {
+    if (t.n_poly_tasks == 0) return hipSuccess;
+    g.tasks = t.poly_tasks;
+    hipLaunchKernelGGL(gemm_kernel<kPoly>, dim3(t.n_poly_tasks), dim3(kGemmThreads), 0, st, g);
+  } else {
+    if (t.n_update_tasks == 0) return hipSuccess;
+    g.tasks = t.update_tasks;
+    hipLaunchKernelGGL(gemm_kernel<kUpdate>, dim3(t.n_update_tasks), dim3(kGemmThreads), 0, st, g);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_split_sums(const DevTables& t, hipStream_t st) {
+  for (int i = 0; i < t.n_split; ++i) {
+    const int mat = t.split_mats_host[i];
+    const int64_t nn = (int64_t)t.split_n_host[i] * t.split_n_host[i];
+    const int blocks = (int)((nn / 4 + 255) / 256 + 1);
+    hipLaunchKernelGGL(gram_split_sum_kernel, dim3(blocks), dim3(256), 0, st, t.mats, mat, t.gpart,
+                       t.gram);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gram_norm(const DevTables& t, int mode, int steps, hipStream_t st) {
+  if (t.n_mat == 0) return hipSuccess;
+  hipLaunchKernelGGL(gram_norm_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.gram, t.scalars, mode,
+                     steps);
+  return hipGetLastError();
+}
+
+hipError_t launch_trace(const DevTables& t, const float* q, hipStream_t st) {
+  if (t.n_iso_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, q,
+                     t.delta, t.part_tr);
+  hipLaunchKernelGGL(sigma_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_tr,
+                     t.scalars, t.n_mat);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish(const DevTables& t, const float* q, const StepArgs& a, hipStream_t st) {
+  if (t.n_iso_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks,
+                     t.scalars, q, a.theta, a.mom, a.alpha, a.lr, a.mu);
+  return hipGetLastError();
+}
+
+}  // namespace isoloco

@@ -1,0 +1,71 @@
+// Device-visible tables shared by the host planner and the HIP kernels.
+#pragma once
+#include <stdint.h>
+
+namespace isoloco {
+
+// Tile shape of the batched matrix-product kernels (output BM x BN, K slab BK).
+constexpr int kBM = 128;
+constexpr int kBN = 128;
+constexpr int kBK = 16;
+constexpr int kGemmThreads = 256;
+
+// Elements per workgroup of the streaming kernels (reduction, trace, write-back).
+constexpr int kChunk = 16384;
+constexpr int kStreamThreads = 256;
+
+constexpr int kMaxWorkers = 128;
+
+// One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
+// element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
+// where (sr, sc) = (n, 1) if the tensor is stored with rows >= cols, and
+// (1, m) if it is stored wide (rows < cols, kept in its own row-major layout).
+struct MatInfo {
+  int64_t ws_off;    // element offset in the Delta / X buffers (64-element aligned)
+  int64_t src_off;   // element offset in theta / momentum / workers
+  int64_t sq_off;    // element offset of this matrix's n x n buffers (Gram, polynomial)
+  int64_t part_off;  // element offset of the split-K Gram partials (ksplit * n * n)
+  int32_t m, n;      // tall shape
+  int32_t trans;     // 1 if stored wide (rows < cols)
+  int32_t ksplit;    // number of K slices of the Gram product (1 = no split)
+  int32_t kchunk;    // rows of X per K slice (multiple of kBK)
+  int32_t vec;       // 1 if m and n are multiples of 4 (vector loads allowed)
+  int32_t tensor;    // index in the caller's layout
+  int32_t chunk_begin, chunk_end;  // range of this matrix in the chunk table
+  int32_t pad0;
+};
+
+// A contiguous run of at most kChunk elements of one tensor.
+struct Chunk {
+  int64_t src;    // first element, index into theta / momentum / workers
+  int64_t ws;     // first element in the workspace buffers (-1 for AVG tensors)
+  int32_t count;  // elements
+  int32_t mat;    // matrix index, or -1 for AVG tensors
+  int32_t vec;    // 1 if src (and ws) allow 16-byte vector access of every stream
+  int32_t pad;
+};
+
+// Per-matrix scalars kept in the workspace.
+struct MatScalars {
+  float fro;        // ||Delta||_F
+  float inv_fro;    // 1 / ||Delta||_F (0 for a zero or non-finite matrix)
+  float gscale;     // ||X0^T X0||_F^(-1/2): maps sigma_max of X0 = Delta / ||Delta||_F to <= 1
+  float sigma_bar;  // <Q, Delta>_F / n
+  float resid;      // ||Q^T Q - I||_F / sqrt(n), or -1 if not computed
+  int32_t flags;    // ISOLOCO_FLAG_* bits
+  int32_t steps;
+  int32_t pad;
+};
+
+// Work item of a batched matrix product: one output tile of one matrix.
+struct Task {
+  int32_t mat;
+  int32_t tm, tn;  // tile row / column
+  int32_t ks;      // K slice (Gram only)
+};
+
+struct WorkerPtrs {
+  const void* p[kMaxWorkers];
+};
+
+}  // namespace isoloco

@@ -1,0 +1,154 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and exports
+every function that include/isoloco.h declares, the planner validates
+layouts and options, and the polynomial schedule it builds maps every
+singular value in [ell0, 1] to within tol of 1."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "isoloco.h")
+
+iso = pytest.importorskip("paper_2607_03011_amd")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:isoloco_status|const char\*)\s+(isoloco_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 9
+    lib = ctypes.CDLL(iso.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(iso.EXPORTED_SYMBOLS)
+
+
+def test_status_strings():
+    for s in range(0, -8, -1):
+        assert iso.isoloco_status_string(s) not in ("", "unknown status")
+    assert iso.isoloco_status_string(-99) == "unknown status"
+
+
+LAY = [(0, 128, 64, 0), (8192, 64, 1, 1)]
+
+
+@pytest.mark.parametrize("layout,n,K,dtype,err", [
+    (LAY, 8256, 0, 0, -1),
+    (LAY, 8256, 129, 0, -1),
+    (LAY, 8256, 4, 7, -1),
+    (LAY, -1, 4, 0, -1),
+    ([(0, 10, 10, 0), (99, 2, 1, 1)], 200, 4, 0, -2),     # overlap
+    ([(0, 10, 10, 0)], 99, 4, 0, -2),                     # past the end
+    ([(0, 0, 10, 0)], 100, 4, 0, -2),                     # empty rows
+    ([(0, 10, 10, 3)], 100, 4, 0, -2),                    # bad kind
+    ([(-5, 10, 10, 0)], 100, 4, 0, -2),                   # negative offset
+])
+def test_plan_rejects(layout, n, K, dtype, err):
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_plan(layout, n, K, dtype)
+    assert ei.value.status == err
+    assert iso.isoloco_last_error() != ""
+
+
+@pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
+                                  dict(tol=0.7), dict(check=3)])
+def test_plan_rejects_options(opts):
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_plan(LAY, 8256, 4, 0, opts)
+    assert ei.value.status == -1
+
+
+def test_reserved_field_must_be_zero():
+    arr = (iso.isoloco_tensor * 1)(iso.isoloco_tensor(0, 4, 4, 0, 1))
+    h = ctypes.c_void_p()
+    st = iso._lib.isoloco_plan(arr, 1, 16, 2, 0, None, ctypes.byref(h))
+    assert st == -2
+
+
+def test_empty_layout_and_workspace_errors():
+    h = iso.isoloco_plan([], 0, 1)
+    assert iso.isoloco_workspace_size(h) > 0
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_set_workspace(h, 0, 1 << 20)
+    assert ei.value.status == -5
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_set_workspace(h, 4096 + 16, 1 << 20)      # misaligned (checked before any HIP call)
+    assert ei.value.status == -5
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_aggregate(h, 0, [0], 0, 1.0, 0.7, 0.9)
+    assert ei.value.status == -5
+    iso.isoloco_plan_destroy(h)
+
+
+def test_workspace_too_small():
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    need = iso.isoloco_workspace_size(h)
+    with pytest.raises(iso.IsoLoCoError) as ei:
+        iso.isoloco_set_workspace(h, 1 << 20, need - 1)
+    assert ei.value.status == -5
+    iso.isoloco_plan_destroy(h)
+
+
+def test_stats_before_any_aggregate():
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    st = iso.isoloco_get_stats(h, 2)
+    assert st[0].steps == 0 and st[1].fro_norm == -1.0
+    with pytest.raises(iso.IsoLoCoError):
+        iso.isoloco_get_stats(h, 3)
+    iso.isoloco_plan_destroy(h)
+
+
+def _compose(sched, x):
+    for a, b, c in sched:
+        x = a * x + b * x ** 3 + c * x ** 5
+    return x
+
+
+@pytest.mark.parametrize("ell0,tol", [(1e-10, 1e-6), (1e-6, 1e-6), (1e-3, 1e-5), (0.3, 1e-7)])
+def test_schedule_converges_on_interval(ell0, tol):
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell0=ell0, tol=tol))
+    sched = iso.isoloco_schedule(h)
+    iso.isoloco_plan_destroy(h)
+    x = np.concatenate([np.geomspace(ell0, 1.0, 200001), np.linspace(ell0, 1.0, 200001)])
+    y = _compose(sched, x)
+    assert np.all(np.abs(y - 1.0) <= 1.01 * tol), (len(sched), np.abs(y - 1).max())
+    # every step is an odd polynomial that keeps small values positive and growing
+    for a, b, c in sched:
+        assert a > 1.0
+
+
+def test_schedule_tolerates_overshoot_and_shrinks_small_values_never():
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    sched = iso.isoloco_schedule(h)
+    iso.isoloco_plan_destroy(h)
+    # singular values 1% above the normalisation bound still converge
+    y = _compose(sched, np.linspace(1.0, 1.01, 101))
+    assert np.all(np.abs(y - 1) < 1e-4)
+    # values below ell0 are amplified, never mapped to <= 0
+    y = _compose(sched, np.geomspace(1e-14, 1e-10, 50))
+    assert np.all(y > 0)
+
+
+def test_schedule_length_default():
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    n = len(iso.isoloco_schedule(h))
+    iso.isoloco_plan_destroy(h)
+    assert 10 <= n <= 30
+
+
+def test_big_layout_plans_quickly():
+    from workload import CONFIGS
+    for k in (2, 3, 4):
+        c = CONFIGS[k]
+        h = iso.isoloco_plan(c.layout, c.n_elems, c.K, 0 if c.worker_dtype == "f32" else 1)
+        ws = iso.isoloco_workspace_size(h)
+        n2d = sum(r * cc for (_, r, cc, kind) in c.layout if kind == 0)
+        assert ws >= 3 * 4 * n2d
+        assert ws < 3 * 4 * n2d * 1.5 + (1 << 30)
+        iso.isoloco_plan_destroy(h)

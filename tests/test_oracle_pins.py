@@ -76,6 +76,36 @@ def test_jacobi_matches_lapack(shape):
     np.testing.assert_allclose(Vt @ Vt.T, np.eye(r), atol=1e-12)
 
 
+@pytest.mark.parametrize("shape", [(6, 6), (9, 4), (4, 9), (40, 31), (64, 64)])
+def test_compiled_and_numpy_jacobi_agree(shape, monkeypatch):
+    import oracle.jacobi as J
+    if J._clib is None:
+        pytest.skip("compiled Jacobi twin not built")
+    rng = np.random.default_rng(100 + shape[0])
+    M = rng.standard_normal(shape)
+    monkeypatch.setattr(J, "BACKEND", "numpy")
+    U1, s1, V1 = J.jacobi_svd(M)
+    monkeypatch.setattr(J, "BACKEND", "c")
+    U2, s2, V2 = J.jacobi_svd(M)
+    np.testing.assert_allclose(s1, s2, rtol=1e-13)
+    np.testing.assert_allclose(U1 @ V1, U2 @ V2, atol=1e-12)
+
+
+@pytest.mark.parametrize("backend", ["numpy", "c"])
+def test_jacobi_backends_match_lapack(backend, monkeypatch):
+    import oracle.jacobi as J
+    if backend == "c" and J._clib is None:
+        pytest.skip("compiled Jacobi twin not built")
+    monkeypatch.setattr(J, "BACKEND", backend)
+    rng = np.random.default_rng(77)
+    for shape in [(30, 30), (50, 20), (20, 50), (11, 11)]:
+        M = rng.standard_normal(shape) @ np.diag(np.geomspace(1, 1e-6, shape[1]))
+        U, s, Vt = J.jacobi_svd(M)
+        U2, s2, Vt2 = np.linalg.svd(M, full_matrices=False)
+        np.testing.assert_allclose(s, s2, rtol=1e-9)
+        np.testing.assert_allclose(U @ Vt, U2 @ Vt2, atol=1e-8)
+
+
 @pytest.mark.parametrize("kappa", [1e2, 1e4, 1e6])
 def test_polar_factor_matches_lapack_ill_conditioned(kappa):
     rng = np.random.default_rng(int(np.log10(kappa)))
