@@ -59,6 +59,11 @@ class isoloco_timing(ctypes.Structure):
                 ("launches", ctypes.c_int32)]
 
 
+# torch brings its own copy of the HIP runtime (same SONAME as ROCm's).  Load it
+# first so that libisoloco.so binds to that one runtime instead of loading a
+# second copy from /opt/rocm into the same process.
+import torch  # noqa: E402,F401
+
 if not os.path.exists(LIB_PATH):
     raise ImportError("libisoloco.so is not built: run `python -m paper_2607_03011_amd.build` "
                       "(or __graft_entry__.build()) first")
@@ -197,8 +202,8 @@ class IsoLoCoPlan:
         if isinstance(workers, torch.Tensor):
             if workers.dim() != 2 or workers.shape[0] != self.K or workers.shape[1] != self.n_elems:
                 raise ValueError("workers tensor must be [K, n_elems]")
-            if workers.dtype != wdt or not workers.is_contiguous():
-                raise ValueError("workers must be contiguous %s" % wdt)
+            if workers.dtype != wdt or workers.stride(1) != 1:
+                raise ValueError("workers must be %s with contiguous rows" % wdt)
             ptrs = [workers[k].data_ptr() for k in range(self.K)]
         else:
             ws = list(workers)

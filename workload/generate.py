@@ -62,11 +62,13 @@ class ReplicaGenerator:
 
     def workers(self, theta, step, out=None):
         """Replicas for outer step ``step`` around ``theta``: a [K, n_elems]
-        tensor of the worker dtype (written into ``out`` when given)."""
+        view of the worker dtype whose rows start 256-byte aligned (row stride
+        padded to a multiple of 128 elements); written into ``out`` when given."""
         cfg = self.cfg
         K = cfg.K
         if out is None:
-            out = torch.empty((K, cfg.n_elems), dtype=self.wdtype, device=self.device)
+            pad = (cfg.n_elems + 127) // 128 * 128
+            out = torch.empty((K, pad), dtype=self.wdtype, device=self.device)[:, :cfg.n_elems]
         # elements covered by no tensor: replicas equal theta
         out.copy_(theta.to(self.wdtype).unsqueeze(0).expand(K, -1))
         for ti, (off, rows, cols, kind) in enumerate(cfg.layout):
