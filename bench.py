@@ -19,21 +19,37 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
 PEAK_FP32_MFMA_TFS = 157.3   # MI355X dense fp32 matrix, TFLOP/s
+PEAK_BF16_MFMA_TFS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
 
 
-def gemm_flops_per_step(layout, n_steps, check):
-    """Algorithmic flops of the batched products of one outer step: per polar
-    step and m x n matrix (m >= n), Gram X^T X (2 m n^2), polynomial A A
-    (2 n^3) and update X P (2 m n^2); plus one Gram for the check."""
+# Part products per fp32 product for each precision mode: (first 4 steps, later steps)
+PARTS = {"mixed": (6, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
+X6_STEPS = 4
+
+
+def gemm_flops_per_step(layout, stats, check, precision):
+    """Algorithmic flops of the batched products of one outer step, returned as
+    (fp32-equivalent flops, MFMA flops actually issued).  Per polar step of an
+    m x n matrix (m >= n): the symmetric Gram X^T X (n (n+1) m: each of the
+    n (n+1)/2 distinct entries is a length-m dot product), the symmetric
+    polynomial A A (n (n+1) n) and the update X P (2 m n^2).  A matrix that took
+    s steps forms s + 1 Grams with the check (the last one measures Q^T Q), s
+    polynomials and s updates.  Split-bf16 products issue one MFMA product per
+    part product (3 or 6)."""
+    early, late = PARTS[precision]
     f = 0
-    for (_, r, c, kind) in layout:
+    fm = 0
+    for (_, r, c, kind), st in zip(layout, stats):
         if kind != 0:
             continue
         m, n = max(r, c), min(r, c)
-        f += n_steps * (4 * m * n * n + 2 * n ** 3)
-        if check:
-            f += 2 * m * n * n
-    return f
+        gram = n * (n + 1) * m
+        step = gram + n * (n + 1) * n + 2 * m * n * n
+        s = st.steps
+        e = min(s, X6_STEPS)
+        f += s * step + (gram if check else 0)
+        fm += e * step * early + (s - e) * step * late + (gram * late if check else 0)
+    return f, fm
 
 
 def reduce_bytes(layout, n_elems, K, wbytes):
@@ -101,6 +117,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--precision", choices=["mixed", "bf16x3", "bf16x6", "fp32"], default="mixed",
+                    help="arithmetic of the polar iteration's matrix products")
+    ap.add_argument("--ell-fast", type=float, default=0.0,
+                    help="short-schedule bound (0: library default; negative: one phase)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build measures one GPU; the IsoLoCo step here runs unsharded on a "
@@ -121,11 +141,15 @@ def main():
     wdt = iso.ISOLOCO_F32 if cfg.worker_dtype == "f32" else iso.ISOLOCO_BF16
     wbytes = 4 if cfg.worker_dtype == "f32" else 2
     theta0 = theta.clone()
-    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, device=dev)
-    n_polar = len(plan.schedule())
+    prec = {"mixed": iso.ISOLOCO_PREC_MIXED, "bf16x3": iso.ISOLOCO_PREC_BF16X3,
+            "bf16x6": iso.ISOLOCO_PREC_BF16X6, "fp32": iso.ISOLOCO_PREC_FP32}[args.precision]
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast),
+                           device=dev)
+    sched, n_short = plan.schedule_split()
+    n_polar = len(sched)
     stream = torch.cuda.current_stream(dev)
-    print("bench: workload %s, %d params, K=%d, %d polar steps, workspace %.2f GB" %
-          (cfg.name, cfg.n_params, cfg.K, n_polar, plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
+    print("bench: workload %s, %d params, K=%d, %d polar steps (%d in the short phase), workspace %.2f GB" %
+          (cfg.name, cfg.n_params, cfg.K, n_polar, n_short, plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
 
     for _ in range(args.warmup):
         plan.aggregate(theta, workers, mom, cfg.alpha, cfg.outer_lr, cfg.mu)
@@ -152,9 +176,14 @@ def main():
     st = plan.stats()
     resid = max(s.orth_resid for s, t in zip(st, cfg.layout) if t[3] == 0)
 
-    flops = gemm_flops_per_step(cfg.layout, n_polar, True)
+    flops, mfma_flops = gemm_flops_per_step(cfg.layout, st, True, args.precision)
+    steps_hist = {}
+    for sti, t in zip(st, cfg.layout):
+        if t[3] == 0:
+            steps_hist[sti.steps] = steps_hist.get(sti.steps, 0) + 1
     gemm_ms = per["gram_ms"] + per["poly_ms"] + per["update_ms"]
-    gemm_tfs = flops / (gemm_ms * 1e-3) / 1e12
+    peak = PEAK_FP32_MFMA_TFS if args.precision == "fp32" else PEAK_BF16_MFMA_TFS
+    gemm_tfs = mfma_flops / (gemm_ms * 1e-3) / 1e12
     rbytes = reduce_bytes(cfg.layout, cfg.n_elems, cfg.K, wbytes)
     red_gbs = rbytes / (per["reduce_ms"] * 1e-3) / 1e9
     fbytes = finish_bytes(cfg.layout)
@@ -171,15 +200,17 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32 (polar products: %s)" % args.precision,
         "data": "synthetic: seeded low-rank + Gaussian-noise pseudo-gradients, replicas resident in HBM",
         "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
                    "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
-                   "polar_steps": n_polar, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel (Gram, polynomial and update products)",
-                     "achieved": round(gemm_tfs, 3), "peak": PEAK_FP32_MFMA_TFS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tfs / PEAK_FP32_MFMA_TFS, 4), "traffic": None,
-                     "flops_per_step": flops, "ms_per_step": round(gemm_ms, 4),
+                   "polar_steps": n_polar, "short_phase_steps": n_short, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
+        "roofline": {"bound": "mfma", "kernel": "gemm_%s_kernel (Gram, polynomial and update products)" %
+                     ("f32" if args.precision == "fp32" else "bf16"), "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(gemm_tfs / peak, 4), "traffic": None,
+                     "mfma_flops_per_step": mfma_flops, "fp32_equivalent_flops_per_step": flops,
+                     "fp32_equivalent_tflops": round(flops / (gemm_ms * 1e-3) / 1e12, 3),
+                     "ms_per_step": round(gemm_ms, 4),
                      "launches_per_step": launches["gemm"] // args.steps},
         "roofline_reduce": {"bound": "hbm", "kernel": "reduce_kernel", "achieved": round(red_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(red_gbs / PEAK_HBM_GBS, 4),
@@ -189,6 +220,7 @@ def main():
                             "bytes_per_launch": fbytes, "ms": round(per["finish_ms"], 4)},
         "phases_ms": {k: round(v, 4) for k, v in per.items()},
         "max_orth_resid": resid,
+        "matrices_by_steps": {str(k): v for k, v in sorted(steps_hist.items())},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget)

@@ -86,14 +86,29 @@ typedef struct {
                         (default 1e-6)                                                           */
   int32_t check;     /* 1: after the last step also form Q^T Q to report the orthonormality
                         residual per matrix in isoloco_get_stats (default 1); -1: skip it        */
+  int32_t precision; /* arithmetic of the matrix products (ISOLOCO_PREC_*): split-bfloat16
+                        products split every fp32 operand into 2 (bf16x3: 3 bf16 MFMA
+                        products, about 2^-16 relative error) or 3 (bf16x6: 6 products,
+                        about fp32 accuracy) bfloat16 parts and accumulate in fp32.
+                        MIXED (default): bf16x6 for the first 4 steps, then bf16x3       */
+  float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
+                        whose Q^T Q is then the identity to 5e-5 stops there, the others run the
+                        continuation that reaches [ell0, 1] (default 1e-4; a negative value
+                        runs the single schedule for [ell0, 1])                                */
 } isoloco_options;
+
+#define ISOLOCO_PREC_MIXED 0
+#define ISOLOCO_PREC_FP32 1
+#define ISOLOCO_PREC_BF16X3 2
+#define ISOLOCO_PREC_BF16X6 3
 
 /* Per-tensor results of the last isoloco_aggregate() on a plan. */
 typedef struct {
   float sigma_bar;  /* mean singular value of Delta_l (ISO tensors; 0 for AVG)            */
   float fro_norm;   /* ||Delta_l||_F                                                        */
   float orth_resid; /* ||Q^T Q - I||_F / sqrt(r) on the short side (ISO, if checked; else -1) */
-  int32_t steps;    /* polar iteration steps taken (ISO tensors)                             */
+  int32_t steps;    /* polar iteration steps taken (ISO tensors): the short schedule's length
+                       if the matrix stopped there, else the full length                     */
   int32_t flags;    /* bit 0: Delta_l had a non-finite value; bit 1: Delta_l == 0;
                        bit 2: residual above 1e-3 (not converged)                            */
   int32_t reserved;
@@ -140,9 +155,10 @@ isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out,
 
 /* The polynomial schedule of the plan: for step k, p_k(x) = c[3k] x + c[3k+1] x^3 + c[3k+2] x^5
  * (on singular values normalised by ||Delta^T Delta||_F^(1/2)).  Writes at most
- * max_steps triples; *n_steps receives the schedule length.  Host only. */
+ * max_steps triples; *n_steps receives the schedule length and *n_short (if not
+ * NULL) the length of the short first phase (= *n_steps for one phase).  Host only. */
 isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps,
-                                int32_t* n_steps);
+                                int32_t* n_steps, int32_t* n_short);
 
 /* Per-kernel timing of the last aggregate, measured with HIP events recorded
  * on the aggregate's stream around every launch (enable first; the events

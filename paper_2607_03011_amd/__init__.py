@@ -24,6 +24,10 @@ ISOLOCO_F32 = 0
 ISOLOCO_BF16 = 1
 ISOLOCO_KIND_ISO = 0
 ISOLOCO_KIND_AVG = 1
+ISOLOCO_PREC_MIXED = 0
+ISOLOCO_PREC_FP32 = 1
+ISOLOCO_PREC_BF16X3 = 2
+ISOLOCO_PREC_BF16X6 = 3
 ISOLOCO_FLAG_NONFINITE = 1
 ISOLOCO_FLAG_ZERO = 2
 ISOLOCO_FLAG_NOT_CONVERGED = 4
@@ -42,7 +46,7 @@ class isoloco_tensor(ctypes.Structure):
 
 class isoloco_options(ctypes.Structure):
     _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
-                ("check", ctypes.c_int32)]
+                ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):
@@ -80,7 +84,7 @@ _sig = {
                                          ctypes.c_float, ctypes.c_float, _P]),
     "isoloco_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_tensor_stats), ctypes.c_int32]),
     "isoloco_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
-                                        ctypes.POINTER(ctypes.c_int32)]),
+                                        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "isoloco_plan_destroy": (ctypes.c_int, [_P]),
     "isoloco_enable_timing": (ctypes.c_int, [_P, ctypes.c_int32]),
     "isoloco_get_timing": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_timing)]),
@@ -151,11 +155,15 @@ def isoloco_get_stats(plan, n_tensors):
     return [arr[i] for i in range(n_tensors)]
 
 
-def isoloco_schedule(plan, max_steps=256):
+def isoloco_schedule(plan, max_steps=256, with_split=False):
+    """List of (a, b, c) per step; with_split=True also returns the length of
+    the short first phase."""
     buf = (ctypes.c_double * (3 * max_steps))()
     n = ctypes.c_int32()
-    _check(_lib.isoloco_schedule(plan, buf, max_steps, ctypes.byref(n)), "isoloco_schedule")
-    return [tuple(buf[3 * k: 3 * k + 3]) for k in range(min(n.value, max_steps))]
+    ns = ctypes.c_int32()
+    _check(_lib.isoloco_schedule(plan, buf, max_steps, ctypes.byref(n), ctypes.byref(ns)), "isoloco_schedule")
+    sched = [tuple(buf[3 * k: 3 * k + 3]) for k in range(min(n.value, max_steps))]
+    return (sched, ns.value) if with_split else sched
 
 
 def isoloco_enable_timing(plan, enable=True):
@@ -229,6 +237,9 @@ class IsoLoCoPlan:
 
     def schedule(self):
         return isoloco_schedule(self.handle)
+
+    def schedule_split(self):
+        return isoloco_schedule(self.handle, with_split=True)
 
     def close(self):
         if self.handle is not None:

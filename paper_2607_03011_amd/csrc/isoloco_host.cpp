@@ -59,6 +59,23 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // directly for intervals narrower than 1e-3.
 
 constexpr double kCushion = 0.1;
+// ||X^T X - I||_F / sqrt(n) below which a matrix stops after the short schedule
+// (about 5x the rounding floor of the split-bf16 Gram; the polar factor is then
+// within about half this value of the exact one)
+constexpr float kSwitchTol = 5e-5f;
+// In the mixed precision mode the first kX6Steps steps (where small singular
+// values are still far below 1 and rounding errors in their directions are
+// amplified the most) use bf16x6 products, the later ones bf16x3.
+constexpr int kX6Steps = 4;
+
+int step_arith(int precision, int k) {
+  switch (precision) {
+    case ISOLOCO_PREC_FP32: return kArithFp32;
+    case ISOLOCO_PREC_BF16X3: return kArithBf16x3;
+    case ISOLOCO_PREC_BF16X6: return kArithBf16x6;
+    default: return k < kX6Steps ? kArithBf16x6 : kArithBf16x3;
+  }
+}
 constexpr double kSafety = 1.02;
 
 bool solve4(double M[4][5], double out[4]) {
@@ -204,11 +221,13 @@ struct isoloco_plan_s {
   int n_iso_chunks = 0;
   std::vector<Task> gram_tasks, poly_tasks, update_tasks;
   std::vector<int> split_mats, split_n;
-  std::vector<double> sched;
+  std::vector<double> sched;  // short schedule followed by its continuation
+  int n_short = 0;            // steps of the short schedule
   int64_t n2d = 0;   // elements of one Delta / X buffer
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
+  size_t off_pnorm = 0;
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_poly = 0, off_gpart = 0, total = 0;
   char* ws = nullptr;
@@ -306,16 +325,17 @@ void plan_matrices(isoloco_plan_s* p) {
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int T = (M.n + kBM - 1) / kBM;
+    // the Gram matrix is symmetric: tiles on and above the diagonal only
     for (int ks = 0; ks < M.ksplit; ++ks)
       for (int a = 0; a < T; ++a)
-        for (int b = 0; b < T; ++b) p->gram_tasks.push_back(Task{mi, a, b, ks});
+        for (int b = a; b < T; ++b) p->gram_tasks.push_back(Task{mi, a, b, ks});
   }
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int T = (M.n + kBM - 1) / kBM;
     for (int a = 0; a < T; ++a)
-      for (int b = 0; b < T; ++b) p->poly_tasks.push_back(Task{mi, a, b, 0});
+      for (int b = a; b < T; ++b) p->poly_tasks.push_back(Task{mi, a, b, 0});
   }
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
@@ -345,6 +365,7 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_sc = take(p->mats.size() * sizeof(MatScalars));
   p->off_psq = take(p->chunks.size() * sizeof(double));
   p->off_ptr = take(p->chunks.size() * sizeof(double));
+  p->off_pnorm = take(p->mats.size() * kNormSlices * sizeof(double));
   p->off_delta = take((size_t)p->n2d * sizeof(float));
   p->off_x0 = take((size_t)p->n2d * sizeof(float));
   p->off_x1 = take((size_t)p->n2d * sizeof(float));
@@ -365,6 +386,7 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.scalars = reinterpret_cast<MatScalars*>(w + p->off_sc);
   t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
+  t.part_norm = reinterpret_cast<double*>(w + p->off_pnorm);
   t.delta = reinterpret_cast<float*>(w + p->off_delta);
   t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
   t.x[1] = reinterpret_cast<float*>(w + p->off_x1);
@@ -411,11 +433,16 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.ell0 == 0.f) o.ell0 = 1e-10f;
   if (o.tol == 0.f) o.tol = 1e-6f;
   if (o.check == 0) o.check = 1;
+  if (o.ell_fast == 0.f) o.ell_fast = 1e-4f;
   if (o.max_steps < 1 || o.max_steps > 200)
     return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
   if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
   if (!(o.tol > 0.f && o.tol < 0.5f)) return fail(ISOLOCO_ERR_INVALID_ARG, "tol must be in (0, 0.5)");
+  if (!(o.ell_fast < 1.f) || std::isnan(o.ell_fast))
+    return fail(ISOLOCO_ERR_INVALID_ARG, "ell_fast must be < 1 (negative: one phase)");
   if (o.check != 1 && o.check != -1) return fail(ISOLOCO_ERR_INVALID_ARG, "check must be 1 or -1");
+  if (o.precision < ISOLOCO_PREC_MIXED || o.precision > ISOLOCO_PREC_BF16X6)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown precision %d", o.precision);
 
   std::vector<std::pair<int64_t, int64_t>> spans;
   for (int32_t i = 0; i < n_tensors; ++i) {
@@ -446,7 +473,22 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     p->dtype = worker_dtype;
     p->opts = o;
     plan_matrices(p);
-    p->sched = build_schedule(o.ell0, o.tol, o.max_steps);
+    // Two phases: a short schedule that assumes sigma_min >= ell_fast, after
+    // which every matrix whose Q^T Q is already the identity stops; the others
+    // continue with the schedule for what the short one made of [ell0, 1].
+    if (o.ell_fast > o.ell0) {
+      p->sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
+      p->n_short = (int)p->sched.size() / 3;
+      double lb = o.ell0;
+      for (int k = 0; k < p->n_short; ++k) lb = peval(&p->sched[3 * k], lb);
+      if (p->n_short < o.max_steps && lb < 1.0 - o.tol) {
+        const std::vector<double> rest = build_schedule(lb, o.tol, o.max_steps - p->n_short);
+        p->sched.insert(p->sched.end(), rest.begin(), rest.end());
+      }
+    } else {
+      p->sched = build_schedule(o.ell0, o.tol, o.max_steps);
+      p->n_short = (int)p->sched.size() / 3;
+    }
     plan_workspace(p);
   } catch (...) {
     delete p;
@@ -555,9 +597,29 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   e = timed(kPhReduce, [&] { return launch_reduce(t, a, st); });
   if (e != hipSuccess) return hip_fail(e, "reduce launch");
   if (t.n_mat > 0) {
-    if ((e = timed(kPhOther, [&] { return launch_fro(t, st); })) != hipSuccess)
-      return hip_fail(e, "fro launch");
     const int S = (int)plan->sched.size() / 3;
+    const int Sa = plan->n_short;
+    const bool two = Sa < S;
+    const int buf_short = (Sa - 1) & 1, buf_total = (S - 1) & 1;
+    if ((e = timed(kPhOther, [&] { return launch_fro(t, S, buf_total, st); })) != hipSuccess)
+      return hip_fail(e, "fro launch");
+    NormArgs na{};
+    na.steps_short = Sa;
+    na.steps_total = S;
+    na.buf_short = buf_short;
+    na.buf_total = buf_total;
+    na.tol_switch = kSwitchTol;
+    auto gram = [&](const PolarStep& ps) -> hipError_t {
+      hipError_t r = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); });
+      if (r == hipSuccess && t.n_split)
+        r = timed(kPhOther, [&] { return launch_split_sums(t, ps.only_active, st); });
+      return r;
+    };
+    auto norm = [&](int mode, int only_active) -> hipError_t {
+      na.mode = mode;
+      na.only_active = only_active;
+      return timed(kPhOther, [&] { return launch_gram_norm(t, na, st); });
+    };
     const float* xin = t.delta;
     for (int k = 0; k < S; ++k) {
       PolarStep ps{};
@@ -567,24 +629,33 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       ps.cb = (float)plan->sched[3 * k + 1];
       ps.cc = (float)plan->sched[3 * k + 2];
       ps.first = (k == 0);
-      if ((e = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); })) != hipSuccess ||
-          (t.n_split && (e = timed(kPhOther, [&] { return launch_split_sums(t, st); })) != hipSuccess) ||
-          (k == 0 && (e = timed(kPhOther, [&] { return launch_gram_norm(t, 0, S, st); })) != hipSuccess) ||
-          (e = timed(kPhPoly, [&] { return launch_gemm(t, 1, ps, st); })) != hipSuccess ||
+      ps.only_active = (k >= Sa);
+      ps.arith = step_arith(plan->opts.precision, k);
+      // the first Gram of the second phase was formed by the switch check
+      if (!(two && k == Sa) && (e = gram(ps)) != hipSuccess) return hip_fail(e, "Gram launch");
+      if (k == 0 && (e = norm(kNormFirst, 0)) != hipSuccess) return hip_fail(e, "norm launch");
+      if ((e = timed(kPhPoly, [&] { return launch_gemm(t, 1, ps, st); })) != hipSuccess ||
           (e = timed(kPhUpdate, [&] { return launch_gemm(t, 2, ps, st); })) != hipSuccess)
         return hip_fail(e, "polar step launch");
       xin = ps.xout;
+      if (two && k == Sa - 1) {
+        PolarStep pc{};
+        pc.xin = xin;
+        pc.arith = step_arith(plan->opts.precision, k + 1);
+        if ((e = gram(pc)) != hipSuccess || (e = norm(kNormSwitch, 0)) != hipSuccess)
+          return hip_fail(e, "switch check launch");
+      }
     }
     if (plan->opts.check == 1) {
-      PolarStep ps{};
-      ps.xin = xin;
-      if ((e = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); })) != hipSuccess ||
-          (t.n_split && (e = timed(kPhOther, [&] { return launch_split_sums(t, st); })) != hipSuccess) ||
-          (e = timed(kPhOther, [&] { return launch_gram_norm(t, 1, S, st); })) != hipSuccess)
+      PolarStep pc{};
+      pc.xin = xin;
+      pc.only_active = two ? 1 : 0;
+      pc.arith = step_arith(plan->opts.precision, S);
+      if ((e = gram(pc)) != hipSuccess || (e = norm(kNormFinal, pc.only_active)) != hipSuccess)
         return hip_fail(e, "check launch");
     }
-    if ((e = timed(kPhOther, [&] { return launch_trace(t, xin, st); })) != hipSuccess ||
-        (e = timed(kPhFinish, [&] { return launch_finish(t, xin, a, st); })) != hipSuccess)
+    if ((e = timed(kPhOther, [&] { return launch_trace(t, st); })) != hipSuccess ||
+        (e = timed(kPhFinish, [&] { return launch_finish(t, a, st); })) != hipSuccess)
       return hip_fail(e, "finish launch");
   }
   plan->last_stream = st;
@@ -623,10 +694,12 @@ isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out,
   return ISOLOCO_OK;
 }
 
-isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps, int32_t* n_steps) {
+isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps, int32_t* n_steps,
+                                int32_t* n_short) {
   if (!plan || !n_steps) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
   const int S = (int)plan->sched.size() / 3;
   *n_steps = S;
+  if (n_short) *n_short = plan->n_short;
   if (coeffs)
     for (int i = 0; i < 3 * std::min<int>(S, std::max(max_steps, 0)); ++i) coeffs[i] = plan->sched[i];
   return ISOLOCO_OK;

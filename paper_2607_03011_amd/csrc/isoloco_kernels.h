@@ -17,6 +17,7 @@ struct DevTables {
   MatScalars* scalars;
   double* part_sq;
   double* part_tr;
+  double* part_norm;  // n_mat x kNormSlices partials of the Gram norms
   float* delta;
   float* x[2];
   float* gram;
@@ -38,21 +39,42 @@ struct StepArgs {
   float alpha, lr, mu;
 };
 
+// Arithmetic of one batched-product launch.
+enum Arith { kArithBf16x3 = 0, kArithBf16x6 = 1, kArithFp32 = 2 };
+
 struct PolarStep {
   const float* xin;
   float* xout;
   float ca, cb, cc;
   int first;
+  int only_active;  // 1: skip matrices whose scalars say active == 0
+  int arith;        // Arith
+};
+
+// Gram-norm modes
+enum NormMode {
+  kNormFirst = 0,   // gscale = ||A||_F^(-1/2) of the first step
+  kNormFinal = 1,   // final check: resid and the not-converged flag
+  kNormSwitch = 2,  // end of the short schedule: resid; converged matrices stop
+};
+
+struct NormArgs {
+  int mode;
+  int only_active;
+  int steps_short, steps_total;  // schedule lengths
+  int buf_short, buf_total;      // X buffer holding the result after each phase
+  float tol_switch;              // residual below which a matrix stops after the short schedule
 };
 
 hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
-hipError_t launch_fro(const DevTables& t, hipStream_t st);
+// also initialises the per-matrix iteration state (active, qbuf, steps)
+hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStream_t st);
 // mode: 0 Gram, 1 polynomial, 2 update
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st);
-hipError_t launch_split_sums(const DevTables& t, hipStream_t st);
-// mode 0: normalisation of the first step; mode 1: orthonormality residual
-hipError_t launch_gram_norm(const DevTables& t, int mode, int steps, hipStream_t st);
-hipError_t launch_trace(const DevTables& t, const float* q, hipStream_t st);
-hipError_t launch_finish(const DevTables& t, const float* q, const StepArgs& a, hipStream_t st);
+hipError_t launch_split_sums(const DevTables& t, int only_active, hipStream_t st);
+hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st);
+// the polar factor of matrix m is in t.x[scalars[m].qbuf]
+hipError_t launch_trace(const DevTables& t, hipStream_t st);
+hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st);
 
 }  // namespace isoloco

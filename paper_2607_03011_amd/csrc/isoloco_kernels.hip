@@ -5,7 +5,7 @@
 //                 for the 2-D tensors, and the whole Nesterov step (Algorithm 2)
 //                 for tensors that are not corrected.
 //   fro           per-matrix Frobenius norm from the partials (pre-scaling).
-//   gemm          batched, grouped fp32 MFMA products for the polar iteration:
+//   gemm          batched, grouped MFMA products (split-bf16 or fp32) for the polar iteration:
 //                 Gram A = X^T X, polynomial P = b A + c A^2, update X <- a X + X P.
 //   gram_norm     ||A||_F (first step: normalisation) or ||A - I||_F (check).
 //   trace/sigma   sigma_bar = <Q, Delta>_F / r (mean singular value, Algorithm 2).
@@ -172,14 +172,22 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
   }
 }
 
-// ||Delta||_F per matrix, from the chunk partials in chunk order.
-__global__ void fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
-                           MatScalars* __restrict__ sc, int n_mat) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= n_mat) return;
-  const MatInfo mi = mats[m];
+// Sum of a matrix's chunk partials by one wavefront: lane l adds partials
+// l, l + 64, ... in order, then a fixed butterfly (deterministic).
+__device__ __forceinline__ double wave_sum_range(const double* part, int begin, int end) {
   double s = 0.0;
-  for (int c = mi.chunk_begin; c < mi.chunk_end; ++c) s += part_sq[c];
+  for (int c = begin + (int)(threadIdx.x & 63); c < end; c += 64) s += part[c];
+  return wave_sum(s);
+}
+
+// ||Delta||_F per matrix (one wavefront per matrix).
+__global__ void __launch_bounds__(64)
+fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
+           MatScalars* __restrict__ sc, int n_mat, int steps_total, int buf_total) {
+  const int m = blockIdx.x;
+  const MatInfo mi = mats[m];
+  const double s = wave_sum_range(part_sq, mi.chunk_begin, mi.chunk_end);
+  if (threadIdx.x != 0) return;
   MatScalars o;
   o.fro = (float)sqrt(s);
   o.flags = 0;
@@ -189,8 +197,9 @@ __global__ void fro_kernel(const MatInfo* __restrict__ mats, const double* __res
   o.gscale = 0.f;
   o.sigma_bar = 0.f;
   o.resid = -1.f;
-  o.steps = 0;
-  o.pad = 0;
+  o.steps = steps_total;
+  o.active = 1;
+  o.qbuf = buf_total;
   sc[m] = o;
 }
 
@@ -288,55 +297,152 @@ struct GemmArgs {
   float* gpart;       // split-K Gram partials
   float ca, cb, cc;   // step coefficients p(x) = ca x + cb x^3 + cc x^5
   int first;          // 1 on the first step (inputs pre-scaled by 1/||Delta||_F, g applied)
+  int only_active;    // 1: tasks of matrices that stopped iterating return at once
+};
+
+// Operands, output bounds and K range of one task.
+//   Gram:    C(i, j) = sum_k X[k][i] X[k][j]   over the task's K slice (C is n x n)
+//   Poly:    C(i, j) = sum_k A[k][i] A[k][j]   (A symmetric, so this is A A)
+//   Update:  C(i, j) = sum_k X[i][k] P[k][j]   (C is m x n, tall coordinates)
+struct GemmSetup {
+  MatInfo mi;
+  Operand A, B;
+  int M, N, k_begin, k_end, i0, j0;
+  int64_t sr, sc;
+  float xscale;  // applied to X operands as they are loaded (1/||Delta||_F on the first step)
+  float gs;      // normalisation g of the first step (1 afterwards)
 };
 
 template <int MODE>
-__global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& task) {
+  GemmSetup s;
+  s.mi = g.mats[task.mat];
+  const MatInfo& mi = s.mi;
+  const int m = mi.m, n = mi.n;
+  s.sr = mi.trans ? 1 : n;
+  s.sc = mi.trans ? m : 1;
+  const bool vec = mi.vec != 0;
+  s.xscale = 1.f;
+  s.gs = 1.f;
+  if (g.first) {
+    const MatScalars q = g.sc[task.mat];
+    s.xscale = q.inv_fro;
+    s.gs = q.gscale;
+  }
+  if (MODE == kGram) {
+    const float* x = g.xin + mi.ws_off;
+    s.k_begin = task.ks * mi.kchunk;
+    s.k_end = min(m, s.k_begin + mi.kchunk);
+    s.A = {x, s.sr, s.sc, s.k_end, n, !mi.trans, vec, s.xscale};
+    s.B = s.A;
+    s.M = n;
+    s.N = n;
+  } else if (MODE == kPoly) {
+    const float* a = g.gram + mi.sq_off;
+    s.A = {a, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
+    s.B = s.A;
+    s.M = n;
+    s.N = n;
+    s.k_begin = 0;
+    s.k_end = n;
+  } else {
+    const float* x = g.xin + mi.ws_off;
+    s.A = {x, s.sc, s.sr, n, m, mi.trans != 0, vec, s.xscale};
+    const float* p = g.poly + mi.sq_off;
+    s.B = {p, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
+    s.M = m;
+    s.N = n;
+    s.k_begin = 0;
+    s.k_end = n;
+  }
+  s.i0 = task.tm * kBM;
+  s.j0 = task.tn * kBN;
+  return s;
+}
+
+// Epilogue.  acc[a][b][r] holds C(i, j) with
+//   i = i0 + wm*64 + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32
+// (the 32 x 32 accumulator layout of the fp32 and bf16 MFMA instructions).
+template <int MODE>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
+                                              const floatx16 (&acc)[2][2]) {
+  const MatInfo& mi = s.mi;
+  const int n = mi.n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int jl = lane & 31;
+  const int ib = 4 * (lane >> 5);
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int j = s.j0 + wn * 64 + b * 32 + jl;
+      if (j >= s.N) continue;
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int ibase = s.i0 + wm * 64 + a * 32 + 8 * grp + ib;
+        if (MODE == kGram || MODE == kPoly) {
+          // symmetric n x n result: only tiles with tm <= tn are computed, and an
+          // off-diagonal tile also writes its mirror image C(j, i) = C(i, j)
+          float* out;
+          floatx4 v;
+          if (MODE == kGram) {
+            out = (mi.ksplit > 1) ? g.gpart + mi.part_off + (int64_t)task.ks * n * n : g.gram + mi.sq_off;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = acc[a][b][4 * grp + r];
+          } else {
+            // P = cb g^2 A + cc g^4 A^2  (g = 1 after the first step)
+            const float g2 = s.gs * s.gs;
+            const float beta = g.cb * g2, gamma = g.cc * g2 * g2;
+            const float* asrc = g.gram + mi.sq_off;
+            out = g.poly + mi.sq_off;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int i = min(ibase + r, s.M - 1);
+              v[r] = beta * asrc[(int64_t)i * n + j] + gamma * acc[a][b][4 * grp + r];
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            if (i < s.M) out[(int64_t)i * n + j] = v[r];
+          }
+          if (task.tm != task.tn) {
+            float* mo = out + (int64_t)j * n + ibase;
+            if ((n & 3) == 0 && ibase + 3 < s.M) {
+              *reinterpret_cast<floatx4*>(mo) = v;
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (ibase + r < s.M) mo[r] = v[r];
+            }
+          }
+        } else {
+          // X' = g (ca X + X P), X read with the same pre-scaling as the product
+          const float* xs = g.xin + mi.ws_off;
+          float* xo = g.xout + mi.ws_off;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            if (i < s.M) {
+              const int64_t o = (int64_t)i * s.sr + (int64_t)j * s.sc;
+              xo[o] = s.gs * (g.ca * (s.xscale * xs[o]) + acc[a][b][4 * grp + r]);
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+// fp32 MFMA main loop (v_mfma_f32_32x32x2f32), K staged in slabs of 16.
+template <int MODE>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
   __shared__ float As[kBK][kLdsW];
   __shared__ float Bs[kBK][kLdsW];
-
   const Task task = g.tasks[blockIdx.x];
-  const MatInfo mi = g.mats[task.mat];
-  const int m = mi.m, n = mi.n;
-  const int64_t sr = mi.trans ? 1 : n;
-  const int64_t sc = mi.trans ? m : 1;
-  const bool vec = mi.vec != 0;
-  float xscale = 1.f;   // applied to X operands as they are loaded
-  float gs = 1.f;       // normalisation g of the first step
-  if (g.first) {
-    const MatScalars s = g.sc[task.mat];
-    xscale = s.inv_fro;
-    gs = s.gscale;
-  }
-
-  Operand A, B;
-  int M, N, k_begin, k_end;
-  if (MODE == kGram) {
-    // C(i, j) = sum_k X[k][i] X[k][j], k over the K slice
-    const float* x = g.xin + mi.ws_off;
-    A = {x, sr, sc, m, n, !mi.trans, vec, xscale};
-    B = A;
-    M = n; N = n;
-    k_begin = task.ks * mi.kchunk;
-    k_end = min(m, k_begin + mi.kchunk);
-  } else if (MODE == kPoly) {
-    // C = A A (A symmetric, read as A[k][i])
-    const float* a = g.gram + mi.sq_off;
-    A = {a, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
-    B = A;
-    M = n; N = n;
-    k_begin = 0; k_end = n;
-  } else {
-    // C(i, j) = sum_k X[i][k] P[k][j]
-    const float* x = g.xin + mi.ws_off;
-    A = {x, sc, sr, n, m, mi.trans != 0, vec, xscale};
-    const float* p = g.poly + mi.sq_off;
-    B = {p, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
-    M = m; N = n;
-    k_begin = 0; k_end = n;
-  }
-  const int i0 = task.tm * kBM, j0 = task.tn * kBN;
-
+  if (g.only_active && !g.sc[task.mat].active) return;
+  const GemmSetup s = gemm_setup<MODE>(g, task);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   floatx16 acc[2][2];
@@ -347,19 +453,16 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  // k indices inside the operand are absolute (k_begin.. k_end); the bound is k_end.
-  A.K = k_end;
-  B.K = k_end;
   SlabRegs ra, rb;
-  slab_load(A, k_begin, i0, ra);
-  slab_load(B, k_begin, j0, rb);
-  for (int k0 = k_begin; k0 < k_end; k0 += kBK) {
-    slab_store(A, ra, As);
-    slab_store(B, rb, Bs);
+  slab_load(s.A, s.k_begin, s.i0, ra);
+  slab_load(s.B, s.k_begin, s.j0, rb);
+  for (int k0 = s.k_begin; k0 < s.k_end; k0 += kBK) {
+    slab_store(s.A, ra, As);
+    slab_store(s.B, rb, Bs);
     __syncthreads();
-    if (k0 + kBK < k_end) {
-      slab_load(A, k0 + kBK, i0, ra);
-      slab_load(B, k0 + kBK, j0, rb);
+    if (k0 + kBK < s.k_end) {
+      slab_load(s.A, k0 + kBK, s.i0, ra);
+      slab_load(s.B, k0 + kBK, s.j0, rb);
     }
 #pragma unroll
     for (int kk = 0; kk < kBK; kk += 2) {
@@ -375,64 +478,163 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs g) {
     }
     __syncthreads();
   }
+  gemm_epilogue<MODE>(g, s, task, acc);
+}
 
-  // Epilogue.  acc[a][b][r] holds C(i, j) with
-  //   i = i0 + wm*64 + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32.
-  const int jl = lane & 31;
-  const int ib = 4 * (lane >> 5);
+// ---------------------------------------------------------------------------
+// Split-bfloat16 main loop (bf16x3 and bf16x6)
+// ---------------------------------------------------------------------------
+//
+// Each fp32 operand x is split into NS bfloat16 parts, x = x0 + x1 (+ x2) + r,
+// x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1), round to nearest
+// even, so |r| <= 2^-16 |x| for NS = 2 and 2^-24 |x| for NS = 3.  The product
+// sum_k a_k b_k is accumulated in fp32 over the part products whose order
+// (a_i b_j with i + j < NS) is kept:
+//   NS = 2 (bf16x3):  a1 b0 + a0 b1 + a0 b0
+//   NS = 3 (bf16x6):  a2 b0 + a1 b1 + a0 b2 + a1 b0 + a0 b1 + a0 b0
+// on v_mfma_f32_32x32x16_bf16.  K is staged in slabs of 32: fp32 global loads
+// into registers (next slab in flight during the current slab's products),
+// split, and stored to LDS as NS bf16 planes per operand in [row][k] order, so
+// that every lane reads its 8 consecutive k values of a row with one 16-byte
+// LDS read.
+
+constexpr int kBK2 = 32;
+constexpr int kLdsK = kBK2 + 8;  // padded row (bf16 elements): 80 bytes
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+struct Slab32 {
+  floatx4 v[4];
+};
+
+// 128 (i) x 32 (k) fp32 slab into registers: thread t owns row i = t % 128
+// and the 16 consecutive k values 16 (t / 128) .. +15, so that its LDS writes
+// are 16-byte row segments and consecutive lanes write consecutive rows
+// (80-byte stride: no bank conflicts).
+__device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, Slab32& r) {
+  const int t = threadIdx.x;
+  const int i = i0 + (t & 127);
+  const int kb = k0 + 16 * (t >> 7);
+  if (op.icontig) {
+    // lanes take consecutive i: every 4-byte load is coalesced across the wave
 #pragma unroll
-  for (int a = 0; a < 2; ++a) {
+    for (int q = 0; q < 4; ++q) {
+      floatx4 x = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int j = j0 + wn * 64 + b * 32 + jl;
-      if (j >= N) continue;
+      for (int e = 0; e < 4; ++e) {
+        const int k = kb + 4 * q + e;
+        if (i < op.I && k < op.K) x[e] = op.base[(int64_t)k * op.s_k + i];
+      }
+      r.v[q] = x * op.scale;
+    }
+  } else {
+    // each lane reads 64 contiguous bytes of its row
+    const float* p = op.base + (int64_t)i * op.s_i + kb;
 #pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const int ibase = i0 + wm * 64 + a * 32 + 8 * grp + ib;
-        if (MODE == kGram) {
-          float* out = (mi.ksplit > 1) ? g.gpart + mi.part_off + (int64_t)task.ks * n * n
-                                       : g.gram + mi.sq_off;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int i = ibase + r;
-            if (i < M) out[(int64_t)i * n + j] = acc[a][b][4 * grp + r];
-          }
-        } else if (MODE == kPoly) {
-          // P = cb g^2 A + cc g^4 A^2  (g = 1 after the first step)
-          const float g2 = gs * gs;
-          const float beta = g.cb * g2, gamma = g.cc * g2 * g2;
-          const float* asrc = g.gram + mi.sq_off;
-          float* out = g.poly + mi.sq_off;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int i = ibase + r;
-            if (i < M) {
-              const int64_t o = (int64_t)i * n + j;
-              out[o] = beta * asrc[o] + gamma * acc[a][b][4 * grp + r];
-            }
-          }
+    for (int q = 0; q < 4; ++q) {
+      floatx4 x = {0.f, 0.f, 0.f, 0.f};
+      if (i < op.I) {
+        if (op.vec && kb + 4 * q + 3 < op.K) {
+          x = *reinterpret_cast<const floatx4*>(p + 4 * q);
         } else {
-          // X' = g (ca X + X P), X read with the same pre-scaling as the product
-          const float* xs = g.xin + mi.ws_off;
-          float* xo = g.xout + mi.ws_off;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int i = ibase + r;
-            if (i < M) {
-              const int64_t o = (int64_t)i * sr + (int64_t)j * sc;
-              xo[o] = gs * (g.ca * (xscale * xs[o]) + acc[a][b][4 * grp + r]);
-            }
-          }
+          for (int e = 0; e < 4; ++e)
+            if (kb + 4 * q + e < op.K) x[e] = p[4 * q + e];
         }
       }
+      r.v[q] = x * op.scale;
     }
   }
 }
 
+template <int NS>
+__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[kBM][kLdsK]) {
+  const int t = threadIdx.x;
+  const int i = t & 127, kb = 16 * (t >> 7);
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    bf16x8 part[NS];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x = r.v[2 * half + e / 4][e % 4];
+#pragma unroll
+      for (int p = 0; p < NS; ++p) {
+        const __bf16 h = (__bf16)x;
+        part[p][e] = h;
+        x -= (float)h;
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x8*>(&planes[p][i][kb + 8 * half]) = part[p];
+  }
+}
+
+template <int MODE, int NS>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NS][kBM][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NS][kBN][kLdsK];
+  const Task task = g.tasks[blockIdx.x];
+  if (g.only_active && !g.sc[task.mat].active) return;
+  const GemmSetup s = gemm_setup<MODE>(g, task);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  Slab32 ra, rb;
+  slab32_load(s.A, s.k_begin, s.i0, ra);
+  slab32_load(s.B, s.k_begin, s.j0, rb);
+  for (int k0 = s.k_begin; k0 < s.k_end; k0 += kBK2) {
+    __syncthreads();
+    slab32_store<NS>(ra, Ap);
+    slab32_store<NS>(rb, Bp);
+    __syncthreads();
+    if (k0 + kBK2 < s.k_end) {
+      slab32_load(s.A, k0 + kBK2, s.i0, ra);
+      slab32_load(s.B, k0 + kBK2, s.j0, rb);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kBK2; kk += 16) {
+      const int kc = kk + 8 * (lane >> 5);
+      bf16x8 av[2][NS], bv[2][NS];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        const int row = wm * 64 + a * 32 + (lane & 31);
+#pragma unroll
+        for (int p = 0; p < NS; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
+      }
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int row = wn * 64 + b * 32 + (lane & 31);
+#pragma unroll
+        for (int p = 0; p < NS; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          // part products of order NS - 1 down to 0 (smallest first)
+#pragma unroll
+          for (int ord = NS - 1; ord >= 0; --ord)
+#pragma unroll
+            for (int pa = ord; pa >= 0; --pa)
+              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
+        }
+    }
+  }
+  gemm_epilogue<MODE>(g, s, task, acc);
+}
+
 // Sum of the split-K Gram partials of one matrix, 4 elements per thread.
 __global__ void __launch_bounds__(256)
-gram_split_sum_kernel(const MatInfo* __restrict__ mats, int mat, const float* __restrict__ gpart,
-                      float* __restrict__ gram) {
+gram_split_sum_kernel(const MatInfo* __restrict__ mats, const MatScalars* __restrict__ sc, int mat,
+                      int only_active, const float* __restrict__ gpart, float* __restrict__ gram) {
+  if (only_active && !sc[mat].active) return;
   const MatInfo mi = mats[mat];
   const int64_t nn = (int64_t)mi.n * mi.n;
   const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
@@ -452,41 +654,60 @@ gram_split_sum_kernel(const MatInfo* __restrict__ mats, int mat, const float* __
   }
 }
 
-// One workgroup per matrix.  mode 0: gscale = ||A||_F^(-1/2) (A = X0^T X0 of
-// the first step); mode 1: resid = ||A - I||_F / sqrt(n).
+// Partial sums of squares over an n x n buffer: block (x, m) takes rows
+// x, x + kNormSlices, ... of matrix m.  mode 0: sum A^2; mode 1: sum (A - I)^2.
+
 __global__ void __launch_bounds__(256)
-gram_norm_kernel(const MatInfo* __restrict__ mats, const float* __restrict__ gram,
-                 MatScalars* __restrict__ sc, int mode, int steps) {
+gram_norm_partial_kernel(const MatInfo* __restrict__ mats, const MatScalars* __restrict__ sc,
+                         const float* __restrict__ gram, double* __restrict__ part, int mode, int only_active) {
   __shared__ double red[4];
-  const MatInfo mi = mats[blockIdx.x];
+  if (only_active && !sc[blockIdx.y].active) return;
+  const MatInfo mi = mats[blockIdx.y];
   const int n = mi.n;
-  const int64_t nn = (int64_t)n * n;
   const float* a = gram + mi.sq_off;
   double s = 0.0;
-  for (int64_t e = threadIdx.x; e < nn; e += 256) {
-    double v = a[e];
-    if (mode == 1 && (e / n) == (e % n)) v -= 1.0;
-    s += v * v;
-  }
-  s = block_sum256(s, red);
-  if (threadIdx.x == 0) {
-    MatScalars& o = sc[blockIdx.x];
-    if (mode == 0) {
-      o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
-    } else {
-      o.resid = (float)sqrt(s / n);
-      if (!(o.resid <= 1e-3f) && o.flags == 0) o.flags |= 4;
+  for (int r = blockIdx.x; r < n; r += kNormSlices)
+    for (int c = threadIdx.x; c < n; c += 256) {
+      double v = a[(int64_t)r * n + c];
+      if (mode != kNormFirst && r == c) v -= 1.0;
+      s += v * v;
     }
-    o.steps = steps;
+  s = block_sum256(s, red);
+  if (threadIdx.x == 0) part[(int64_t)blockIdx.y * kNormSlices + blockIdx.x] = s;
+}
+
+// Per-matrix decisions from the norm partials (see NormMode).
+__global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part,
+                                       MatScalars* __restrict__ sc, int n_mat, NormArgs a) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= n_mat) return;
+  MatScalars& o = sc[m];
+  if (a.only_active && !o.active) return;
+  double s = 0.0;
+  for (int x = 0; x < kNormSlices; ++x) s += part[(int64_t)m * kNormSlices + x];
+  if (a.mode == kNormFirst) {
+    o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
+    return;
+  }
+  o.resid = (float)sqrt(s / mats[m].n);
+  if (a.mode == kNormSwitch) {
+    // stop after the short schedule when every singular value is already at 1
+    const bool go_on = o.flags == 0 && !(o.resid <= a.tol_switch);
+    o.active = go_on ? 1 : 0;
+    o.steps = go_on ? a.steps_total : a.steps_short;
+    o.qbuf = go_on ? a.buf_total : a.buf_short;
+  } else if (!(o.resid <= 1e-3f) && o.flags == 0) {
+    o.flags |= 4;
   }
 }
 
 // <Q, Delta>_F partial per chunk of a corrected matrix.
 __global__ void __launch_bounds__(kStreamThreads)
-trace_kernel(const Chunk* __restrict__ chunks, const float* __restrict__ q,
-             const float* __restrict__ delta, double* __restrict__ part_tr) {
+trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
+             const float* __restrict__ x1, const float* __restrict__ delta, double* __restrict__ part_tr) {
   __shared__ double red[4];
   const Chunk c = chunks[blockIdx.x];
+  const float* q = sc[c.mat].qbuf ? x1 : x0;
   double s = 0.0;
   int done = 0;
   if (c.vec) {
@@ -504,13 +725,13 @@ trace_kernel(const Chunk* __restrict__ chunks, const float* __restrict__ q,
   if (threadIdx.x == 0) part_tr[blockIdx.x] = s;
 }
 
-__global__ void sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
-                             MatScalars* __restrict__ sc, int n_mat) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= n_mat) return;
+__global__ void __launch_bounds__(64)
+sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
+             MatScalars* __restrict__ sc, int n_mat) {
+  const int m = blockIdx.x;
   const MatInfo mi = mats[m];
-  double s = 0.0;
-  for (int c = mi.chunk_begin; c < mi.chunk_end; ++c) s += part_tr[c];
+  const double s = wave_sum_range(part_tr, mi.chunk_begin, mi.chunk_end);
+  if (threadIdx.x != 0) return;
   MatScalars& o = sc[m];
   if (o.flags & 1) o.sigma_bar = __builtin_nanf("");
   else if (o.flags & 2) o.sigma_bar = 0.f;
@@ -520,10 +741,11 @@ __global__ void sigma_kernel(const MatInfo* __restrict__ mats, const double* __r
 // D = alpha sigma_bar Q;  B <- mu B + D;  theta <- theta - lr (D + mu B).
 __global__ void __launch_bounds__(kStreamThreads)
 finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
-              const float* __restrict__ q, float* __restrict__ theta, float* __restrict__ mom,
-              float alpha, float lr, float mu) {
+              const float* __restrict__ x0, const float* __restrict__ x1, float* __restrict__ theta,
+              float* __restrict__ mom, float alpha, float lr, float mu) {
   const Chunk c = chunks[blockIdx.x];
   const MatScalars s = sc[c.mat];
+  const float* q = s.qbuf ? x1 : x0;
   float f = alpha * s.sigma_bar;
   if (s.flags & 2) f = 0.f;
   int done = 0;
@@ -571,10 +793,10 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st) 
   return hipGetLastError();
 }
 
-hipError_t launch_fro(const DevTables& t, hipStream_t st) {
+hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
-  hipLaunchKernelGGL(fro_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_sq,
-                     t.scalars, t.n_mat);
+  hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat,
+                     steps_total, buf_total);
   return hipGetLastError();
 }
 
@@ -591,53 +813,60 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.cb = p.cb;
   g.cc = p.cc;
   g.first = p.first;
-  if (mode == kGram) {
-    if (t.n_gram_tasks == 0) return hipSuccess;
-    g.tasks = t.gram_tasks;
-    hipLaunchKernelGGL(gemm_kernel<kGram>, dim3(t.n_gram_tasks), dim3(kGemmThreads), 0, st, g);
-  } else if (mode == kPoly) {
-    if (t.n_poly_tasks == 0) return hipSuccess;
-    g.tasks = t.poly_tasks;
-    hipLaunchKernelGGL(gemm_kernel<kPoly>, dim3(t.n_poly_tasks), dim3(kGemmThreads), 0, st, g);
+  g.only_active = p.only_active;
+  const Task* tasks = mode == kGram ? t.gram_tasks : mode == kPoly ? t.poly_tasks : t.update_tasks;
+  const int n = mode == kGram ? t.n_gram_tasks : mode == kPoly ? t.n_poly_tasks : t.n_update_tasks;
+  if (n == 0) return hipSuccess;
+  g.tasks = tasks;
+  const dim3 grid(n), block(kGemmThreads);
+  if (p.arith == kArithFp32) {
+    if (mode == kGram) hipLaunchKernelGGL(gemm_f32_kernel<kGram>, grid, block, 0, st, g);
+    else if (mode == kPoly) hipLaunchKernelGGL(gemm_f32_kernel<kPoly>, grid, block, 0, st, g);
+    else hipLaunchKernelGGL(gemm_f32_kernel<kUpdate>, grid, block, 0, st, g);
+  } else if (p.arith == kArithBf16x6) {
+    if (mode == kGram) hipLaunchKernelGGL((gemm_bf16_kernel<kGram, 3>), grid, block, 0, st, g);
+    else if (mode == kPoly) hipLaunchKernelGGL((gemm_bf16_kernel<kPoly, 3>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((gemm_bf16_kernel<kUpdate, 3>), grid, block, 0, st, g);
   } else {
-    if (t.n_update_tasks == 0) return hipSuccess;
-    g.tasks = t.update_tasks;
-    hipLaunchKernelGGL(gemm_kernel<kUpdate>, dim3(t.n_update_tasks), dim3(kGemmThreads), 0, st, g);
+    if (mode == kGram) hipLaunchKernelGGL((gemm_bf16_kernel<kGram, 2>), grid, block, 0, st, g);
+    else if (mode == kPoly) hipLaunchKernelGGL((gemm_bf16_kernel<kPoly, 2>), grid, block, 0, st, g);
+    else hipLaunchKernelGGL((gemm_bf16_kernel<kUpdate, 2>), grid, block, 0, st, g);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_split_sums(const DevTables& t, hipStream_t st) {
+hipError_t launch_split_sums(const DevTables& t, int only_active, hipStream_t st) {
   for (int i = 0; i < t.n_split; ++i) {
     const int mat = t.split_mats_host[i];
     const int64_t nn = (int64_t)t.split_n_host[i] * t.split_n_host[i];
     const int blocks = (int)((nn / 4 + 255) / 256 + 1);
-    hipLaunchKernelGGL(gram_split_sum_kernel, dim3(blocks), dim3(256), 0, st, t.mats, mat, t.gpart,
-                       t.gram);
+    hipLaunchKernelGGL(gram_split_sum_kernel, dim3(blocks), dim3(256), 0, st, t.mats, t.scalars, mat, only_active,
+                       t.gpart, t.gram);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gram_norm(const DevTables& t, int mode, int steps, hipStream_t st) {
+hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
-  hipLaunchKernelGGL(gram_norm_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.gram, t.scalars, mode,
-                     steps);
+  hipLaunchKernelGGL(gram_norm_partial_kernel, dim3(kNormSlices, t.n_mat), dim3(256), 0, st, t.mats, t.scalars,
+                     t.gram, t.part_norm, a.mode, a.only_active);
+  hipLaunchKernelGGL(gram_norm_final_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_norm,
+                     t.scalars, t.n_mat, a);
   return hipGetLastError();
 }
 
-hipError_t launch_trace(const DevTables& t, const float* q, hipStream_t st) {
+hipError_t launch_trace(const DevTables& t, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, q,
-                     t.delta, t.part_tr);
-  hipLaunchKernelGGL(sigma_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_tr,
-                     t.scalars, t.n_mat);
+  hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+                     t.x[0], t.x[1], t.delta, t.part_tr);
+  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat);
   return hipGetLastError();
 }
 
-hipError_t launch_finish(const DevTables& t, const float* q, const StepArgs& a, hipStream_t st) {
+hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks,
-                     t.scalars, q, a.theta, a.mom, a.alpha, a.lr, a.mu);
+  hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu);
   return hipGetLastError();
 }
 

@@ -53,9 +53,13 @@ struct MatScalars {
   float sigma_bar;  // <Q, Delta>_F / n
   float resid;      // ||Q^T Q - I||_F / sqrt(n), or -1 if not computed
   int32_t flags;    // ISOLOCO_FLAG_* bits
-  int32_t steps;
-  int32_t pad;
+  int32_t steps;    // polar steps this matrix has taken
+  int32_t active;   // 1 while the matrix still iterates (second phase of the schedule)
+  int32_t qbuf;     // which X buffer holds the final polar factor
 };
+
+// Partial sums per matrix for the Gram norms (rows r, r + kNormSlices, ...).
+constexpr int kNormSlices = 32;
 
 // Work item of a batched matrix product: one output tile of one matrix.
 struct Task {

@@ -43,9 +43,11 @@ def _oracle_one(args):
     return th, b, sb
 
 
-def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, processes=None):
+def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, processes=1):
     """Oracle outer step evaluated tensor by tensor (the tensors of the step are
-    independent), optionally on a subset, in parallel processes.
+    independent), optionally on a subset.  Runs in this process by default (the
+    compiled Jacobi loop is itself multi-threaded; processes > 1 forks, which is
+    only for callers that have not touched the GPU).
     Returns {tensor index: (theta_new, B_new, sigma_bar)}."""
     idx = list(range(len(layout))) if select is None else list(select)
     jobs = []

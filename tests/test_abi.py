@@ -57,7 +57,8 @@ def test_plan_rejects(layout, n, K, dtype, err):
 
 
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
-                                  dict(tol=0.7), dict(check=3)])
+                                  dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
+                                  dict(ell_fast=float("nan"))])
 def test_plan_rejects_options(opts):
     with pytest.raises(iso.IsoLoCoError) as ei:
         iso.isoloco_plan(LAY, 8256, 4, 0, opts)
@@ -121,6 +122,30 @@ def test_schedule_converges_on_interval(ell0, tol):
     # every step is an odd polynomial that keeps small values positive and growing
     for a, b, c in sched:
         assert a > 1.0
+
+
+@pytest.mark.parametrize("ell_fast", [1e-4, 1e-2])
+def test_two_phase_schedule(ell_fast):
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell_fast=ell_fast))
+    sched, ns = iso.isoloco_schedule(h, with_split=True)
+    iso.isoloco_plan_destroy(h)
+    assert 0 < ns < len(sched)
+    # the short phase alone converges on [ell_fast, 1] ...
+    x = np.geomspace(ell_fast, 1.0, 100001)
+    assert np.abs(_compose(sched[:ns], x) - 1).max() <= 1e-6
+    # ... and the whole schedule on [ell0, 1]
+    x = np.geomspace(1e-10, 1.0, 100001)
+    assert np.abs(_compose(sched, x) - 1).max() <= 1e-6
+    # a value already converged by the short phase stays converged
+    y = _compose(sched[:ns], np.linspace(0.5, 1.0, 1001))
+    assert np.abs(_compose(sched[ns:], y) - 1).max() <= 1e-6
+
+
+def test_one_phase_when_ell_fast_negative():
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell_fast=-1.0))
+    sched, ns = iso.isoloco_schedule(h, with_split=True)
+    iso.isoloco_plan_destroy(h)
+    assert ns == len(sched)
 
 
 def test_schedule_tolerates_overshoot_and_shrinks_small_values_never():

@@ -84,10 +84,11 @@ RAGGED = [(300, 200, KIND_ISO), (129, 1, KIND_AVG), (200, 300, KIND_ISO), (520, 
           (37, 5, KIND_ISO), (1, 7, KIND_ISO), (64, 64, KIND_ISO), (33, 1, KIND_AVG), (2, 2, KIND_ISO)]
 
 
-def test_ragged_multi_tile_f32(iso):
+@pytest.mark.parametrize("precision", [0, 1, 2, 3], ids=["mixed", "fp32", "bf16x3", "bf16x6"])
+def test_ragged_multi_tile_f32(iso, precision):
     from workload import custom_layout
     lay, n = custom_layout(RAGGED, align=4)
-    _run_and_compare(iso, _cfg(lay, n, K=3))
+    _run_and_compare(iso, _cfg(lay, n, K=3), opts=dict(precision=precision))
 
 
 def test_ragged_multi_tile_bf16(iso):
@@ -210,6 +211,111 @@ def test_alpha_zero_and_linearity(iso):
     plan.close()
 
 
-def test_config0_full(iso):
+@pytest.mark.parametrize("precision", [0, 1], ids=["mixed", "fp32"])
+def test_config0_full(iso, precision):
     from workload import CONFIGS
-    _run_and_compare(iso, CONFIGS[0])
+    _run_and_compare(iso, CONFIGS[0], opts=dict(precision=precision))
+
+
+def test_config1_full_block(iso):
+    """One d = 768 decoder block, K = 8, every tensor against the oracle."""
+    from workload import CONFIGS
+    _run_and_compare(iso, CONFIGS[1], select=None)
+
+
+def test_config2_full_size_sampled(iso):
+    """The 109.5M-parameter workload at full size in the benchmark's launch
+    configuration: every 1-D tensor and one tensor of each 2-D shape (q of
+    block 0, gate of block 0, down of block 0, the tied embedding) against
+    the oracle, and for all 85 matrices the polar factor recovered from the
+    momentum must be orthonormal with sigma_bar = <Q, Delta> / r."""
+    from workload import CONFIGS, ReplicaGenerator
+    cfg = CONFIGS[2]
+    lay = cfg.layout
+    sample = [i for i, t in enumerate(lay) if t[3] == KIND_AVG]
+    for shape in [(768, 768), (2048, 768), (768, 2048), (32000, 768)]:
+        sample.append(next(i for i, t in enumerate(lay) if (t[1], t[2]) == shape))
+    theta, mom, st = _run_and_compare(iso, cfg, select=sample)
+    # properties of every corrected matrix, computed from the outputs in fp32 on the GPU
+    dev = theta.device
+    gen = ReplicaGenerator(cfg, seed=0, device=dev)
+    th0, _ = gen.init_state()
+    workers = gen.workers(th0, 1)
+    for i, (off, rows, cols, kind) in enumerate(lay):
+        if kind != KIND_ISO:
+            continue
+        n_el = rows * cols
+        Q = (mom[off:off + n_el].reshape(rows, cols) / st[i].sigma_bar).double()
+        G = Q.T @ Q if rows >= cols else Q @ Q.T
+        r = min(rows, cols)
+        orth = (torch.linalg.norm(G - torch.eye(r, dtype=G.dtype, device=dev)) / r ** 0.5).item()
+        delta = (th0[off:off + n_el].double() - workers[:, off:off + n_el].double()).mean(0).reshape(rows, cols)
+        sb = ((Q * delta).sum() / r).item()
+        assert orth <= TOL, (i, orth)
+        assert abs(sb - st[i].sigma_bar) <= TOL * st[i].sigma_bar, (i, sb, st[i].sigma_bar)
+        assert st[i].flags == 0 and 0 <= st[i].orth_resid <= TOL
+
+
+def _planted(rows, cols, smin, rng):
+    """rows x cols matrix with singular values spaced geometrically in [smin, 1]."""
+    r = min(rows, cols)
+    U, _ = np.linalg.qr(rng.standard_normal((rows, r)))
+    V, _ = np.linalg.qr(rng.standard_normal((cols, r)))
+    return (U * np.geomspace(1.0, smin, r)) @ V.T
+
+
+def test_two_phase_stops_well_conditioned_matrices_early(iso):
+    """With the workload's pseudo-gradients (low rank + noise), a tall matrix
+    (sigma_min / ||Delta^T Delta||_F^(1/2) around 1e-2) stops after the short
+    schedule while a square one (sigma_min around 1e-6 of that) runs the
+    continuation; both match the oracle."""
+    from workload import custom_layout
+    lay, n = custom_layout([(256, 256, KIND_ISO), (192, 64, KIND_ISO), (64, 1, KIND_AVG)], align=4)
+    cfg = _cfg(lay, n, K=4)
+    dev = torch.device("cuda", 0)
+    plan = iso.IsoLoCoPlan(lay, n, 4, iso.ISOLOCO_F32, device=dev)
+    sched, n_short = plan.schedule_split()
+    _, _, st = _run_and_compare(iso, cfg, seed=4, plan=plan)
+    print("steps", [s.steps for s in st[:2]], "of", n_short, len(sched), flush=True)
+    assert st[0].steps == len(sched)
+    assert st[1].steps == n_short
+    plan.close()
+
+
+@pytest.mark.parametrize("precision", [0, 1, 3], ids=["mixed", "fp32", "bf16x6"])
+def test_wide_geometric_spectrum(iso, precision):
+    """Spectra with many singular values far below the largest one need the
+    precise products in the first steps: a 128 x 128 matrix with singular
+    values spaced geometrically over [1e-5, 1] (and a 96 x 48 one over
+    [1e-2, 1]), one step through the C ABI, against the oracle."""
+    from workload import custom_layout
+    lay, n = custom_layout([(128, 128, KIND_ISO), (96, 48, KIND_ISO)], align=4)
+    rng = np.random.default_rng(11)
+    delta = np.zeros(n)
+    for (off, rows, cols, kind), smin in zip(lay, (1e-5, 1e-2)):
+        delta[off:off + rows * cols] = (_planted(rows, cols, smin, rng) * 1e-2).reshape(-1)
+    dev = torch.device("cuda", 0)
+    theta = torch.zeros(n, dtype=torch.float32, device=dev)
+    mom = torch.zeros_like(theta)
+    w = torch.tensor(-delta, dtype=torch.float32, device=dev).reshape(1, n).contiguous()
+    plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, opts=dict(precision=precision), device=dev)
+    plan.aggregate(theta, w, mom, 1.0, 0.7, 0.9)
+    torch.cuda.synchronize()
+    st = plan.stats()
+    ref = oracle_per_tensor(lay, np.zeros(n, np.float32), [w.cpu().numpy()[0]], np.zeros(n, np.float32),
+                            1.0, 0.7, 0.9)
+    th = theta.cpu().numpy()
+    for i, (th_r, b_r, sb_r) in ref.items():
+        off, rows, cols, kind = lay[i]
+        sl = slice(off, off + rows * cols)
+        e = relF(th[sl], th_r)
+        print("tensor %d steps %d: theta %.2e" % (i, st[i].steps, e), flush=True)
+        assert e <= TOL
+    plan.close()
+
+
+@pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
+def test_single_phase_schedule(iso, precision):
+    from workload import custom_layout
+    lay, n = custom_layout(RAGGED, align=4)
+    _run_and_compare(iso, _cfg(lay, n, K=3), seed=9, opts=dict(ell_fast=-1.0, precision=precision))
