@@ -22,9 +22,9 @@ PEAK_FP32_MFMA_TFS = 157.3   # MI355X dense fp32 matrix, TFLOP/s
 PEAK_BF16_MFMA_TFS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
 
 
-# Part products per fp32 product for each precision mode: (first 4 steps, later steps)
+# Part products per fp32 product for each precision mode: (first 3 steps, later steps)
 PARTS = {"mixed": (6, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
-X6_STEPS = 4
+X6_STEPS = 3
 
 
 def gemm_flops_per_step(layout, stats, check, precision):
@@ -119,6 +119,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--precision", choices=["mixed", "bf16x3", "bf16x6", "fp32"], default="mixed",
                     help="arithmetic of the polar iteration's matrix products")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (reference for HBM counters)")
     ap.add_argument("--ell-fast", type=float, default=0.0,
                     help="short-schedule bound (0: library default; negative: one phase)")
     args = ap.parse_args()
@@ -151,6 +153,14 @@ def main():
     print("bench: workload %s, %d params, K=%d, %d polar steps (%d in the short phase), workspace %.2f GB" %
           (cfg.name, cfg.n_params, cfg.K, n_polar, n_short, plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
 
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         plan.aggregate(theta, workers, mom, cfg.alpha, cfg.outer_lr, cfg.mu)
     torch.cuda.synchronize()

@@ -90,7 +90,7 @@ typedef struct {
                         products split every fp32 operand into 2 (bf16x3: 3 bf16 MFMA
                         products, about 2^-16 relative error) or 3 (bf16x6: 6 products,
                         about fp32 accuracy) bfloat16 parts and accumulate in fp32.
-                        MIXED (default): bf16x6 for the first 4 steps, then bf16x3       */
+                        MIXED (default): bf16x6 for the first 3 steps, then bf16x3       */
   float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
                         whose Q^T Q is then the identity to 5e-5 stops there, the others run the
                         continuation that reaches [ell0, 1] (default 1e-4; a negative value

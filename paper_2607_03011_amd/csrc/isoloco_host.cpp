@@ -66,7 +66,7 @@ constexpr float kSwitchTol = 5e-5f;
 // In the mixed precision mode the first kX6Steps steps (where small singular
 // values are still far below 1 and rounding errors in their directions are
 // amplified the most) use bf16x6 products, the later ones bf16x3.
-constexpr int kX6Steps = 4;
+constexpr int kX6Steps = 3;
 
 int step_arith(int precision, int k) {
   switch (precision) {
@@ -209,6 +209,12 @@ std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
 // Plan
 // ---------------------------------------------------------------------------
 
+struct TaskListHost {
+  std::vector<Task> tasks;
+  int seg_off[3] = {0, 0, 0};
+  int seg_cnt[3] = {0, 0, 0};
+};
+
 struct isoloco_plan_s {
   std::vector<isoloco_tensor> layout;
   int64_t n_elems = 0;
@@ -219,7 +225,7 @@ struct isoloco_plan_s {
   std::vector<MatInfo> mats;
   std::vector<Chunk> chunks;
   int n_iso_chunks = 0;
-  std::vector<Task> gram_tasks, poly_tasks, update_tasks;
+  TaskListHost gram_list, poly_list, update_list;
   std::vector<int> split_mats, split_n;
   std::vector<double> sched;  // short schedule followed by its continuation
   int n_short = 0;            // steps of the short schedule
@@ -270,7 +276,7 @@ void plan_matrices(isoloco_plan_s* p) {
       ks = std::max(ks, 1);
     }
     int64_t kchunk = (mi.m + ks - 1) / ks;
-    kchunk = (kchunk + kBK - 1) / kBK * kBK;
+    kchunk = (kchunk + 31) / 32 * 32;  // whole K slabs of both product kernels
     ks = (int)((mi.m + kchunk - 1) / kchunk);
     mi.ksplit = ks;
     mi.kchunk = (int32_t)kchunk;
@@ -316,7 +322,21 @@ void plan_matrices(isoloco_plan_s* p) {
   p->nsq = sq;
   p->npart = part;
 
-  // Work lists, longest tasks first.
+  // Work lists, longest tasks first, each in three segments (interior tiles of
+  // row-major matrices, interior tiles of wide-stored matrices, ragged tiles).
+  std::vector<Task> seg[3];
+  auto flush = [&](TaskListHost& L) {
+    L.tasks.clear();
+    for (int q = 0; q < 3; ++q) {
+      L.seg_off[q] = (int)L.tasks.size();
+      L.seg_cnt[q] = (int)seg[q].size();
+      L.tasks.insert(L.tasks.end(), seg[q].begin(), seg[q].end());
+      seg[q].clear();
+    }
+  };
+  auto put = [&](const MatInfo& M, bool interior, const Task& tk) {
+    seg[!(interior && M.vec) ? 2 : (M.trans ? 1 : 0)].push_back(tk);
+  };
   std::vector<int> order(p->mats.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
@@ -326,23 +346,30 @@ void plan_matrices(isoloco_plan_s* p) {
     const MatInfo& M = p->mats[mi];
     const int T = (M.n + kBM - 1) / kBM;
     // the Gram matrix is symmetric: tiles on and above the diagonal only
-    for (int ks = 0; ks < M.ksplit; ++ks)
+    for (int ks = 0; ks < M.ksplit; ++ks) {
+      const int64_t kb = (int64_t)ks * M.kchunk, ke = std::min<int64_t>(M.m, kb + M.kchunk);
       for (int a = 0; a < T; ++a)
-        for (int b = a; b < T; ++b) p->gram_tasks.push_back(Task{mi, a, b, ks});
+        for (int b = a; b < T; ++b)
+          put(M, (b + 1) * kBM <= M.n && (ke - kb) % 32 == 0, Task{mi, a, b, ks});
+    }
   }
+  flush(p->gram_list);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int T = (M.n + kBM - 1) / kBM;
     for (int a = 0; a < T; ++a)
-      for (int b = a; b < T; ++b) p->poly_tasks.push_back(Task{mi, a, b, 0});
+      for (int b = a; b < T; ++b) put(M, (b + 1) * kBM <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
   }
+  flush(p->poly_list);
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
     for (int a = 0; a < TM; ++a)
-      for (int b = 0; b < TN; ++b) p->update_tasks.push_back(Task{mi, a, b, 0});
+      for (int b = 0; b < TN; ++b)
+        put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
   }
+  flush(p->update_list);
   for (size_t i = 0; i < p->mats.size(); ++i)
     if (p->mats[i].ksplit > 1) {
       p->split_mats.push_back((int)i);
@@ -359,9 +386,9 @@ void plan_workspace(isoloco_plan_s* p) {
   };
   p->off_mats = take(p->mats.size() * sizeof(MatInfo));
   p->off_chunks = take(p->chunks.size() * sizeof(Chunk));
-  p->off_gt = take(p->gram_tasks.size() * sizeof(Task));
-  p->off_pt = take(p->poly_tasks.size() * sizeof(Task));
-  p->off_ut = take(p->update_tasks.size() * sizeof(Task));
+  p->off_gt = take(p->gram_list.tasks.size() * sizeof(Task));
+  p->off_pt = take(p->poly_list.tasks.size() * sizeof(Task));
+  p->off_ut = take(p->update_list.tasks.size() * sizeof(Task));
   p->off_sc = take(p->mats.size() * sizeof(MatScalars));
   p->off_psq = take(p->chunks.size() * sizeof(double));
   p->off_ptr = take(p->chunks.size() * sizeof(double));
@@ -380,9 +407,18 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   char* w = p->ws;
   t.mats = reinterpret_cast<const MatInfo*>(w + p->off_mats);
   t.chunks = reinterpret_cast<const Chunk*>(w + p->off_chunks);
-  t.gram_tasks = reinterpret_cast<const Task*>(w + p->off_gt);
-  t.poly_tasks = reinterpret_cast<const Task*>(w + p->off_pt);
-  t.update_tasks = reinterpret_cast<const Task*>(w + p->off_ut);
+  auto list = [&](const TaskListHost& L, size_t off) {
+    TaskList d{};
+    d.tasks = reinterpret_cast<const Task*>(w + off);
+    for (int q = 0; q < 3; ++q) {
+      d.seg_off[q] = L.seg_off[q];
+      d.seg_cnt[q] = L.seg_cnt[q];
+    }
+    return d;
+  };
+  t.gram_list = list(p->gram_list, p->off_gt);
+  t.poly_list = list(p->poly_list, p->off_pt);
+  t.update_list = list(p->update_list, p->off_ut);
   t.scalars = reinterpret_cast<MatScalars*>(w + p->off_sc);
   t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
@@ -396,9 +432,6 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.n_mat = (int)p->mats.size();
   t.n_chunks = (int)p->chunks.size();
   t.n_iso_chunks = p->n_iso_chunks;
-  t.n_gram_tasks = (int)p->gram_tasks.size();
-  t.n_poly_tasks = (int)p->poly_tasks.size();
-  t.n_update_tasks = (int)p->update_tasks.size();
   t.n_split = (int)p->split_mats.size();
   t.split_mats_host = p->split_mats.data();
   t.split_n_host = p->split_n.data();
@@ -521,9 +554,9 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
   };
   if ((e = up(plan->off_mats, plan->mats.data(), plan->mats.size() * sizeof(MatInfo))) != hipSuccess ||
       (e = up(plan->off_chunks, plan->chunks.data(), plan->chunks.size() * sizeof(Chunk))) != hipSuccess ||
-      (e = up(plan->off_gt, plan->gram_tasks.data(), plan->gram_tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_pt, plan->poly_tasks.data(), plan->poly_tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_ut, plan->update_tasks.data(), plan->update_tasks.size() * sizeof(Task))) != hipSuccess)
+      (e = up(plan->off_gt, plan->gram_list.tasks.data(), plan->gram_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_pt, plan->poly_list.tasks.data(), plan->poly_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess)
     return hip_fail(e, "copying plan tables to the workspace");
   if (!plan->mats.empty()) {
     e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));

@@ -6,14 +6,21 @@
 
 namespace isoloco {
 
+// A task list in three segments: interior tiles of row-major (T0) matrices,
+// interior tiles of wide-stored (T1) matrices, and tiles that touch a ragged
+// edge (any layout, bounds-checked kernel).
+struct TaskList {
+  const Task* tasks;
+  int seg_off[3];
+  int seg_cnt[3];
+};
+
 // Device tables and buffers inside the caller's workspace, plus the host copies
 // of the few values the launchers need to size grids.
 struct DevTables {
   const MatInfo* mats;
   const Chunk* chunks;  // ISO chunks first, then AVG chunks
-  const Task* gram_tasks;
-  const Task* poly_tasks;
-  const Task* update_tasks;
+  TaskList gram_list, poly_list, update_list;
   MatScalars* scalars;
   double* part_sq;
   double* part_tr;
@@ -24,7 +31,6 @@ struct DevTables {
   float* poly;
   float* gpart;
   int n_mat, n_chunks, n_iso_chunks;
-  int n_gram_tasks, n_poly_tasks, n_update_tasks;
   int n_split;
   const int* split_mats_host;  // host arrays of length n_split
   const int* split_n_host;

@@ -114,12 +114,20 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
       }
 #pragma unroll
       for (int q = 0; q < V; ++q) acc[q] = 0.f;
-#pragma unroll 4
-      for (int k = 0; k < K; ++k) {
-        float wv[V];
-        WL::vec(w.p[k], e, wv);
+      // workers in groups of 8: the group's 16-byte loads are all issued
+      // before any of them is consumed (differences summed in worker order)
+#pragma unroll 1
+      for (int k0 = 0; k0 < K; k0 += 8) {
+        float wv[8][V];
 #pragma unroll
-        for (int q = 0; q < V; ++q) acc[q] += th[q] - wv[q];
+        for (int j = 0; j < 8; ++j)
+          if (k0 + j < K) WL::vec(w.p[k0 + j], e, wv[j]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (k0 + j < K) {
+#pragma unroll
+            for (int q = 0; q < V; ++q) acc[q] += th[q] - wv[j][q];
+          }
       }
 #pragma unroll
       for (int q = 0; q < V; ++q) acc[q] *= inv_k;
@@ -511,39 +519,82 @@ struct Slab32 {
 // and the 16 consecutive k values 16 (t / 128) .. +15, so that its LDS writes
 // are 16-byte row segments and consecutive lanes write consecutive rows
 // (80-byte stride: no bank conflicts).
+// Interior slab (no bounds checks; the host only routes tiles whose rows,
+// columns and K range are all inside the matrix, with m, n multiples of 4).
+template <bool ICONTIG>
+__device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int i0, Slab32& r) {
+  const int t = threadIdx.x;
+  if (ICONTIG) {
+    // element (k, i) at base + k s_k + i: lanes take consecutive i (coalesced
+    // 4-byte loads); uniform slab base + 32-bit lane offsets
+    const char* sb = reinterpret_cast<const char*>(op.base + (int64_t)k0 * op.s_k + i0);
+    const uint32_t step = (uint32_t)op.s_k * 4u;
+    uint32_t ob = (uint32_t)(16 * (t >> 7)) * step + 4u * (uint32_t)(t & 127);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        r.v[q][e] = *reinterpret_cast<const float*>(sb + ob);
+        ob += step;
+      }
+  } else {
+    // element (k, i) at base + i s_i + k: each lane reads 64 contiguous bytes of its row
+    const char* sb = reinterpret_cast<const char*>(op.base + (int64_t)i0 * op.s_i + k0);
+    const uint32_t ob = (uint32_t)(t & 127) * (uint32_t)op.s_i * 4u + 64u * (uint32_t)(t >> 7);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.v[q] = *reinterpret_cast<const floatx4*>(sb + ob + 16 * q);
+  }
+  if (op.scale != 1.f) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.v[q] *= op.scale;
+  }
+}
+
+// Any slab: runtime layout, every element bounds-checked (zero outside).
 __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, Slab32& r) {
   const int t = threadIdx.x;
   const int i = i0 + (t & 127);
   const int kb = k0 + 16 * (t >> 7);
   if (op.icontig) {
-    // lanes take consecutive i: every 4-byte load is coalesced across the wave
+    const float* p = op.base + (int64_t)kb * op.s_k + i;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      floatx4 x = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int k = kb + 4 * q + e;
-        if (i < op.I && k < op.K) x[e] = op.base[(int64_t)k * op.s_k + i];
+        r.v[q][e] = (i < op.I && k < op.K) ? p[(int64_t)(4 * q + e) * op.s_k] : 0.f;
       }
-      r.v[q] = x * op.scale;
-    }
   } else {
-    // each lane reads 64 contiguous bytes of its row
     const float* p = op.base + (int64_t)i * op.s_i + kb;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      floatx4 x = {0.f, 0.f, 0.f, 0.f};
-      if (i < op.I) {
-        if (op.vec && kb + 4 * q + 3 < op.K) {
-          x = *reinterpret_cast<const floatx4*>(p + 4 * q);
-        } else {
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (kb + 4 * q + e < op.K) x[e] = p[4 * q + e];
-        }
+      for (int e = 0; e < 4; ++e) {
+        const int k = kb + 4 * q + e;
+        r.v[q][e] = (i < op.I && k < op.K) ? p[4 * q + e] : 0.f;
       }
-      r.v[q] = x * op.scale;
-    }
+  }
+  if (op.scale != 1.f) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.v[q] *= op.scale;
+  }
+}
+
+// Loader selected at compile time: LAYOUT kGeneric uses runtime layout and
+// bounds; the fast layouts fix the contiguity of the A and B operands.
+enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2 };
+
+template <int MODE, int LAYOUT, bool IS_A>
+__device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, Slab32& r) {
+  if (LAYOUT == kGeneric) {
+    slab32_load(op, k0, i0, r);
+  } else {
+    // Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
+    // k-contiguous for wide storage (T1).  Poly: A[k][i], always i-contiguous.
+    // Update: A = X[i][k] (k-contiguous for T0, i-contiguous for T1), B = P[k][j].
+    constexpr bool icontig =
+        MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? true : (IS_A ? (LAYOUT == kFastT1) : true);
+    slab32_load_fast<icontig>(op, k0, i0, r);
   }
 }
 
@@ -569,7 +620,7 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[k
   }
 }
 
-template <int MODE, int NS>
+template <int MODE, int NS, int LAYOUT>
 __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) __bf16 Ap[NS][kBM][kLdsK];
   __shared__ __attribute__((aligned(16))) __bf16 Bp[NS][kBN][kLdsK];
@@ -587,16 +638,16 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
   Slab32 ra, rb;
-  slab32_load(s.A, s.k_begin, s.i0, ra);
-  slab32_load(s.B, s.k_begin, s.j0, rb);
+  load_operand<MODE, LAYOUT, true>(s.A, s.k_begin, s.i0, ra);
+  load_operand<MODE, LAYOUT, false>(s.B, s.k_begin, s.j0, rb);
   for (int k0 = s.k_begin; k0 < s.k_end; k0 += kBK2) {
     __syncthreads();
     slab32_store<NS>(ra, Ap);
     slab32_store<NS>(rb, Bp);
     __syncthreads();
     if (k0 + kBK2 < s.k_end) {
-      slab32_load(s.A, k0 + kBK2, s.i0, ra);
-      slab32_load(s.B, k0 + kBK2, s.j0, rb);
+      load_operand<MODE, LAYOUT, true>(s.A, k0 + kBK2, s.i0, ra);
+      load_operand<MODE, LAYOUT, false>(s.B, k0 + kBK2, s.j0, rb);
     }
 #pragma unroll
     for (int kk = 0; kk < kBK2; kk += 16) {
@@ -800,6 +851,38 @@ hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStr
   return hipGetLastError();
 }
 
+template <int MODE, int NS>
+static void launch_bf16_segments(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
+  GemmArgs g = g0;
+  const dim3 block(kGemmThreads);
+  if (L.seg_cnt[0]) {
+    g.tasks = L.tasks + L.seg_off[0];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0>), dim3(L.seg_cnt[0]), block, 0, st, g);
+  }
+  if (L.seg_cnt[1]) {
+    g.tasks = L.tasks + L.seg_off[1];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1>), dim3(L.seg_cnt[1]), block, 0, st, g);
+  }
+  if (L.seg_cnt[2]) {
+    g.tasks = L.tasks + L.seg_off[2];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric>), dim3(L.seg_cnt[2]), block, 0, st, g);
+  }
+}
+
+template <int MODE>
+static void launch_mode(const TaskList& L, const GemmArgs& g0, int arith, hipStream_t st) {
+  if (arith == kArithFp32) {
+    GemmArgs g = g0;
+    g.tasks = L.tasks;
+    const int n = L.seg_cnt[0] + L.seg_cnt[1] + L.seg_cnt[2];
+    if (n) hipLaunchKernelGGL(gemm_f32_kernel<MODE>, dim3(n), dim3(kGemmThreads), 0, st, g);
+  } else if (arith == kArithBf16x6) {
+    launch_bf16_segments<MODE, 3>(L, g0, st);
+  } else {
+    launch_bf16_segments<MODE, 2>(L, g0, st);
+  }
+}
+
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st) {
   GemmArgs g;
   g.mats = t.mats;
@@ -814,24 +897,10 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.cc = p.cc;
   g.first = p.first;
   g.only_active = p.only_active;
-  const Task* tasks = mode == kGram ? t.gram_tasks : mode == kPoly ? t.poly_tasks : t.update_tasks;
-  const int n = mode == kGram ? t.n_gram_tasks : mode == kPoly ? t.n_poly_tasks : t.n_update_tasks;
-  if (n == 0) return hipSuccess;
-  g.tasks = tasks;
-  const dim3 grid(n), block(kGemmThreads);
-  if (p.arith == kArithFp32) {
-    if (mode == kGram) hipLaunchKernelGGL(gemm_f32_kernel<kGram>, grid, block, 0, st, g);
-    else if (mode == kPoly) hipLaunchKernelGGL(gemm_f32_kernel<kPoly>, grid, block, 0, st, g);
-    else hipLaunchKernelGGL(gemm_f32_kernel<kUpdate>, grid, block, 0, st, g);
-  } else if (p.arith == kArithBf16x6) {
-    if (mode == kGram) hipLaunchKernelGGL((gemm_bf16_kernel<kGram, 3>), grid, block, 0, st, g);
-    else if (mode == kPoly) hipLaunchKernelGGL((gemm_bf16_kernel<kPoly, 3>), grid, block, 0, st, g);
-    else hipLaunchKernelGGL((gemm_bf16_kernel<kUpdate, 3>), grid, block, 0, st, g);
-  } else {
-    if (mode == kGram) hipLaunchKernelGGL((gemm_bf16_kernel<kGram, 2>), grid, block, 0, st, g);
-    else if (mode == kPoly) hipLaunchKernelGGL((gemm_bf16_kernel<kPoly, 2>), grid, block, 0, st, g);
-    else hipLaunchKernelGGL((gemm_bf16_kernel<kUpdate, 2>), grid, block, 0, st, g);
-  }
+  g.tasks = nullptr;
+  if (mode == kGram) launch_mode<kGram>(t.gram_list, g, p.arith, st);
+  else if (mode == kPoly) launch_mode<kPoly>(t.poly_list, g, p.arith, st);
+  else launch_mode<kUpdate>(t.update_list, g, p.arith, st);
   return hipGetLastError();
 }
 

@@ -83,8 +83,8 @@ class ReplicaGenerator:
                 shared = (G1 @ G2.T).mul_(c / math.sqrt(r)).reshape(-1)
             else:
                 shared = torch.randn(n, generator=g, device=self.device, dtype=torch.float32).mul_(c)
-            for k in range(K):
-                e = torch.randn(n, generator=g, device=self.device, dtype=torch.float32)
-                dk = shared + e.mul_(cfg.noise_std)
-                out[k, off:off + n] = (th - dk).to(self.wdtype)
+            # all K workers' noise in one draw: row k is worker k
+            e = torch.randn((K, n), generator=g, device=self.device, dtype=torch.float32)
+            e.mul_(cfg.noise_std).add_(shared)
+            out[:, off:off + n] = (th.unsqueeze(0) - e).to(self.wdtype)
         return out
