@@ -22,6 +22,7 @@ namespace isoloco {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -62,7 +63,8 @@ template <>
 struct WorkerLoad<0> {
   static constexpr int kVec = 4;  // elements per 16-byte access
   __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
-    const floatx4 v = *reinterpret_cast<const floatx4*>(static_cast<const float*>(p) + i);
+    // replicas are read once: non-temporal loads keep them from displacing cached data
+    const floatx4 v = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(static_cast<const float*>(p) + i));
     out[0] = v[0]; out[1] = v[1]; out[2] = v[2]; out[3] = v[3];
   }
   __device__ static __forceinline__ float one(const void* p, int64_t i) {
@@ -74,8 +76,8 @@ template <>
 struct WorkerLoad<1> {
   static constexpr int kVec = 8;
   __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
-    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p) + i));
+    const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       out[2 * q] = __uint_as_float(w[q] << 16);

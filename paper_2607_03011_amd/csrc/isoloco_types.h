@@ -11,7 +11,7 @@ constexpr int kBK = 16;
 constexpr int kGemmThreads = 256;
 
 // Elements per workgroup of the streaming kernels (reduction, trace, write-back).
-constexpr int kChunk = 16384;
+constexpr int kChunk = 4096;
 constexpr int kStreamThreads = 256;
 
 constexpr int kMaxWorkers = 128;
