@@ -32,17 +32,27 @@ def _cfg(layout, n, K, dtype="f32", rank=16, c=1e-3, steps=1):
                           steps=steps, low_rank_scale=c)
 
 
+def _host_slices(theta, workers, mom, layout, select):
+    """Host copies of the selected tensors only: {i: (theta, [worker_k], B)}."""
+    out = {}
+    for i in select:
+        off, rows, cols, kind = layout[i]
+        sl = slice(off, off + rows * cols)
+        out[i] = (theta[sl].cpu().numpy().copy(), workers_host(workers[:, sl]), mom[sl].cpu().numpy().copy())
+    return out
+
+
 def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select=None, check_q=True,
-                     theta=None, mom=None, plan=None, opts=None):
+                     theta=None, mom=None, plan=None, opts=None, return_inputs=False):
     from workload import ReplicaGenerator
     dev = torch.device("cuda", 0)
     gen = ReplicaGenerator(cfg, seed=seed, device=dev)
     if theta is None:
         theta, mom = gen.init_state()
     workers = gen.workers(theta, step)
-    th0 = theta.cpu().numpy().copy()
-    b0 = mom.cpu().numpy().copy()
-    wh = workers_host(workers)
+    sel = list(range(len(cfg.layout))) if select is None else list(select)
+    host = _host_slices(theta, workers, mom, cfg.layout, sel)
+    theta_in = theta.clone() if return_inputs else None
     own = plan is None
     if own:
         wdt = iso.ISOLOCO_F32 if cfg.worker_dtype == "f32" else iso.ISOLOCO_BF16
@@ -52,24 +62,24 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
     plan.aggregate(theta, workers, mom, alpha, lr, mu)
     torch.cuda.synchronize()
     st = plan.stats()
-    th = theta.cpu().numpy().astype(np.float64)
-    b = mom.cpu().numpy().astype(np.float64)
-    ref = oracle_per_tensor(cfg.layout, th0, wh, b0, alpha, lr, mu, select=select)
-    zero_b0 = not b0.any()
-    for i, (th_r, b_r, sb_r) in ref.items():
+    for i in sel:
         off, rows, cols, kind = cfg.layout[i]
         sl = slice(off, off + rows * cols)
-        e_th = relF(th[sl], th_r)
-        e_b = relF(b[sl], b_r)
-        e_upd = relF(th[sl] - th0[sl], th_r - th0[sl])
+        th0, wh, b0 = host[i]
+        th_r, b_r, sb_r = oracle_per_tensor([(0, rows, cols, kind)], th0, wh, b0, alpha, lr, mu)[0]
+        th = theta[sl].double().cpu().numpy()
+        b = mom[sl].double().cpu().numpy()
+        e_th = relF(th, th_r)
+        e_b = relF(b, b_r)
+        e_upd = relF(th - th0, th_r - th0)
         msg = "tensor %d (%dx%d kind %d): theta %.2e B %.2e update %.2e" % (i, rows, cols, kind, e_th, e_b, e_upd)
         if kind == KIND_ISO:
             msg += " sigma_bar gpu %.6e oracle %.6e steps %d resid %.2e flags %d" % (
                 st[i].sigma_bar, sb_r, st[i].steps, st[i].orth_resid, st[i].flags)
         print(msg, flush=True)
         assert e_th <= TOL and e_b <= TOL and e_upd <= TOL, msg
-        if kind == KIND_ISO and check_q and zero_b0 and sb_r > 0 and alpha != 0:
-            Q = b[sl].reshape(rows, cols) / (alpha * st[i].sigma_bar)
+        if kind == KIND_ISO and check_q and not b0.any() and sb_r > 0 and alpha != 0:
+            Q = b.reshape(rows, cols) / (alpha * st[i].sigma_bar)
             G = Q.T @ Q if rows >= cols else Q @ Q.T
             r = min(rows, cols)
             orth = np.linalg.norm(G - np.eye(r)) / np.sqrt(r)
@@ -77,7 +87,45 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
             assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
     if own:
         plan.close()
+    if return_inputs:
+        return theta, mom, st, theta_in, workers
     return theta, mom, st
+
+
+def _check_polar_properties(lay, st, mom, theta_in, workers, alpha=1.0):
+    """For every corrected matrix, from the outputs of a first step (B = 0
+    before it): Q = B / (alpha sigma_bar) has orthonormal columns (short side),
+    sigma_bar = <Q, Delta> / r, and H = Q^T Delta is symmetric positive
+    semi-definite -- which characterises Q as the polar factor of Delta when
+    Delta has full rank.  Computed in float64 on the GPU."""
+    dev = mom.device
+    worst = [0.0, 0.0, 0.0]
+    for i, (off, rows, cols, kind) in enumerate(lay):
+        if kind != KIND_ISO:
+            continue
+        n_el = rows * cols
+        Q = (mom[off:off + n_el].double() / (alpha * st[i].sigma_bar)).reshape(rows, cols)
+        th = theta_in[off:off + n_el].double()
+        delta = torch.zeros_like(th)
+        for k in range(workers.shape[0]):
+            delta += th - workers[k, off:off + n_el].double()
+        delta = (delta / workers.shape[0]).reshape(rows, cols)
+        if rows < cols:
+            Q, delta = Q.T, delta.T
+        r = Q.shape[1]
+        orth = (torch.linalg.norm(Q.T @ Q - torch.eye(r, dtype=Q.dtype, device=dev)) / r ** 0.5).item()
+        H = Q.T @ delta
+        hn = torch.linalg.norm(H).item()
+        asym = (torch.linalg.norm(H - H.T) / hn).item()
+        lmin = torch.linalg.eigvalsh((H + H.T) / 2)[0].item() / hn
+        sb = (torch.trace(H) / r).item()
+        worst = [max(worst[0], orth), max(worst[1], asym), min(worst[2], lmin)]
+        assert orth <= TOL, (i, orth)
+        assert asym <= TOL, (i, asym)
+        assert lmin >= -TOL, (i, lmin)
+        assert abs(sb - st[i].sigma_bar) <= TOL * st[i].sigma_bar, (i, sb, st[i].sigma_bar)
+        assert st[i].flags == 0 and 0 <= st[i].orth_resid <= TOL
+    print("all matrices: max orth %.2e, max asym(Q^T Delta) %.2e, min eig %.2e" % tuple(worst), flush=True)
 
 
 RAGGED = [(300, 200, KIND_ISO), (129, 1, KIND_AVG), (200, 300, KIND_ISO), (520, 130, KIND_ISO),
@@ -223,37 +271,52 @@ def test_config1_full_block(iso):
     _run_and_compare(iso, CONFIGS[1], select=None)
 
 
-def test_config2_full_size_sampled(iso):
-    """The 109.5M-parameter workload at full size in the benchmark's launch
-    configuration: every 1-D tensor and one tensor of each 2-D shape (q of
-    block 0, gate of block 0, down of block 0, the tied embedding) against
-    the oracle, and for all 85 matrices the polar factor recovered from the
-    momentum must be orthonormal with sigma_bar = <Q, Delta> / r."""
-    from workload import CONFIGS, ReplicaGenerator
-    cfg = CONFIGS[2]
-    lay = cfg.layout
+def _one_of_each_shape(lay):
     sample = [i for i, t in enumerate(lay) if t[3] == KIND_AVG]
-    for shape in [(768, 768), (2048, 768), (768, 2048), (32000, 768)]:
-        sample.append(next(i for i, t in enumerate(lay) if (t[1], t[2]) == shape))
-    theta, mom, st = _run_and_compare(iso, cfg, select=sample)
-    # properties of every corrected matrix, computed from the outputs in fp32 on the GPU
-    dev = theta.device
-    gen = ReplicaGenerator(cfg, seed=0, device=dev)
-    th0, _ = gen.init_state()
-    workers = gen.workers(th0, 1)
-    for i, (off, rows, cols, kind) in enumerate(lay):
-        if kind != KIND_ISO:
-            continue
-        n_el = rows * cols
-        Q = (mom[off:off + n_el].reshape(rows, cols) / st[i].sigma_bar).double()
-        G = Q.T @ Q if rows >= cols else Q @ Q.T
-        r = min(rows, cols)
-        orth = (torch.linalg.norm(G - torch.eye(r, dtype=G.dtype, device=dev)) / r ** 0.5).item()
-        delta = (th0[off:off + n_el].double() - workers[:, off:off + n_el].double()).mean(0).reshape(rows, cols)
-        sb = ((Q * delta).sum() / r).item()
-        assert orth <= TOL, (i, orth)
-        assert abs(sb - st[i].sigma_bar) <= TOL * st[i].sigma_bar, (i, sb, st[i].sigma_bar)
-        assert st[i].flags == 0 and 0 <= st[i].orth_resid <= TOL
+    seen = set()
+    for i, (off, r, c, kind) in enumerate(lay):
+        if kind == KIND_ISO and (r, c) not in seen:
+            seen.add((r, c))
+            sample.append(i)
+    return sample
+
+
+def test_config2_full_size_sampled(iso):
+    """The 109.5M-parameter workload (K = 16, fp32 replicas) at full size in
+    the benchmark's launch configuration: every 1-D tensor and one tensor of
+    each 2-D shape against the oracle; the polar-factor properties for all 85
+    matrices."""
+    from workload import CONFIGS
+    cfg = CONFIGS[2]
+    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
+                                                      return_inputs=True)
+    _check_polar_properties(cfg.layout, st, mom, th_in, workers)
+
+
+@pytest.mark.timeout(900)
+def test_config3_full_size_sampled(iso):
+    """24 blocks d = 1024 / FFN 2816 + 32000 x 1024 (341M parameters), K = 32
+    bf16 replicas with per-tensor scales from LogUniform(1e-4, 1e-2): 1-D
+    tensors and one tensor of each shape against the oracle, properties for
+    all 169 matrices."""
+    from workload import CONFIGS
+    cfg = CONFIGS[3]
+    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
+                                                      return_inputs=True)
+    _check_polar_properties(cfg.layout, st, mom, th_in, workers)
+
+
+@pytest.mark.timeout(900)
+def test_config4_full_size_sampled(iso):
+    """16 blocks d = 2048 / FFN 5632 + 32000 x 2048 (888M parameters), K = 64
+    bf16 replicas (114 GB in HBM): 1-D tensors and one square matrix against
+    the oracle, properties for all 113 matrices."""
+    from workload import CONFIGS
+    cfg = CONFIGS[4]
+    sample = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_AVG]
+    sample.append(next(i for i, t in enumerate(cfg.layout) if (t[1], t[2]) == (2048, 2048)))
+    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True)
+    _check_polar_properties(cfg.layout, st, mom, th_in, workers)
 
 
 def _planted(rows, cols, smin, rng):
