@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -203,6 +204,67 @@ std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
   return out;
 }
 
+// Workgroup b of a launch runs on XCD b % 8, and each XCD has its own L2.
+// The tiles of one matrix (of one K slice, for the split Gram) read the same
+// row and column panels, so they are kept on one XCD where the panels stay in
+// its L2: the tasks are cut into such groups, the groups of each shape class
+// are dealt round robin to the 8 XCDs (each XCD then carries the same share
+// of every class, whichever classes are still iterating), the groups left
+// over after whole rounds are cut into 8 contiguous runs of tiles, and the
+// 8 queues are interleaved into one grid.  Short queues are padded with
+// empty tasks (mat = -1), which return at once.
+constexpr int kXcds = 8;
+
+std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<Task>& in, bool by_slice) {
+  struct Group {
+    size_t begin, end;
+  };
+  std::vector<Group> groups;
+  for (size_t i = 0; i < in.size();) {
+    size_t j = i + 1;
+    while (j < in.size() && in[j].mat == in[i].mat && (!by_slice || in[j].ks == in[i].ks)) ++j;
+    groups.push_back({i, j});
+    i = j;
+  }
+  // shape class of a group: the matrix shape and layout, the group's size and,
+  // for a K slice, its length
+  auto key = [&](const Group& g) {
+    const MatInfo& M = mats[in[g.begin].mat];
+    const int64_t kb = (int64_t)in[g.begin].ks * M.kchunk;
+    const int64_t klen = by_slice ? std::min<int64_t>(M.m, kb + M.kchunk) - kb : 0;
+    return std::array<int64_t, 5>{M.m, M.n, M.trans, (int64_t)(g.end - g.begin), klen};
+  };
+  std::vector<std::array<int64_t, 5>> keys;
+  std::vector<std::vector<size_t>> classes;
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const auto k = key(groups[gi]);
+    size_t c = 0;
+    while (c < keys.size() && keys[c] != k) ++c;
+    if (c == keys.size()) {
+      keys.push_back(k);
+      classes.emplace_back();
+    }
+    classes[c].push_back(gi);
+  }
+  std::vector<Task> q[kXcds];
+  for (const auto& cl : classes) {
+    const size_t whole = cl.size() - cl.size() % kXcds;
+    for (size_t j = 0; j < whole; ++j)
+      for (size_t t = groups[cl[j]].begin; t < groups[cl[j]].end; ++t) q[j % kXcds].push_back(in[t]);
+    std::vector<Task> rest;
+    for (size_t j = whole; j < cl.size(); ++j)
+      for (size_t t = groups[cl[j]].begin; t < groups[cl[j]].end; ++t) rest.push_back(in[t]);
+    for (int x = 0; x < kXcds; ++x)
+      for (size_t t = rest.size() * x / kXcds; t < rest.size() * (x + 1) / kXcds; ++t) q[x].push_back(rest[t]);
+  }
+  size_t len = 0;
+  for (int x = 0; x < kXcds; ++x) len = std::max(len, q[x].size());
+  std::vector<Task> out(len * kXcds, Task{-1, 0, 0, 0});
+  for (int x = 0; x < kXcds; ++x)
+    for (size_t s = 0; s < q[x].size(); ++s) out[s * kXcds + x] = q[x][s];
+  return out;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -323,19 +385,24 @@ void plan_matrices(isoloco_plan_s* p) {
   p->npart = part;
 
   // Work lists, longest tasks first, each in three segments (interior tiles of
-  // row-major matrices, interior tiles of wide-stored matrices, ragged tiles).
+  // row-major matrices, interior tiles of wide-stored matrices, ragged tiles),
+  // each segment reordered for the XCD round robin of the dispatcher.
   std::vector<Task> seg[3];
-  auto flush = [&](TaskListHost& L) {
+  auto flush = [&](TaskListHost& L, bool by_slice) {
     L.tasks.clear();
     for (int q = 0; q < 3; ++q) {
+      const std::vector<Task> o = xcd_order(p->mats, seg[q], by_slice);
       L.seg_off[q] = (int)L.tasks.size();
-      L.seg_cnt[q] = (int)seg[q].size();
-      L.tasks.insert(L.tasks.end(), seg[q].begin(), seg[q].end());
+      L.seg_cnt[q] = (int)o.size();
+      L.tasks.insert(L.tasks.end(), o.begin(), o.end());
       seg[q].clear();
     }
   };
+  // The interior kernels address a matrix with 32-bit byte offsets: matrices
+  // of 2^29 elements or more take the generic kernel.
   auto put = [&](const MatInfo& M, bool interior, const Task& tk) {
-    seg[!(interior && M.vec) ? 2 : (M.trans ? 1 : 0)].push_back(tk);
+    const bool fast = interior && M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29);
+    seg[!fast ? 2 : (M.trans ? 1 : 0)].push_back(tk);
   };
   std::vector<int> order(p->mats.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
@@ -353,7 +420,7 @@ void plan_matrices(isoloco_plan_s* p) {
           put(M, (b + 1) * kBM <= M.n && (ke - kb) % 32 == 0, Task{mi, a, b, ks});
     }
   }
-  flush(p->gram_list);
+  flush(p->gram_list, true);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
@@ -361,7 +428,7 @@ void plan_matrices(isoloco_plan_s* p) {
     for (int a = 0; a < T; ++a)
       for (int b = a; b < T; ++b) put(M, (b + 1) * kBM <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
   }
-  flush(p->poly_list);
+  flush(p->poly_list, false);
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
@@ -369,7 +436,7 @@ void plan_matrices(isoloco_plan_s* p) {
       for (int b = 0; b < TN; ++b)
         put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
   }
-  flush(p->update_list);
+  flush(p->update_list, false);
   for (size_t i = 0; i < p->mats.size(); ++i)
     if (p->mats[i].ksplit > 1) {
       p->split_mats.push_back((int)i);

@@ -451,7 +451,7 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
   __shared__ float As[kBK][kLdsW];
   __shared__ float Bs[kBK][kLdsW];
   const Task task = g.tasks[blockIdx.x];
-  if (g.only_active && !g.sc[task.mat].active) return;
+  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   const GemmSetup s = gemm_setup<MODE>(g, task);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -517,38 +517,47 @@ struct Slab32 {
   floatx4 v[4];
 };
 
+// Word 3 of a raw buffer resource on CDNA3/CDNA4 (32-bit data format, no
+// swizzle; the range check compares byte offsets with the record count).
+constexpr int kBufferFlags = 0x00020000;
+
 // 128 (i) x 32 (k) fp32 slab into registers: thread t owns row i = t % 128
 // and the 16 consecutive k values 16 (t / 128) .. +15, so that its LDS writes
 // are 16-byte row segments and consecutive lanes write consecutive rows
-// (80-byte stride: no bank conflicts).
+// (80-byte stride: no bank conflicts).  SCALED multiplies by the operand's
+// scale (the 1/||Delta||_F of the first polar step; 1 afterwards, when the
+// multiply is left out).
 // Interior slab (no bounds checks; the host only routes tiles whose rows,
 // columns and K range are all inside the matrix, with m, n multiples of 4).
 template <bool ICONTIG>
 __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int i0, Slab32& r) {
   const int t = threadIdx.x;
+  // Buffer loads: a uniform resource for the operand's matrix, one 32-bit lane
+  // offset that is fixed for the whole slab, and the k advance as a scalar
+  // offset (t / 128 is uniform over a wave), so that no per-load address
+  // arithmetic runs on the vector ALU.  The host keeps matrices of these tiles
+  // under 2^29 elements, so every byte offset fits 31 bits.
+  const int kh = __builtin_amdgcn_readfirstlane(t >> 7);
+  const int bytes = 4 * ((op.K - 1) * (int)op.s_k + (op.I - 1) * (int)op.s_i + 1);
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(op.base), (short)0, bytes, kBufferFlags);
+  const int kb = k0 + 16 * kh;
   if (ICONTIG) {
     // element (k, i) at base + k s_k + i: lanes take consecutive i (coalesced
-    // 4-byte loads); uniform slab base + 32-bit lane offsets
-    const char* sb = reinterpret_cast<const char*>(op.base + (int64_t)k0 * op.s_k + i0);
-    const uint32_t step = (uint32_t)op.s_k * 4u;
-    uint32_t ob = (uint32_t)(16 * (t >> 7)) * step + 4u * (uint32_t)(t & 127);
+    // 4-byte loads)
+    const int vo = 4 * (i0 + (t & 127));
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        r.v[q][e] = *reinterpret_cast<const float*>(sb + ob);
-        ob += step;
-      }
+      for (int e = 0; e < 4; ++e)
+        r.v[q][e] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(rs, vo, 4 * (kb + 4 * q + e) * (int)op.s_k, 0));
   } else {
     // element (k, i) at base + i s_i + k: each lane reads 64 contiguous bytes of its row
-    const char* sb = reinterpret_cast<const char*>(op.base + (int64_t)i0 * op.s_i + k0);
-    const uint32_t ob = (uint32_t)(t & 127) * (uint32_t)op.s_i * 4u + 64u * (uint32_t)(t >> 7);
+    const int vo = 4 * (i0 + (t & 127)) * (int)op.s_i;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) r.v[q] = *reinterpret_cast<const floatx4*>(sb + ob + 16 * q);
-  }
-  if (op.scale != 1.f) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) r.v[q] *= op.scale;
+    for (int q = 0; q < 4; ++q)
+      r.v[q] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 16 * q, 4 * kb, 0));
   }
 }
 
@@ -576,10 +585,6 @@ __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, S
         r.v[q][e] = (i < op.I && k < op.K) ? p[4 * q + e] : 0.f;
       }
   }
-  if (op.scale != 1.f) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) r.v[q] *= op.scale;
-  }
 }
 
 // Loader selected at compile time: LAYOUT kGeneric uses runtime layout and
@@ -600,21 +605,30 @@ __device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, 
   }
 }
 
-template <int NS>
-__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[kBM][kLdsK]) {
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Split the thread's 16 values into NS bf16 parts, two values per convert,
+// and store each part plane as two 16-byte row segments.  SCALED multiplies
+// the values by the operand's scale first (the 1/||Delta||_F of the first
+// polar step; 1 afterwards, when the multiply is left out).
+template <int NS, bool SCALED = false>
+__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale = 1.f) {
   const int t = threadIdx.x;
   const int i = t & 127, kb = 16 * (t >> 7);
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     bf16x8 part[NS];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float x = r.v[2 * half + e / 4][e % 4];
+    for (int e = 0; e < 8; e += 2) {
+      floatx2 x = {r.v[2 * half + e / 4][e % 4], r.v[2 * half + e / 4][e % 4 + 1]};
+      if (SCALED) x *= scale;
 #pragma unroll
       for (int p = 0; p < NS; ++p) {
-        const __bf16 h = (__bf16)x;
-        part[p][e] = h;
-        x -= (float)h;
+        const bf16x2 h = __builtin_convertvector(x, bf16x2);
+        part[p][e] = h[0];
+        part[p][e + 1] = h[1];
+        if (p + 1 < NS) x -= __builtin_convertvector(h, floatx2);
       }
     }
 #pragma unroll
@@ -622,15 +636,57 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[k
   }
 }
 
-template <int MODE, int NS, int LAYOUT>
-__global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NS][kBM][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NS][kBN][kLdsK];
-  const Task task = g.tasks[blockIdx.x];
-  if (g.only_active && !g.sc[task.mat].active) return;
-  const GemmSetup s = gemm_setup<MODE>(g, task);
+// One k16 substep of the 64 x 64 wave tile: read the operand fragments of
+// the NS planes from LDS and issue the part products (smallest order first).
+template <int NS>
+__device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[kBM][kLdsK], const __bf16 (*Bp)[kBN][kLdsK],
+                                             int kk, floatx16 (&acc)[2][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const int kc = kk + 8 * (lane >> 5);
+  bf16x8 av[2][NS], bv[2][NS];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int row = wm * 64 + a * 32 + (lane & 31);
+#pragma unroll
+    for (int p = 0; p < NS; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
+  }
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int row = wn * 64 + b * 32 + (lane & 31);
+#pragma unroll
+    for (int p = 0; p < NS; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
+  }
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int ord = NS - 1; ord >= 0; --ord)
+#pragma unroll
+        for (int pa = ord; pa >= 0; --pa)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
+}
+
+// bf16x3 (NS = 2) double-buffers the LDS slabs: while the products of slab s
+// run from one buffer, slab s + 1 is split and stored into the other and the
+// global loads of slab s + 2 are in flight; one barrier per slab, and the
+// steady-state loop body is a single basic block (the look-ahead slab index
+// is clamped to the last slab instead of branching), so that the compiler can
+// interleave the split arithmetic with the matrix products.  bf16x6 (NS = 3)
+// needs 1.5x the LDS per buffer and keeps a single buffer with two barriers.
+// SCALED: the X operands are multiplied by the first step's 1/||Delta||_F.
+template <int MODE, int NS, int LAYOUT, bool SCALED>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
+  constexpr int NB = NS == 2 ? 2 : 1;
+  // only X operands carry a scale (Gram: both, Update: A)
+  constexpr bool SA = SCALED && MODE != kPoly;
+  constexpr bool SB = SCALED && MODE == kGram;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBM][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBN][kLdsK];
+  const Task task = g.tasks[blockIdx.x];
+  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
+  const GemmSetup s = gemm_setup<MODE>(g, task);
   floatx16 acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -639,46 +695,70 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
+  const int nslab = (s.k_end - s.k_begin + kBK2 - 1) / kBK2;
+  const int klast = s.k_begin + (nslab - 1) * kBK2;
   Slab32 ra, rb;
+  if (nslab > 0) {
   load_operand<MODE, LAYOUT, true>(s.A, s.k_begin, s.i0, ra);
   load_operand<MODE, LAYOUT, false>(s.B, s.k_begin, s.j0, rb);
-  for (int k0 = s.k_begin; k0 < s.k_end; k0 += kBK2) {
+  if (NB == 2) {
+    // Registers hold two slabs in flight: at the top of the products of slab
+    // sl, slab sl + 1 is in (ra1, rb1) and slab sl + 2 in (ra, rb).  Each
+    // iteration splits and stores the first into the idle LDS buffer and
+    // reloads its registers with slab sl + 3, so a load has about two slabs of
+    // products to land.  The loop is unrolled by two so that the register
+    // roles are static.
+    auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
+    Slab32 ra1, rb1;
+    load_operand<MODE, LAYOUT, true>(s.A, kat(1), s.i0, ra1);
+    load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
+    slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
+    slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+    load_operand<MODE, LAYOUT, true>(s.A, kat(2), s.i0, ra);
+    load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
     __syncthreads();
-    slab32_store<NS>(ra, Ap);
-    slab32_store<NS>(rb, Bp);
-    __syncthreads();
-    if (k0 + kBK2 < s.k_end) {
-      load_operand<MODE, LAYOUT, true>(s.A, k0 + kBK2, s.i0, ra);
-      load_operand<MODE, LAYOUT, false>(s.B, k0 + kBK2, s.j0, rb);
+    int sl = 0;
+    for (; sl + 2 < nslab; sl += 2) {
+      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
+      slab32_store<NS, SA>(ra1, Ap[1], s.A.scale);
+      slab32_store<NS, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+      load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
+      load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
+      __syncthreads();
+      mfma_substep<NS>(Ap[1], Bp[1], 0, acc);
+      slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
+      slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+      mfma_substep<NS>(Ap[1], Bp[1], 16, acc);
+      load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
+      load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
+      __syncthreads();
     }
-#pragma unroll
-    for (int kk = 0; kk < kBK2; kk += 16) {
-      const int kc = kk + 8 * (lane >> 5);
-      bf16x8 av[2][NS], bv[2][NS];
-#pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        const int row = wm * 64 + a * 32 + (lane & 31);
-#pragma unroll
-        for (int p = 0; p < NS; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
-      }
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int row = wn * 64 + b * 32 + (lane & 31);
-#pragma unroll
-        for (int p = 0; p < NS; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
-      }
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          // part products of order NS - 1 down to 0 (smallest first)
-#pragma unroll
-          for (int ord = NS - 1; ord >= 0; --ord)
-#pragma unroll
-            for (int pa = ord; pa >= 0; --pa)
-              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
-        }
+    // one or two slabs remain: slab sl in buffer 0, slab sl + 1 in (ra1, rb1)
+    int last = 0;
+    if (sl + 1 < nslab) {
+      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
+      slab32_store<NS, SA>(ra1, Ap[1], s.A.scale);
+      slab32_store<NS, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+      __syncthreads();
+      last = 1;
     }
+    mfma_substep<NS>(Ap[last], Bp[last], 0, acc);
+    mfma_substep<NS>(Ap[last], Bp[last], 16, acc);
+  } else {
+    for (int sl = 0; sl < nslab; ++sl) {
+      __syncthreads();
+      slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
+      slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+      __syncthreads();
+      const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
+      load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
+      load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
+      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+    }
+  }
   }
   gemm_epilogue<MODE>(g, s, task, acc);
 }
@@ -853,22 +933,30 @@ hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStr
   return hipGetLastError();
 }
 
-template <int MODE, int NS>
+template <int MODE, int NS, bool SCALED>
 static void launch_bf16_segments(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kGemmThreads);
   if (L.seg_cnt[0]) {
     g.tasks = L.tasks + L.seg_off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0>), dim3(L.seg_cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0, SCALED>), dim3(L.seg_cnt[0]), block, 0, st, g);
   }
   if (L.seg_cnt[1]) {
     g.tasks = L.tasks + L.seg_off[1];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1>), dim3(L.seg_cnt[1]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1, SCALED>), dim3(L.seg_cnt[1]), block, 0, st, g);
   }
   if (L.seg_cnt[2]) {
     g.tasks = L.tasks + L.seg_off[2];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric>), dim3(L.seg_cnt[2]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric, SCALED>), dim3(L.seg_cnt[2]), block, 0, st, g);
   }
+}
+
+// The first step's X operands carry the 1/||Delta||_F pre-scaling (Poly reads
+// only Gram outputs and never does).
+template <int MODE, int NS>
+static void launch_bf16(const TaskList& L, const GemmArgs& g, hipStream_t st) {
+  if (MODE != kPoly && g.first) launch_bf16_segments<MODE, NS, MODE != kPoly>(L, g, st);
+  else launch_bf16_segments<MODE, NS, false>(L, g, st);
 }
 
 template <int MODE>
@@ -879,9 +967,9 @@ static void launch_mode(const TaskList& L, const GemmArgs& g0, int arith, hipStr
     const int n = L.seg_cnt[0] + L.seg_cnt[1] + L.seg_cnt[2];
     if (n) hipLaunchKernelGGL(gemm_f32_kernel<MODE>, dim3(n), dim3(kGemmThreads), 0, st, g);
   } else if (arith == kArithBf16x6) {
-    launch_bf16_segments<MODE, 3>(L, g0, st);
+    launch_bf16<MODE, 3>(L, g0, st);
   } else {
-    launch_bf16_segments<MODE, 2>(L, g0, st);
+    launch_bf16<MODE, 2>(L, g0, st);
   }
 }
 

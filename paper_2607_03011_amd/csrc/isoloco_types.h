@@ -63,7 +63,7 @@ constexpr int kNormSlices = 32;
 
 // Work item of a batched matrix product: one output tile of one matrix.
 struct Task {
-  int32_t mat;
+  int32_t mat;     // matrix index; -1 marks an empty task that returns at once
   int32_t tm, tn;  // tile row / column
   int32_t ks;      // K slice (Gram only)
 };
