@@ -401,15 +401,16 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = acc[a][b][4 * grp + r];
           } else {
-            // P = cb g^2 A + cc g^4 A^2  (g = 1 after the first step)
+            // P = g (ca I + cb g^2 A + cc g^4 A^2)  (g = 1 after the first
+            // step), so that the update is the plain product X' = X P
             const float g2 = s.gs * s.gs;
-            const float beta = g.cb * g2, gamma = g.cc * g2 * g2;
+            const float beta = g.cb * g2 * s.gs, gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
             const float* asrc = g.gram + mi.sq_off;
             out = g.poly + mi.sq_off;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int i = min(ibase + r, s.M - 1);
-              v[r] = beta * asrc[(int64_t)i * n + j] + gamma * acc[a][b][4 * grp + r];
+              v[r] = beta * asrc[(int64_t)i * n + j] + gamma * acc[a][b][4 * grp + r] + (i == j ? diag : 0.f);
             }
           }
 #pragma unroll
@@ -428,16 +429,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
             }
           }
         } else {
-          // X' = g (ca X + X P), X read with the same pre-scaling as the product
-          const float* xs = g.xin + mi.ws_off;
+          // X' = X P (the linear term and g are folded into P)
           float* xo = g.xout + mi.ws_off;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int i = ibase + r;
-            if (i < s.M) {
-              const int64_t o = (int64_t)i * s.sr + (int64_t)j * s.sc;
-              xo[o] = s.gs * (g.ca * (s.xscale * xs[o]) + acc[a][b][4 * grp + r]);
-            }
+            if (i < s.M) xo[(int64_t)i * s.sr + (int64_t)j * s.sc] = acc[a][b][4 * grp + r];
           }
         }
       }
