@@ -20,6 +20,7 @@
 
 namespace isoloco {
 
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -531,17 +532,17 @@ __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int 
   const int t = threadIdx.x;
   // Buffer loads: a uniform resource for the operand's matrix, one 32-bit lane
   // offset that is fixed for the whole slab, and the k advance as a scalar
-  // offset (t / 128 is uniform over a wave), so that no per-load address
-  // arithmetic runs on the vector ALU.  The host keeps matrices of these tiles
-  // under 2^29 elements, so every byte offset fits 31 bits.
-  const int kh = __builtin_amdgcn_readfirstlane(t >> 7);
+  // offset, so that no per-load address arithmetic runs on the vector ALU.
+  // The host keeps matrices of these tiles under 2^29 elements, so every byte
+  // offset fits 31 bits.
   const int bytes = 4 * ((op.K - 1) * (int)op.s_k + (op.I - 1) * (int)op.s_i + 1);
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(op.base), (short)0, bytes, kBufferFlags);
-  const int kb = k0 + 16 * kh;
   if (ICONTIG) {
-    // element (k, i) at base + k s_k + i: lanes take consecutive i (coalesced
-    // 4-byte loads)
+    // element (k, i) at base + k s_k + i: thread t holds row i0 + t % 128 and
+    // k = k0 + 16 (t / 128) .. +15; lanes take consecutive i (coalesced 4-byte
+    // loads); t / 128 is uniform over a wave
+    const int kb = k0 + 16 * __builtin_amdgcn_readfirstlane(t >> 7);
     const int vo = 4 * (i0 + (t & 127));
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -550,11 +551,15 @@ __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int 
         r.v[q][e] = __builtin_bit_cast(
             float, __builtin_amdgcn_raw_buffer_load_b32(rs, vo, 4 * (kb + 4 * q + e) * (int)op.s_k, 0));
   } else {
-    // element (k, i) at base + i s_i + k: each lane reads 64 contiguous bytes of its row
-    const int vo = 4 * (i0 + (t & 127)) * (int)op.s_i;
+    // element (k, i) at base + i s_i + k: row mapping -- eight lanes cover the
+    // slab's 128 contiguous bytes of one row, a wave eight rows per load
+    // (thread t: rows i0 + t / 8 + 32 q, k = k0 + 4 (t % 8) .. +3), so that a
+    // load touches 8 cache lines instead of 64
+    const int vo = 4 * ((i0 + (t >> 3)) * (int)op.s_i + 4 * (t & 7));
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      r.v[q] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + 16 * q, 4 * kb, 0));
+      r.v[q] = __builtin_bit_cast(
+          floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo, 4 * (k0 + 32 * q * (int)op.s_i), 0));
   }
 }
 
@@ -588,21 +593,23 @@ __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, S
 // bounds; the fast layouts fix the contiguity of the A and B operands.
 enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2 };
 
+// Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
+// k-contiguous for wide storage (T1).  Poly: A[k][i], always i-contiguous.
+// Update: A = X[i][k] (k-contiguous for T0, i-contiguous for T1), B = P[k][j].
+// k-contiguous interior operands use the row mapping of the registers.
+template <int MODE, int LAYOUT, bool IS_A>
+struct OperandLayout {
+  static constexpr bool icontig =
+      MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? true : (IS_A ? (LAYOUT == kFastT1) : true);
+  static constexpr bool rowmap = LAYOUT != kGeneric && !icontig;
+};
+
 template <int MODE, int LAYOUT, bool IS_A>
 __device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, Slab32& r) {
-  if (LAYOUT == kGeneric) {
-    slab32_load(op, k0, i0, r);
-  } else {
-    // Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
-    // k-contiguous for wide storage (T1).  Poly: A[k][i], always i-contiguous.
-    // Update: A = X[i][k] (k-contiguous for T0, i-contiguous for T1), B = P[k][j].
-    constexpr bool icontig =
-        MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? true : (IS_A ? (LAYOUT == kFastT1) : true);
-    slab32_load_fast<icontig>(op, k0, i0, r);
-  }
+  if (LAYOUT == kGeneric) slab32_load(op, k0, i0, r);
+  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig>(op, k0, i0, r);
 }
 
-typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Split the thread's 16 values into NS bf16 parts, two values per convert,
@@ -631,6 +638,40 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[k
 #pragma unroll
     for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x8*>(&planes[p][i][kb + 8 * half]) = part[p];
   }
+}
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// The same for registers in the row mapping (thread t: rows t / 8 + 32 q,
+// k = 4 (t % 8) .. +3): 8-byte LDS writes.
+template <int NS, bool SCALED = false>
+__device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale = 1.f) {
+  const int t = threadIdx.x;
+  const int i = t >> 3, kb = 4 * (t & 7);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    bf16x4 part[NS];
+#pragma unroll
+    for (int e = 0; e < 4; e += 2) {
+      floatx2 x = {r.v[q][e], r.v[q][e + 1]};
+      if (SCALED) x *= scale;
+#pragma unroll
+      for (int p = 0; p < NS; ++p) {
+        const bf16x2 h = __builtin_convertvector(x, bf16x2);
+        part[p][e] = h[0];
+        part[p][e + 1] = h[1];
+        if (p + 1 < NS) x -= __builtin_convertvector(h, floatx2);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x4*>(&planes[p][i + 32 * q][kb]) = part[p];
+  }
+}
+
+template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED>
+__device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale) {
+  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED>(r, planes, scale);
+  else slab32_store<NS, SCALED>(r, planes, scale);
 }
 
 // One k16 substep of the 64 x 64 wave tile: read the operand fragments of
@@ -709,23 +750,23 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
     Slab32 ra1, rb1;
     load_operand<MODE, LAYOUT, true>(s.A, kat(1), s.i0, ra1);
     load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
-    slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
-    slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+    store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
+    store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
     load_operand<MODE, LAYOUT, true>(s.A, kat(2), s.i0, ra);
     load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
     __syncthreads();
     int sl = 0;
     for (; sl + 2 < nslab; sl += 2) {
       mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
-      slab32_store<NS, SA>(ra1, Ap[1], s.A.scale);
-      slab32_store<NS, SB>(rb1, Bp[1], s.B.scale);
+      store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
       mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
       __syncthreads();
       mfma_substep<NS>(Ap[1], Bp[1], 0, acc);
-      slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
-      slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
       mfma_substep<NS>(Ap[1], Bp[1], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
@@ -735,8 +776,8 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
     int last = 0;
     if (sl + 1 < nslab) {
       mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
-      slab32_store<NS, SA>(ra1, Ap[1], s.A.scale);
-      slab32_store<NS, SB>(rb1, Bp[1], s.B.scale);
+      store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
       mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
       __syncthreads();
       last = 1;
@@ -746,8 +787,8 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   } else {
     for (int sl = 0; sl < nslab; ++sl) {
       __syncthreads();
-      slab32_store<NS, SA>(ra, Ap[0], s.A.scale);
-      slab32_store<NS, SB>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
       __syncthreads();
       const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
       load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
