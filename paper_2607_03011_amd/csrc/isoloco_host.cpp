@@ -214,6 +214,11 @@ std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
 // 8 queues are interleaved into one grid.  Short queues are padded with
 // empty tasks (mat = -1), which return at once.
 constexpr int kXcds = 8;
+// 256 x 256 tiles for the symmetric Gram and polynomial products: off.  With
+// 6 such tiles per 768 x 768 matrix there are too few tasks to fill 256 CUs
+// evenly, and these phases ran slower than on 128 x 128 tiles; the update
+// (9 to 375 tiles per matrix) uses them.
+constexpr bool kBigGram = false;
 
 std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<Task>& in, bool by_slice) {
   struct Group {
@@ -275,6 +280,10 @@ struct TaskListHost {
   std::vector<Task> tasks;
   int seg_off[3] = {0, 0, 0};
   int seg_cnt[3] = {0, 0, 0};
+  int big_off[2] = {0, 0};
+  int big_cnt[2] = {0, 0};
+  int rem_off[3] = {0, 0, 0};
+  int rem_cnt[3] = {0, 0, 0};
 };
 
 struct isoloco_plan_s {
@@ -386,23 +395,34 @@ void plan_matrices(isoloco_plan_s* p) {
 
   // Work lists, longest tasks first, each in three segments (interior tiles of
   // row-major matrices, interior tiles of wide-stored matrices, ragged tiles),
-  // each segment reordered for the XCD round robin of the dispatcher.
-  std::vector<Task> seg[3];
+  // each segment reordered for the XCD round robin of the dispatcher.  Next to
+  // this cover by 128 x 128 tiles, the bf16x3 steps use interior 256 x 256
+  // tiles where a matrix has them and 128 x 128 tiles for the rest.
+  std::vector<Task> seg[3], big[2], rem[3];
   auto flush = [&](TaskListHost& L, bool by_slice) {
     L.tasks.clear();
-    for (int q = 0; q < 3; ++q) {
-      const std::vector<Task> o = xcd_order(p->mats, seg[q], by_slice);
-      L.seg_off[q] = (int)L.tasks.size();
-      L.seg_cnt[q] = (int)o.size();
+    auto append = [&](std::vector<Task>& v, int& off, int& cnt) {
+      const std::vector<Task> o = xcd_order(p->mats, v, by_slice);
+      off = (int)L.tasks.size();
+      cnt = (int)o.size();
       L.tasks.insert(L.tasks.end(), o.begin(), o.end());
-      seg[q].clear();
-    }
+      v.clear();
+    };
+    for (int q = 0; q < 3; ++q) append(seg[q], L.seg_off[q], L.seg_cnt[q]);
+    for (int q = 0; q < 2; ++q) append(big[q], L.big_off[q], L.big_cnt[q]);
+    for (int q = 0; q < 3; ++q) append(rem[q], L.rem_off[q], L.rem_cnt[q]);
   };
   // The interior kernels address a matrix with 32-bit byte offsets: matrices
   // of 2^29 elements or more take the generic kernel.
-  auto put = [&](const MatInfo& M, bool interior, const Task& tk) {
-    const bool fast = interior && M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29);
-    seg[!fast ? 2 : (M.trans ? 1 : 0)].push_back(tk);
+  auto fast_ok = [](const MatInfo& M) { return M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29); };
+  auto segment = [&](const MatInfo& M, bool interior) { return !(interior && fast_ok(M)) ? 2 : (M.trans ? 1 : 0); };
+  // a 128 x 128 tile goes to the full cover and, unless the 256 x 256 tile
+  // (a / 2, b / 2) covers it (that tile is listed once, with its first
+  // 128 x 128 tile), to the remainder
+  auto put = [&](const MatInfo& M, bool interior, bool covered, const Task& tk) {
+    seg[segment(M, interior)].push_back(tk);
+    if (!covered) rem[segment(M, interior)].push_back(tk);
+    else if (tk.tm % 2 == 0 && tk.tn % 2 == 0) big[M.trans ? 1 : 0].push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
   };
   std::vector<int> order(p->mats.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
@@ -411,30 +431,36 @@ void plan_matrices(isoloco_plan_s* p) {
   });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM;
+    const int T = (M.n + kBM - 1) / kBM, T2 = M.n / 256;
     // the Gram matrix is symmetric: tiles on and above the diagonal only
     for (int ks = 0; ks < M.ksplit; ++ks) {
       const int64_t kb = (int64_t)ks * M.kchunk, ke = std::min<int64_t>(M.m, kb + M.kchunk);
+      const bool kin = (ke - kb) % 32 == 0;
       for (int a = 0; a < T; ++a)
         for (int b = a; b < T; ++b)
-          put(M, (b + 1) * kBM <= M.n && (ke - kb) % 32 == 0, Task{mi, a, b, ks});
+          put(M, (b + 1) * kBM <= M.n && kin, kBigGram && fast_ok(M) && kin && b < 2 * T2, Task{mi, a, b, ks});
     }
   }
   flush(p->gram_list, true);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM;
+    const int T = (M.n + kBM - 1) / kBM, T2 = M.n / 256;
+    const bool kin = M.n % 32 == 0;
     for (int a = 0; a < T; ++a)
-      for (int b = a; b < T; ++b) put(M, (b + 1) * kBM <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
+      for (int b = a; b < T; ++b)
+        put(M, (b + 1) * kBM <= M.n && kin, kBigGram && fast_ok(M) && kin && b < 2 * T2, Task{mi, a, b, 0});
   }
   flush(p->poly_list, false);
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
+    const int TM2 = M.m / 256, TN2 = M.n / 256;
+    const bool kin = M.n % 32 == 0;
     for (int a = 0; a < TM; ++a)
       for (int b = 0; b < TN; ++b)
-        put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && M.n % 32 == 0, Task{mi, a, b, 0});
+        put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && kin,
+            fast_ok(M) && kin && a < 2 * TM2 && b < 2 * TN2, Task{mi, a, b, 0});
   }
   flush(p->update_list, false);
   for (size_t i = 0; i < p->mats.size(); ++i)
@@ -480,6 +506,12 @@ DevTables dev_tables(const isoloco_plan_s* p) {
     for (int q = 0; q < 3; ++q) {
       d.seg_off[q] = L.seg_off[q];
       d.seg_cnt[q] = L.seg_cnt[q];
+      d.rem_off[q] = L.rem_off[q];
+      d.rem_cnt[q] = L.rem_cnt[q];
+    }
+    for (int q = 0; q < 2; ++q) {
+      d.big_off[q] = L.big_off[q];
+      d.big_cnt[q] = L.big_cnt[q];
     }
     return d;
   };

@@ -6,13 +6,20 @@
 
 namespace isoloco {
 
-// A task list in three segments: interior tiles of row-major (T0) matrices,
-// interior tiles of wide-stored (T1) matrices, and tiles that touch a ragged
-// edge (any layout, bounds-checked kernel).
+// A task list of 128 x 128 tiles in three segments: interior tiles of
+// row-major (T0) matrices, interior tiles of wide-stored (T1) matrices, and
+// tiles that touch a ragged edge (any layout, bounds-checked kernel).  The
+// same array also holds the cover used by the bf16x3 steps: interior
+// 256 x 256 tiles (T0, T1) plus, in three segments as above, the 128 x 128
+// tiles they leave uncovered.
 struct TaskList {
   const Task* tasks;
   int seg_off[3];
   int seg_cnt[3];
+  int big_off[2];
+  int big_cnt[2];
+  int rem_off[3];
+  int rem_cnt[3];
 };
 
 // Device tables and buffers inside the caller's workspace, plus the host copies

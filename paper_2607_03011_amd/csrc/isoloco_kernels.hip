@@ -324,7 +324,7 @@ struct GemmSetup {
   float gs;      // normalisation g of the first step (1 afterwards)
 };
 
-template <int MODE>
+template <int MODE, int TILE = kBM>
 __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& task) {
   GemmSetup s;
   s.mi = g.mats[task.mat];
@@ -366,32 +366,34 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     s.k_begin = 0;
     s.k_end = n;
   }
-  s.i0 = task.tm * kBM;
-  s.j0 = task.tn * kBN;
+  s.i0 = task.tm * TILE;
+  s.j0 = task.tn * TILE;
   return s;
 }
 
-// Epilogue.  acc[a][b][r] holds C(i, j) with
-//   i = i0 + wm*64 + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32
+// Epilogue.  A wave owns NA x 2 accumulator tiles of 32 x 32: with WNC waves
+// across the block's columns, wm = wave / WNC and wn = wave % WNC,
+// acc[a][b][r] holds C(i, j) with
+//   i = i0 + wm*32*NA + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32
 // (the 32 x 32 accumulator layout of the fp32 and bf16 MFMA instructions).
-template <int MODE>
+template <int MODE, int NA = 2, int WNC = 2>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
-                                              const floatx16 (&acc)[2][2]) {
+                                              const floatx16 (&acc)[NA][2]) {
   const MatInfo& mi = s.mi;
   const int n = mi.n;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WNC, wn = wave % WNC;
   const int jl = lane & 31;
   const int ib = 4 * (lane >> 5);
 #pragma unroll
-  for (int a = 0; a < 2; ++a) {
+  for (int a = 0; a < NA; ++a) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int j = s.j0 + wn * 64 + b * 32 + jl;
       if (j >= s.N) continue;
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
-        const int ibase = s.i0 + wm * 64 + a * 32 + 8 * grp + ib;
+        const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
         if (MODE == kGram || MODE == kPoly) {
           // symmetric n x n result: only tiles with tm <= tn are computed, and an
           // off-diagonal tile also writes its mirror image C(j, i) = C(i, j)
@@ -527,7 +529,9 @@ constexpr int kBufferFlags = 0x00020000;
 // multiply is left out).
 // Interior slab (no bounds checks; the host only routes tiles whose rows,
 // columns and K range are all inside the matrix, with m, n multiples of 4).
-template <bool ICONTIG>
+// ROWS = 128 (256 threads) or 256 (512 threads): the slab is ROWS x 32 and
+// every thread holds 16 of its values.
+template <bool ICONTIG, int ROWS = kBM>
 __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int i0, Slab32& r) {
   const int t = threadIdx.x;
   // Buffer loads: a uniform resource for the operand's matrix, one 32-bit lane
@@ -539,11 +543,11 @@ __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int 
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(op.base), (short)0, bytes, kBufferFlags);
   if (ICONTIG) {
-    // element (k, i) at base + k s_k + i: thread t holds row i0 + t % 128 and
-    // k = k0 + 16 (t / 128) .. +15; lanes take consecutive i (coalesced 4-byte
-    // loads); t / 128 is uniform over a wave
-    const int kb = k0 + 16 * __builtin_amdgcn_readfirstlane(t >> 7);
-    const int vo = 4 * (i0 + (t & 127));
+    // element (k, i) at base + k s_k + i: thread t holds row i0 + t % ROWS and
+    // k = k0 + 16 (t / ROWS) .. +15; lanes take consecutive i (coalesced 4-byte
+    // loads); t / ROWS is uniform over a wave
+    const int kb = k0 + 16 * __builtin_amdgcn_readfirstlane(t / ROWS);
+    const int vo = 4 * (i0 + t % ROWS);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -553,13 +557,13 @@ __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int 
   } else {
     // element (k, i) at base + i s_i + k: row mapping -- eight lanes cover the
     // slab's 128 contiguous bytes of one row, a wave eight rows per load
-    // (thread t: rows i0 + t / 8 + 32 q, k = k0 + 4 (t % 8) .. +3), so that a
-    // load touches 8 cache lines instead of 64
+    // (thread t: rows i0 + t / 8 + (ROWS / 4) q, k = k0 + 4 (t % 8) .. +3), so
+    // that a load touches 8 cache lines instead of 64
     const int vo = 4 * ((i0 + (t >> 3)) * (int)op.s_i + 4 * (t & 7));
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       r.v[q] = __builtin_bit_cast(
-          floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo, 4 * (k0 + 32 * q * (int)op.s_i), 0));
+          floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo, 4 * (k0 + (ROWS / 4) * q * (int)op.s_i), 0));
   }
 }
 
@@ -604,10 +608,11 @@ struct OperandLayout {
   static constexpr bool rowmap = LAYOUT != kGeneric && !icontig;
 };
 
-template <int MODE, int LAYOUT, bool IS_A>
+template <int MODE, int LAYOUT, bool IS_A, int ROWS = kBM>
 __device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, Slab32& r) {
+  static_assert(LAYOUT != kGeneric || ROWS == kBM, "ragged tiles use the 128-row kernel");
   if (LAYOUT == kGeneric) slab32_load(op, k0, i0, r);
-  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig>(op, k0, i0, r);
+  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig, ROWS>(op, k0, i0, r);
 }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -616,10 +621,10 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // and store each part plane as two 16-byte row segments.  SCALED multiplies
 // the values by the operand's scale first (the 1/||Delta||_F of the first
 // polar step; 1 afterwards, when the multiply is left out).
-template <int NS, bool SCALED = false>
-__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale = 1.f) {
+template <int NS, bool SCALED = false, int ROWS = kBM>
+__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale = 1.f) {
   const int t = threadIdx.x;
-  const int i = t & 127, kb = 16 * (t >> 7);
+  const int i = t % ROWS, kb = 16 * (t / ROWS);
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     bf16x8 part[NS];
@@ -642,10 +647,10 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[k
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
-// The same for registers in the row mapping (thread t: rows t / 8 + 32 q,
+// The same for registers in the row mapping (thread t: rows t / 8 + (ROWS / 4) q,
 // k = 4 (t % 8) .. +3): 8-byte LDS writes.
-template <int NS, bool SCALED = false>
-__device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale = 1.f) {
+template <int NS, bool SCALED = false, int ROWS = kBM>
+__device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale = 1.f) {
   const int t = threadIdx.x;
   const int i = t >> 3, kb = 4 * (t & 7);
 #pragma unroll
@@ -664,28 +669,29 @@ __device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*plan
       }
     }
 #pragma unroll
-    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x4*>(&planes[p][i + 32 * q][kb]) = part[p];
+    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x4*>(&planes[p][i + (ROWS / 4) * q][kb]) = part[p];
   }
 }
 
-template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED>
-__device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[kBM][kLdsK], float scale) {
-  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED>(r, planes, scale);
-  else slab32_store<NS, SCALED>(r, planes, scale);
+template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED, int ROWS = kBM>
+__device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale) {
+  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED, ROWS>(r, planes, scale);
+  else slab32_store<NS, SCALED, ROWS>(r, planes, scale);
 }
 
-// One k16 substep of the 64 x 64 wave tile: read the operand fragments of
-// the NS planes from LDS and issue the part products (smallest order first).
-template <int NS>
-__device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[kBM][kLdsK], const __bf16 (*Bp)[kBN][kLdsK],
-                                             int kk, floatx16 (&acc)[2][2]) {
+// One k16 substep of a wave's (32 NA) x 64 tile: read the operand fragments
+// of the NS planes from LDS and issue the part products (smallest order
+// first).  WNC waves span the block's columns (wm = wave / WNC, wn = wave % WNC).
+template <int NS, int NA = 2, int WNC = 2, int ROWS = kBM>
+__device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], const __bf16 (*Bp)[ROWS][kLdsK],
+                                             int kk, floatx16 (&acc)[NA][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WNC, wn = wave % WNC;
   const int kc = kk + 8 * (lane >> 5);
-  bf16x8 av[2][NS], bv[2][NS];
+  bf16x8 av[NA][NS], bv[2][NS];
 #pragma unroll
-  for (int a = 0; a < 2; ++a) {
-    const int row = wm * 64 + a * 32 + (lane & 31);
+  for (int a = 0; a < NA; ++a) {
+    const int row = wm * 32 * NA + a * 32 + (lane & 31);
 #pragma unroll
     for (int p = 0; p < NS; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
   }
@@ -696,7 +702,7 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[kBM][kLdsK], con
     for (int p = 0; p < NS; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
   }
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < NA; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -799,6 +805,63 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   }
   }
   gemm_epilogue<MODE>(g, s, task, acc);
+}
+
+// bf16x3 on 256 x 256 block tiles (interior tiles only): 512 threads in 8
+// waves of 128 x 64 (2 x 4), so that every fp32 operand value staged through
+// LDS feeds twice as many products as on 128 x 128 tiles -- half the global
+// loads, splits, LDS writes and barriers per product.  The two LDS buffers
+// (2 planes x 512 rows x 80 bytes each) take the whole 160 KB of the CU, and
+// one slab is in flight in registers (issued after the split of the previous
+// one, landing during the second half of the current slab's products).
+constexpr int kBig = 256;
+constexpr int kBigThreads = 512;
+
+template <int MODE, int LAYOUT, bool SCALED>
+__global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
+  constexpr int NS = 2;
+  constexpr bool SA = SCALED && MODE != kPoly;
+  constexpr bool SB = SCALED && MODE == kGram;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[2][NS][kBig][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[2][NS][kBig][kLdsK];
+  const Task task = g.tasks[blockIdx.x];
+  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
+  const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
+  floatx16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int nslab = (s.k_end - s.k_begin + kBK2 - 1) / kBK2;
+  if (nslab > 0) {
+    const int klast = s.k_begin + (nslab - 1) * kBK2;
+    auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
+    Slab32 ra, rb;
+    load_operand<MODE, LAYOUT, true, kBig>(s.A, s.k_begin, s.i0, ra);
+    load_operand<MODE, LAYOUT, false, kBig>(s.B, s.k_begin, s.j0, rb);
+    store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
+    store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
+    load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
+    load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
+    __syncthreads();
+    for (int sl = 0; sl + 1 < nslab; ++sl) {
+      const int cur = sl & 1;
+      mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 0, acc);
+      store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
+      mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 16, acc);
+      load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
+      load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
+      __syncthreads();
+    }
+    const int last = (nslab - 1) & 1;
+    mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 0, acc);
+    mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 16, acc);
+  }
+  gemm_epilogue<MODE, 4, 4>(g, s, task, acc);
 }
 
 // Sum of the split-K Gram partials of one matrix, 4 elements per thread.
@@ -972,29 +1035,52 @@ hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStr
 }
 
 template <int MODE, int NS, bool SCALED>
-static void launch_bf16_segments(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
+static void launch_bf16_segments(const Task* tasks, const int* off, const int* cnt, const GemmArgs& g0,
+                                 hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kGemmThreads);
-  if (L.seg_cnt[0]) {
-    g.tasks = L.tasks + L.seg_off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0, SCALED>), dim3(L.seg_cnt[0]), block, 0, st, g);
+  if (cnt[0]) {
+    g.tasks = tasks + off[0];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
   }
-  if (L.seg_cnt[1]) {
-    g.tasks = L.tasks + L.seg_off[1];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1, SCALED>), dim3(L.seg_cnt[1]), block, 0, st, g);
+  if (cnt[1]) {
+    g.tasks = tasks + off[1];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1, SCALED>), dim3(cnt[1]), block, 0, st, g);
   }
-  if (L.seg_cnt[2]) {
-    g.tasks = L.tasks + L.seg_off[2];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric, SCALED>), dim3(L.seg_cnt[2]), block, 0, st, g);
+  if (cnt[2]) {
+    g.tasks = tasks + off[2];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric, SCALED>), dim3(cnt[2]), block, 0, st, g);
   }
+}
+
+// bf16x3: the 256 x 256 interior tiles, then the 128 x 128 tiles left over.
+template <int MODE, bool SCALED>
+static void launch_bf16x3(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
+  GemmArgs g = g0;
+  const dim3 block(kBigThreads);
+  if (L.big_cnt[0]) {
+    g.tasks = L.tasks + L.big_off[0];
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+  }
+  if (L.big_cnt[1]) {
+    g.tasks = L.tasks + L.big_off[1];
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
+  }
+  launch_bf16_segments<MODE, 2, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
 }
 
 // The first step's X operands carry the 1/||Delta||_F pre-scaling (Poly reads
 // only Gram outputs and never does).
 template <int MODE, int NS>
 static void launch_bf16(const TaskList& L, const GemmArgs& g, hipStream_t st) {
-  if (MODE != kPoly && g.first) launch_bf16_segments<MODE, NS, MODE != kPoly>(L, g, st);
-  else launch_bf16_segments<MODE, NS, false>(L, g, st);
+  const bool scaled = MODE != kPoly && g.first;
+  if (NS == 2) {
+    if (scaled) launch_bf16x3<MODE, MODE != kPoly>(L, g, st);
+    else launch_bf16x3<MODE, false>(L, g, st);
+  } else {
+    if (scaled) launch_bf16_segments<MODE, NS, MODE != kPoly>(L.tasks, L.seg_off, L.seg_cnt, g, st);
+    else launch_bf16_segments<MODE, NS, false>(L.tasks, L.seg_off, L.seg_cnt, g, st);
+  }
 }
 
 template <int MODE>

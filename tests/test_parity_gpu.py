@@ -139,6 +139,20 @@ def test_ragged_multi_tile_f32(iso, precision):
     _run_and_compare(iso, _cfg(lay, n, K=3), opts=dict(precision=precision))
 
 
+# Shapes whose bf16x3 steps mix 256 x 256 interior tiles with 128 x 128
+# remainder tiles: interior and ragged strips, tall and wide storage, a Gram
+# whose K range (m = 1000) is not a multiple of 32, and one-tile matrices.
+BIG_MIXED = [(800, 576, KIND_ISO), (576, 800, KIND_ISO), (1000, 512, KIND_ISO), (640, 640, KIND_ISO),
+             (300, 260, KIND_ISO), (512, 1024, KIND_ISO), (256, 256, KIND_ISO), (40, 1, KIND_AVG)]
+
+
+@pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
+def test_big_tiles_with_remainders(iso, precision):
+    from workload import custom_layout
+    lay, n = custom_layout(BIG_MIXED, align=4)
+    _run_and_compare(iso, _cfg(lay, n, K=3), opts=dict(precision=precision))
+
+
 def test_ragged_multi_tile_bf16(iso):
     from workload import custom_layout
     lay, n = custom_layout(RAGGED, align=8)
