@@ -22,7 +22,9 @@ PEAK_FP32_MFMA_TFS = 157.3   # MI355X dense fp32 matrix, TFLOP/s
 PEAK_BF16_MFMA_TFS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
 
 
-# Part products per fp32 product for each precision mode: (first 3 steps, later steps)
+# Part products per fp32 product for each precision mode: (update products of
+# the first 3 steps, every other product).  Mixed runs the early updates in
+# bf16x6 and everything else in bf16x3.
 PARTS = {"mixed": (6, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
 X6_STEPS = 3
 
@@ -44,11 +46,12 @@ def gemm_flops_per_step(layout, stats, check, precision):
             continue
         m, n = max(r, c), min(r, c)
         gram = n * (n + 1) * m
-        step = gram + n * (n + 1) * n + 2 * m * n * n
+        poly = n * (n + 1) * n
+        upd = 2 * m * n * n
         s = st.steps
         e = min(s, X6_STEPS)
-        f += s * step + (gram if check else 0)
-        fm += e * step * early + (s - e) * step * late + (gram * late if check else 0)
+        f += s * (gram + poly + upd) + (gram if check else 0)
+        fm += s * (gram + poly) * late + (e * early + (s - e) * late) * upd + (gram * late if check else 0)
     return f, fm
 
 

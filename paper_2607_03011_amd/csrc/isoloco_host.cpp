@@ -64,17 +64,23 @@ constexpr double kCushion = 0.1;
 // (about 5x the rounding floor of the split-bf16 Gram; the polar factor is then
 // within about half this value of the exact one)
 constexpr float kSwitchTol = 5e-5f;
-// In the mixed precision mode the first kX6Steps steps (where small singular
-// values are still far below 1 and rounding errors in their directions are
-// amplified the most) use bf16x6 products, the later ones bf16x3.
+// In the mixed precision mode the update products of the first kX6Steps steps
+// use bf16x6, everything else bf16x3.  Those early updates X' = X P' carry
+// the large coefficients of the steps that amplify the small singular values
+// (P' holds a I + b A + c A^2 with |a| + |b| + |c| far above |p|), so their
+// rounding in the directions of small singular values is amplified the most;
+// the Gram and polynomial products of the same steps are as accurate in
+// bf16x3 (emulation of the iteration on spectra down to 1e-6: the same error
+// as bf16x6 updates with bf16x6 everywhere, within 5%).
 constexpr int kX6Steps = 3;
+enum Product { kProdGram = 0, kProdPoly = 1, kProdUpdate = 2 };
 
-int step_arith(int precision, int k) {
+int step_arith(int precision, int k, int product) {
   switch (precision) {
     case ISOLOCO_PREC_FP32: return kArithFp32;
     case ISOLOCO_PREC_BF16X3: return kArithBf16x3;
     case ISOLOCO_PREC_BF16X6: return kArithBf16x6;
-    default: return k < kX6Steps ? kArithBf16x6 : kArithBf16x3;
+    default: return (product == kProdUpdate && k < kX6Steps) ? kArithBf16x6 : kArithBf16x3;
   }
 }
 constexpr double kSafety = 1.02;
@@ -762,18 +768,21 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       ps.cc = (float)plan->sched[3 * k + 2];
       ps.first = (k == 0);
       ps.only_active = (k >= Sa);
-      ps.arith = step_arith(plan->opts.precision, k);
+      ps.arith = step_arith(plan->opts.precision, k, kProdGram);
       // the first Gram of the second phase was formed by the switch check
       if (!(two && k == Sa) && (e = gram(ps)) != hipSuccess) return hip_fail(e, "Gram launch");
       if (k == 0 && (e = norm(kNormFirst, 0)) != hipSuccess) return hip_fail(e, "norm launch");
-      if ((e = timed(kPhPoly, [&] { return launch_gemm(t, 1, ps, st); })) != hipSuccess ||
-          (e = timed(kPhUpdate, [&] { return launch_gemm(t, 2, ps, st); })) != hipSuccess)
+      PolarStep pp = ps, pu = ps;
+      pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
+      pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
+      if ((e = timed(kPhPoly, [&] { return launch_gemm(t, 1, pp, st); })) != hipSuccess ||
+          (e = timed(kPhUpdate, [&] { return launch_gemm(t, 2, pu, st); })) != hipSuccess)
         return hip_fail(e, "polar step launch");
       xin = ps.xout;
       if (two && k == Sa - 1) {
         PolarStep pc{};
         pc.xin = xin;
-        pc.arith = step_arith(plan->opts.precision, k + 1);
+        pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
         if ((e = gram(pc)) != hipSuccess || (e = norm(kNormSwitch, 0)) != hipSuccess)
           return hip_fail(e, "switch check launch");
       }
@@ -782,7 +791,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       PolarStep pc{};
       pc.xin = xin;
       pc.only_active = two ? 1 : 0;
-      pc.arith = step_arith(plan->opts.precision, S);
+      pc.arith = step_arith(plan->opts.precision, S, kProdGram);
       if ((e = gram(pc)) != hipSuccess || (e = norm(kNormFinal, pc.only_active)) != hipSuccess)
         return hip_fail(e, "check launch");
     }
