@@ -421,14 +421,22 @@ void plan_matrices(isoloco_plan_s* p) {
   // The interior kernels address a matrix with 32-bit byte offsets: matrices
   // of 2^29 elements or more take the generic kernel.
   auto fast_ok = [](const MatInfo& M) { return M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29); };
-  auto segment = [&](const MatInfo& M, bool interior) { return !(interior && fast_ok(M)) ? 2 : (M.trans ? 1 : 0); };
+  // Interior tiles of wide-stored matrices go to segment 1 of the Gram and
+  // update lists (a launch of their own) and share segment 0 with the
+  // row-major ones in the polynomial list (one launch; the kernel picks the
+  // loaders per task): the choices measured fastest.
+  bool split_layouts = true;
+  auto segment = [&](const MatInfo& M, bool interior) {
+    return !(interior && fast_ok(M)) ? 2 : (split_layouts && M.trans ? 1 : 0);
+  };
   // a 128 x 128 tile goes to the full cover and, unless the 256 x 256 tile
   // (a / 2, b / 2) covers it (that tile is listed once, with its first
   // 128 x 128 tile), to the remainder
   auto put = [&](const MatInfo& M, bool interior, bool covered, const Task& tk) {
     seg[segment(M, interior)].push_back(tk);
     if (!covered) rem[segment(M, interior)].push_back(tk);
-    else if (tk.tm % 2 == 0 && tk.tn % 2 == 0) big[M.trans ? 1 : 0].push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
+    else if (tk.tm % 2 == 0 && tk.tn % 2 == 0)
+      big[split_layouts && M.trans ? 1 : 0].push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
   };
   std::vector<int> order(p->mats.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
@@ -449,6 +457,7 @@ void plan_matrices(isoloco_plan_s* p) {
   }
   flush(p->gram_list, true);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
+  split_layouts = false;
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int T = (M.n + kBM - 1) / kBM, T2 = M.n / 256;
@@ -458,6 +467,7 @@ void plan_matrices(isoloco_plan_s* p) {
         put(M, (b + 1) * kBM <= M.n && kin, kBigGram && fast_ok(M) && kin && b < 2 * T2, Task{mi, a, b, 0});
   }
   flush(p->poly_list, false);
+  split_layouts = true;
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
     const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;

@@ -6,12 +6,12 @@
 
 namespace isoloco {
 
-// A task list of 128 x 128 tiles in three segments: interior tiles of
-// row-major (T0) matrices, interior tiles of wide-stored (T1) matrices, and
-// tiles that touch a ragged edge (any layout, bounds-checked kernel).  The
+// A task list of 128 x 128 tiles in segments: interior tiles (segment 0, both
+// storage orders; the kernel picks the loaders per task; segment 1 is empty)
+// and tiles that touch a ragged edge (segment 2, bounds-checked kernel).  The
 // same array also holds the cover used by the bf16x3 steps: interior
-// 256 x 256 tiles (T0, T1) plus, in three segments as above, the 128 x 128
-// tiles they leave uncovered.
+// 256 x 256 tiles (big segment 0; 1 is empty) plus, in segments as above, the
+// 128 x 128 tiles they leave uncovered.
 struct TaskList {
   const Task* tasks;
   int seg_off[3];

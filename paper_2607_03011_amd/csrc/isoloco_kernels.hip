@@ -595,7 +595,7 @@ __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, S
 
 // Loader selected at compile time: LAYOUT kGeneric uses runtime layout and
 // bounds; the fast layouts fix the contiguity of the A and B operands.
-enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2 };
+enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2, kFastAny = 3 };
 
 // Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
 // k-contiguous for wide storage (T1).  Poly: A[k][i], always i-contiguous.
@@ -720,16 +720,12 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], co
 // interleave the split arithmetic with the matrix products.  bf16x6 (NS = 3)
 // needs 1.5x the LDS per buffer and keeps a single buffer with two barriers.
 // SCALED: the X operands are multiplied by the first step's 1/||Delta||_F.
-template <int MODE, int NS, int LAYOUT, bool SCALED>
-__global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
-  constexpr int NB = NS == 2 ? 2 : 1;
+template <int MODE, int NS, int LAYOUT, bool SCALED, int NB>
+__device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[NS][kBM][kLdsK],
+                                          __bf16 (*Bp)[NS][kBN][kLdsK]) {
   // only X operands carry a scale (Gram: both, Update: A)
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBM][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBN][kLdsK];
-  const Task task = g.tasks[blockIdx.x];
-  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   const GemmSetup s = gemm_setup<MODE>(g, task);
   floatx16 acc[2][2];
 #pragma unroll
@@ -807,6 +803,24 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   gemm_epilogue<MODE>(g, s, task, acc);
 }
 
+// The interior tiles of row-major (T0) and wide-stored (T1) matrices share one
+// launch (kFastAny picks the loaders per task), so that neither layout class
+// forms a launch of its own with a ragged tail.
+template <int MODE, int NS, int LAYOUT, bool SCALED>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
+  constexpr int NB = NS == 2 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBM][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBN][kLdsK];
+  const Task task = g.tasks[blockIdx.x];
+  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
+  if constexpr (LAYOUT == kFastAny) {
+    if (g.mats[task.mat].trans) bf16_tile<MODE, NS, kFastT1, SCALED, NB>(g, task, Ap, Bp);
+    else bf16_tile<MODE, NS, kFastT0, SCALED, NB>(g, task, Ap, Bp);
+  } else {
+    bf16_tile<MODE, NS, LAYOUT, SCALED, NB>(g, task, Ap, Bp);
+  }
+}
+
 // bf16x3 on 256 x 256 block tiles (interior tiles only): 512 threads in 8
 // waves of 128 x 64 (2 x 4), so that every fp32 operand value staged through
 // LDS feeds twice as many products as on 128 x 128 tiles -- half the global
@@ -818,14 +832,11 @@ constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 
 template <int MODE, int LAYOUT, bool SCALED>
-__global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
+__device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[2][kBig][kLdsK],
+                                              __bf16 (*Bp)[2][kBig][kLdsK]) {
   constexpr int NS = 2;
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[2][NS][kBig][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[2][NS][kBig][kLdsK];
-  const Task task = g.tasks[blockIdx.x];
-  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
   floatx16 acc[4][2];
 #pragma unroll
@@ -862,6 +873,20 @@ __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs 
     mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 16, acc);
   }
   gemm_epilogue<MODE, 4, 4>(g, s, task, acc);
+}
+
+template <int MODE, int LAYOUT, bool SCALED>
+__global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[2][2][kBig][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[2][2][kBig][kLdsK];
+  const Task task = g.tasks[blockIdx.x];
+  if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
+  if constexpr (LAYOUT == kFastAny) {
+    if (g.mats[task.mat].trans) bf16_big_tile<MODE, kFastT1, SCALED>(g, task, Ap, Bp);
+    else bf16_big_tile<MODE, kFastT0, SCALED>(g, task, Ap, Bp);
+  } else {
+    bf16_big_tile<MODE, LAYOUT, SCALED>(g, task, Ap, Bp);
+  }
 }
 
 // Sum of the split-K Gram partials of one matrix, 4 elements per thread.
@@ -1039,9 +1064,14 @@ static void launch_bf16_segments(const Task* tasks, const int* off, const int* c
                                  hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kGemmThreads);
-  if (cnt[0]) {
+  // segment 0 holds both storage orders unless segment 1 takes the
+  // wide-stored tiles (then each has a launch of its own)
+  if (cnt[0] && cnt[1]) {
     g.tasks = tasks + off[0];
     hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
+  } else if (cnt[0]) {
+    g.tasks = tasks + off[0];
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastAny, SCALED>), dim3(cnt[0]), block, 0, st, g);
   }
   if (cnt[1]) {
     g.tasks = tasks + off[1];
@@ -1058,9 +1088,12 @@ template <int MODE, bool SCALED>
 static void launch_bf16x3(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kBigThreads);
-  if (L.big_cnt[0]) {
+  if (L.big_cnt[0] && L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[0];
     hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+  } else if (L.big_cnt[0]) {
+    g.tasks = L.tasks + L.big_off[0];
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
   }
   if (L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[1];
