@@ -821,20 +821,21 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   }
 }
 
-// bf16x3 on 256 x 256 block tiles (interior tiles only): 512 threads in 8
-// waves of 128 x 64 (2 x 4), so that every fp32 operand value staged through
-// LDS feeds twice as many products as on 128 x 128 tiles -- half the global
-// loads, splits, LDS writes and barriers per product.  The two LDS buffers
-// (2 planes x 512 rows x 80 bytes each) take the whole 160 KB of the CU, and
-// one slab is in flight in registers (issued after the split of the previous
-// one, landing during the second half of the current slab's products).
+// 256 x 256 block tiles (interior tiles only): 512 threads in 8 waves of
+// 128 x 64 (2 x 4), so that every fp32 operand value staged through LDS
+// feeds twice as many products as on 128 x 128 tiles -- half the global
+// loads, splits, LDS writes and barriers per product.  bf16x3 double-buffers
+// LDS (2 buffers x 2 planes x 512 rows x 80 bytes: the whole 160 KB of the
+// CU) with one slab in flight in registers (issued after the split of the
+// previous one, landing during the second half of the current slab's
+// products); bf16x6 keeps one buffer of 3 planes (120 KB) and two barriers
+// per slab.
 constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 
-template <int MODE, int LAYOUT, bool SCALED>
-__device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[2][kBig][kLdsK],
-                                              __bf16 (*Bp)[2][kBig][kLdsK]) {
-  constexpr int NS = 2;
+template <int MODE, int NS, int LAYOUT, bool SCALED, int NB>
+__device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[NS][kBig][kLdsK],
+                                              __bf16 (*Bp)[NS][kBig][kLdsK]) {
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
   const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
@@ -853,39 +854,53 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
     Slab32 ra, rb;
     load_operand<MODE, LAYOUT, true, kBig>(s.A, s.k_begin, s.i0, ra);
     load_operand<MODE, LAYOUT, false, kBig>(s.B, s.k_begin, s.j0, rb);
-    store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
-    store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
-    load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
-    load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
-    __syncthreads();
-    for (int sl = 0; sl + 1 < nslab; ++sl) {
-      const int cur = sl & 1;
-      mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 0, acc);
-      store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
-      mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 16, acc);
-      load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
-      load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
+    if constexpr (NB == 2) {
+      store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
+      load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
+      load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
       __syncthreads();
+      for (int sl = 0; sl + 1 < nslab; ++sl) {
+        const int cur = sl & 1;
+        mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 0, acc);
+        store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
+        store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
+        mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 16, acc);
+        load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
+        load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
+        __syncthreads();
+      }
+      const int last = (nslab - 1) & 1;
+      mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 0, acc);
+      mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 16, acc);
+    } else {
+      for (int sl = 0; sl < nslab; ++sl) {
+        __syncthreads();
+        store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
+        store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
+        __syncthreads();
+        load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 1), s.i0, ra);
+        load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 1), s.j0, rb);
+        mfma_substep<NS, 4, 4, kBig>(Ap[0], Bp[0], 0, acc);
+        mfma_substep<NS, 4, 4, kBig>(Ap[0], Bp[0], 16, acc);
+      }
     }
-    const int last = (nslab - 1) & 1;
-    mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 0, acc);
-    mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 16, acc);
   }
   gemm_epilogue<MODE, 4, 4>(g, s, task, acc);
 }
 
-template <int MODE, int LAYOUT, bool SCALED>
+template <int MODE, int NS, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[2][2][kBig][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[2][2][kBig][kLdsK];
+  constexpr int NB = NS == 2 ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBig][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBig][kLdsK];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   if constexpr (LAYOUT == kFastAny) {
-    if (g.mats[task.mat].trans) bf16_big_tile<MODE, kFastT1, SCALED>(g, task, Ap, Bp);
-    else bf16_big_tile<MODE, kFastT0, SCALED>(g, task, Ap, Bp);
+    if (g.mats[task.mat].trans) bf16_big_tile<MODE, NS, kFastT1, SCALED, NB>(g, task, Ap, Bp);
+    else bf16_big_tile<MODE, NS, kFastT0, SCALED, NB>(g, task, Ap, Bp);
   } else {
-    bf16_big_tile<MODE, LAYOUT, SCALED>(g, task, Ap, Bp);
+    bf16_big_tile<MODE, NS, LAYOUT, SCALED, NB>(g, task, Ap, Bp);
   }
 }
 
@@ -1083,37 +1098,32 @@ static void launch_bf16_segments(const Task* tasks, const int* off, const int* c
   }
 }
 
-// bf16x3: the 256 x 256 interior tiles, then the 128 x 128 tiles left over.
-template <int MODE, bool SCALED>
-static void launch_bf16x3(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
+// The 256 x 256 interior tiles, then the 128 x 128 tiles left over (for lists
+// without 256 x 256 tiles this is the plain 128 x 128 cover).
+template <int MODE, int NS, bool SCALED>
+static void launch_big_cover(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kBigThreads);
   if (L.big_cnt[0] && L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
   } else if (L.big_cnt[0]) {
     g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
   }
   if (L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[1];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
   }
-  launch_bf16_segments<MODE, 2, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
+  launch_bf16_segments<MODE, NS, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
 }
 
 // The first step's X operands carry the 1/||Delta||_F pre-scaling (Poly reads
 // only Gram outputs and never does).
 template <int MODE, int NS>
 static void launch_bf16(const TaskList& L, const GemmArgs& g, hipStream_t st) {
-  const bool scaled = MODE != kPoly && g.first;
-  if (NS == 2) {
-    if (scaled) launch_bf16x3<MODE, MODE != kPoly>(L, g, st);
-    else launch_bf16x3<MODE, false>(L, g, st);
-  } else {
-    if (scaled) launch_bf16_segments<MODE, NS, MODE != kPoly>(L.tasks, L.seg_off, L.seg_cnt, g, st);
-    else launch_bf16_segments<MODE, NS, false>(L.tasks, L.seg_off, L.seg_cnt, g, st);
-  }
+  if (MODE != kPoly && g.first) launch_big_cover<MODE, NS, MODE != kPoly>(L, g, st);
+  else launch_big_cover<MODE, NS, false>(L, g, st);
 }
 
 template <int MODE>
