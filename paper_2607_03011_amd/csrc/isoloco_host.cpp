@@ -189,7 +189,9 @@ std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
     } else {
       const double ud = u * ((l / u < 0.5) ? kSafety : 1.0);
       const double ld = std::max(l, kCushion * u);
-      if (!remez_quintic(ld / ud, co)) {
+      // (the product kernels divide by the x^5 coefficient: a quintic
+      // without one is replaced as if the exchange had failed)
+      if (!remez_quintic(ld / ud, co) || !(std::fabs(co[2]) > 1e-6 * (std::fabs(co[0]) + std::fabs(co[1])))) {
         co[0] = 15.0 / 8.0;
         co[1] = -10.0 / 8.0;
         co[2] = 3.0 / 8.0;

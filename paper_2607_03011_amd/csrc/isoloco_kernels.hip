@@ -371,6 +371,56 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
   return s;
 }
 
+// Accumulator start values.  Zero, except for the polynomial product, whose
+// epilogue forms P' = g (a I + b g^2 A + c g^4 A^2) = gamma (rho A + A A) +
+// a g I with gamma = c g^5 and rho = b / (c g^2): the accumulators start at
+// rho A(i, j), read here with the first operand slabs in flight, so that the
+// epilogue does not wait on a second read of A.  (The schedule's quintics all
+// have c != 0.)  A is symmetric: A(i, j) is read as the 4 consecutive
+// values A(j, i .. i + 3) that one lane holds in the accumulator layout.
+template <int MODE, int NA = 2, int WNC = 2>
+__device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup& s, floatx16 (&acc)[NA][2]) {
+  if (MODE != kPoly) {
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+    return;
+  }
+  const int n = s.mi.n;
+  // (g = 0 marks a zero or non-finite Delta: P' = 0 then, and rho is kept finite)
+  const float rho = s.gs != 0.f ? g.cb / (g.cc * s.gs * s.gs) : 0.f;
+  const float* A = g.gram + s.mi.sq_off;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WNC, wn = wave % WNC;
+  const bool v4 = (n & 3) == 0;
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int j = s.j0 + wn * 64 + b * 32 + (lane & 31);
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int ib = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + 4 * (lane >> 5);
+        floatx4 v = {0.f, 0.f, 0.f, 0.f};
+        if (j < n) {
+          const float* row = A + (int64_t)j * n + ib;
+          if (v4 && ib + 3 < n) {
+            v = *reinterpret_cast<const floatx4*>(row);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (ib + r < n) v[r] = row[r];
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[a][b][4 * grp + r] = rho * v[r];
+      }
+    }
+}
+
 // Epilogue.  A wave owns NA x 2 accumulator tiles of 32 x 32: with WNC waves
 // across the block's columns, wm = wave / WNC and wn = wave % WNC,
 // acc[a][b][r] holds C(i, j) with
@@ -405,15 +455,15 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
             for (int r = 0; r < 4; ++r) v[r] = acc[a][b][4 * grp + r];
           } else {
             // P = g (ca I + cb g^2 A + cc g^4 A^2)  (g = 1 after the first
-            // step), so that the update is the plain product X' = X P
+            // step), so that the update is the plain product X' = X P; the
+            // accumulators hold rho A + A A (see gemm_acc_init)
             const float g2 = s.gs * s.gs;
-            const float beta = g.cb * g2 * s.gs, gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
-            const float* asrc = g.gram + mi.sq_off;
+            const float gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
             out = g.poly + mi.sq_off;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int i = min(ibase + r, s.M - 1);
-              v[r] = beta * asrc[(int64_t)i * n + j] + gamma * acc[a][b][4 * grp + r] + (i == j ? diag : 0.f);
+              const int i = ibase + r;
+              v[r] = gamma * acc[a][b][4 * grp + r] + (i == j ? diag : 0.f);
             }
           }
 #pragma unroll
@@ -456,12 +506,7 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   floatx16 acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+  gemm_acc_init<MODE>(g, s, acc);
 
   SlabRegs ra, rb;
   slab_load(s.A, s.k_begin, s.i0, ra);
@@ -728,12 +773,7 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
   constexpr bool SB = SCALED && MODE == kGram;
   const GemmSetup s = gemm_setup<MODE>(g, task);
   floatx16 acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+  gemm_acc_init<MODE>(g, s, acc);
 
   const int nslab = (s.k_end - s.k_begin + kBK2 - 1) / kBK2;
   const int klast = s.k_begin + (nslab - 1) * kBK2;
@@ -840,12 +880,7 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
   constexpr bool SB = SCALED && MODE == kGram;
   const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
   floatx16 acc[4][2];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+  gemm_acc_init<MODE, 4, 4>(g, s, acc);
 
   const int nslab = (s.k_end - s.k_begin + kBK2 - 1) / kBK2;
   if (nslab > 0) {

@@ -119,9 +119,11 @@ def test_schedule_converges_on_interval(ell0, tol):
     x = np.concatenate([np.geomspace(ell0, 1.0, 200001), np.linspace(ell0, 1.0, 200001)])
     y = _compose(sched, x)
     assert np.all(np.abs(y - 1.0) <= 1.01 * tol), (len(sched), np.abs(y - 1).max())
-    # every step is an odd polynomial that keeps small values positive and growing
+    # every step is an odd polynomial that keeps small values positive and
+    # growing, with a nonzero x^5 coefficient (the polynomial kernel divides by it)
     for a, b, c in sched:
         assert a > 1.0
+        assert abs(c) > 1e-6 * (abs(a) + abs(b))
 
 
 @pytest.mark.parametrize("ell_fast", [1e-4, 1e-2])
