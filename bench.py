@@ -9,6 +9,8 @@ HBM.  Prints one JSON line.
     python bench.py [--steps 20] [--warmup 3] [--workload 2] [--no-cpu-baseline]
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -53,6 +55,43 @@ def gemm_flops_per_step(layout, stats, check, precision):
         f += s * (gram + poly + upd) + (gram if check else 0)
         fm += s * (gram + poly) * late + (e * early + (s - e) * late) * upd + (gram * late if check else 0)
     return f, fm
+
+
+def gemm_bytes_per_step(layout, stats):
+    """Algorithmic HBM bytes of the batched products of one outer step: per
+    polar step of an m x n matrix (m >= n) the Gram reads X and writes A
+    (4mn + 4n^2; a split-K Gram also writes and re-reads its slices), the
+    polynomial reads A and writes P (8n^2), the update reads X and P and
+    writes X' (8mn + 4n^2); s steps form s + 1 Grams."""
+    b = 0
+    for (_, r, c, kind), st in zip(layout, stats):
+        if kind != 0:
+            continue
+        m, n = max(r, c), min(r, c)
+        s = st.steps
+        b += (s + 1) * (4 * m * n + 4 * n * n) + s * (8 * n * n) + s * (8 * m * n + 4 * n * n)
+    return b
+
+
+# HBM traffic measured with rocprofv3 (FETCH_SIZE x 2.0 + WRITE_SIZE, calibrated on a
+# device copy; summaries in profiles/) for the default workload and precision.  It is
+# reported only while the kernel and planner sources are the ones it was measured on.
+MEASURED_TRAFFIC = {
+    "sources_sha256": "74bbb1ef1332230a65dbad6f4c01ecffbb861e48bb8e796c6e71fc57178fb4f6",
+    "workload": 2, "precision": "mixed",
+    "gemm_bytes_per_step": 34.89e9, "reduce_bytes_per_launch": 7.891e9, "finish_bytes_per_launch": 2.194e9,
+}
+
+
+def sources_sha256():
+    root = os.path.dirname(os.path.abspath(__file__))
+    files = sorted(glob.glob(os.path.join(root, "paper_2607_03011_amd", "csrc", "*"))) + \
+        [os.path.join(root, "include", "isoloco.h")]
+    h = hashlib.sha256()
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def reduce_bytes(layout, n_elems, K, wbytes):
@@ -221,6 +260,10 @@ def main():
     red_gbs = rbytes / (per["reduce_ms"] * 1e-3) / 1e9
     fbytes = finish_bytes(cfg.layout)
     fin_gbs = fbytes / (per["finish_ms"] * 1e-3) / 1e9
+    gbytes = gemm_bytes_per_step(cfg.layout, st)
+    mt = MEASURED_TRAFFIC
+    measured = (mt["sources_sha256"] == sources_sha256() and mt["workload"] == args.workload
+                and mt["precision"] == args.precision)
 
     out = {
         "metric": "ms per IsoLoCo outer step",
@@ -241,16 +284,21 @@ def main():
                    "polar_steps": n_polar, "short_phase_steps": n_short, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
         "roofline": {"bound": "mfma", "kernel": "gemm_%s_kernel (Gram, polynomial and update products)" %
                      ("f32" if args.precision == "fp32" else "bf16"), "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(gemm_tfs / peak, 4), "traffic": None,
+                     "frac": round(gemm_tfs / peak, 4),
+                     "traffic": mt["gemm_bytes_per_step"] if measured else None,
+                     "traffic_unit": "HBM bytes per step over all product launches",
+                     "algorithmic_bytes_per_step": gbytes,
                      "mfma_flops_per_step": mfma_flops, "fp32_equivalent_flops_per_step": flops,
                      "fp32_equivalent_tflops": round(flops / (gemm_ms * 1e-3) / 1e12, 3),
                      "ms_per_step": round(gemm_ms, 4),
                      "launches_per_step": launches["gemm"] // args.steps},
         "roofline_reduce": {"bound": "hbm", "kernel": "reduce_kernel", "achieved": round(red_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(red_gbs / PEAK_HBM_GBS, 4),
-                            "traffic": None, "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4)},
+                            "traffic": mt["reduce_bytes_per_launch"] if measured else None,
+                            "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4)},
         "roofline_finish": {"bound": "hbm", "kernel": "finish_kernel", "achieved": round(fin_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(fin_gbs / PEAK_HBM_GBS, 4),
+                            "traffic": mt["finish_bytes_per_launch"] if measured else None,
                             "bytes_per_launch": fbytes, "ms": round(per["finish_ms"], 4)},
         "phases_ms": {k: round(v, 4) for k, v in per.items()},
         "input_restore_ms": round(restore_ms, 4),
