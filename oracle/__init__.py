@@ -15,7 +15,11 @@ Contents
                  pseudo-gradient, averaged as in Algorithm 2), the isotropic
                  correction of every exactly-2-D tensor (Algorithm 2's SVD
                  branch, i.e. Iso-C of Section 2.2), and Nesterov momentum
-                 (Algorithm 2's last three assignments).
+                 (Algorithm 2's last three assignments); and the variants
+                 the paper studies: the fast five-step Newton-Schulz with the
+                 RMS scale (Section 4.3), Muon's spectral scale (Appendix B),
+                 standard momentum and correcting the momentum update
+                 instead of the pseudo-gradient (Section 4.5).
 
 Every function is pinned by ``tests/test_oracle_pins.py`` against values fixed
 by the mathematics (closed forms, invariants, library routines, brute force)
@@ -25,9 +29,17 @@ behaviour on inputs whose smallest singular value is below float64 resolution
 """
 from .jacobi import jacobi_svd, polar_factor  # noqa: F401
 from .isoloco_step import (  # noqa: F401
+    NS5_COEFFS,
+    NS5_STEPS,
+    VARIANT_DEFAULT,
+    correct_matrix,
     decode_bf16,
-    pseudo_gradient_mean,
+    heavy_ball_update,
     iso_correct,
     nesterov_update,
+    newton_schulz5,
     outer_step,
+    pseudo_gradient_mean,
+    rms_singular_value,
+    spectral_scale,
 )

@@ -371,3 +371,181 @@ def test_planted_mistake_is_caught(monkeypatch, mistake):
         monkeypatch.setattr(oracle, "iso_correct", iso)
     assert not _pins_pass(), "planted mistake %s was not caught" % mistake
     del orig_nest
+
+
+# --- variants: the fast Newton-Schulz path, the scales, momentum, target -----
+
+
+def _svd_of_spectrum(rows, cols, s, rng):
+    """U diag(s) V^T with random orthonormal U (rows x r) and V (cols x r)."""
+    r = min(rows, cols)
+    U, _ = np.linalg.qr(rng.standard_normal((rows, r)))
+    V, _ = np.linalg.qr(rng.standard_normal((cols, r)))
+    return (U * s) @ V.T, U, V
+
+
+@pytest.mark.parametrize("shape", [(7, 4), (4, 7), (5, 5)])
+def test_newton_schulz5_acts_on_singular_values(shape):
+    # NS is an odd matrix polynomial: NS(U diag(s) V^T) = U diag(p^5(s / ||s||)) V^T,
+    # with p the scalar quintic -- checked against the scalar recursion
+    rng = np.random.default_rng(11)
+    r = min(shape)
+    s = np.geomspace(1.0, 1e-3, r)
+    M, U, V = _svd_of_spectrum(shape[0], shape[1], s, rng)
+    a, b, c = oracle.NS5_COEFFS
+    x = s / np.linalg.norm(s)
+    for _ in range(5):
+        x = a * x + b * x ** 3 + c * x ** 5
+    np.testing.assert_allclose(oracle.newton_schulz5(M), (U * x) @ V.T, atol=1e-13)
+    assert np.all(oracle.newton_schulz5(np.zeros(shape)) == 0)
+
+
+def test_newton_schulz5_coefficients_and_range():
+    # the named quintic: p(1) = a + b + c = 0.701, and five steps map singular
+    # values in [3e-3, 1] (relative to the Frobenius norm) into [0.68, 1.21]
+    assert oracle.NS5_COEFFS == (3.4445, -4.7750, 2.0315) and oracle.NS5_STEPS == 5
+    a, b, c = oracle.NS5_COEFFS
+    assert abs(a + b + c - 0.701) < 1e-12
+    x = np.linspace(3e-3, 1.0, 10001)
+    for _ in range(5):
+        x = a * x + b * x ** 3 + c * x ** 5
+    assert 0.68 < x.min() and x.max() < 1.21
+
+
+def test_rms_at_least_mean_equal_iff_flat():
+    rng = np.random.default_rng(12)
+    M = rng.standard_normal((9, 6))
+    s = np.sqrt(np.linalg.eigvalsh(M.T @ M))          # brute-force singular values
+    rms = oracle.rms_singular_value(M)
+    np.testing.assert_allclose(rms, np.sqrt(np.mean(s ** 2)), rtol=1e-13)
+    assert rms > s.mean() * (1 + 1e-3)
+    Q0, _ = np.linalg.qr(rng.standard_normal((9, 6)))
+    F = 2.5 * Q0                                      # flat spectrum: equality
+    np.testing.assert_allclose(oracle.rms_singular_value(F), oracle.iso_correct(F)[1], rtol=1e-12)
+
+
+def test_scales_of_correct_matrix():
+    rng = np.random.default_rng(13)
+    M = rng.standard_normal((6, 4))
+    D, f, Q = oracle.correct_matrix(M, 2.0, "svd", "spectral")
+    assert f == np.sqrt(6 / 4)
+    np.testing.assert_allclose(D, 2.0 * np.sqrt(1.5) * polar_factor(M)[0], atol=1e-13)
+    D, f, Q = oracle.correct_matrix(M, 1.0, "svd", "rms")
+    np.testing.assert_allclose(np.linalg.norm(D), np.linalg.norm(M), rtol=1e-12)   # rms * sqrt(r) = ||M||_F
+    D, f, Q = oracle.correct_matrix(M, 1.0, "ns5", "rms")
+    np.testing.assert_allclose(Q, oracle.newton_schulz5(M), atol=0)
+    with pytest.raises(ValueError):
+        oracle.correct_matrix(M, 1.0, "ns5", "mean")
+
+
+def test_heavy_ball_matches_torch_sgd():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(14)
+    n, lr, mu = 7, 0.7, 0.6
+    theta = rng.standard_normal(n)
+    p = torch.nn.Parameter(torch.tensor(theta.copy(), dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=lr, momentum=mu, nesterov=False, dampening=0.0)
+    B = np.zeros(n)
+    th = theta.copy()
+    for t in range(5):
+        D = rng.standard_normal(n)
+        p.grad = torch.tensor(D, dtype=torch.float64)
+        opt.step()
+        th, B = oracle.heavy_ball_update(th, B, D, lr, mu)
+        np.testing.assert_allclose(th, p.detach().numpy(), rtol=1e-14, atol=1e-14)
+
+
+@pytest.mark.parametrize("momentum", ["nesterov", "heavy_ball"])
+def test_correcting_the_update_first_step_and_mu_zero(momentum):
+    # With B = 0: B_new = Delta (uncorrected) and the step is the correction of
+    # (1 + mu) Delta (Nesterov) or of Delta (heavy ball), i.e. by homogeneity
+    # (1 + mu) iso(Delta) or iso(Delta).  With mu = 0 both targets coincide.
+    rng = np.random.default_rng(15)
+    lay = [(0, 5, 3, step.KIND_ISO), (15, 4, 1, step.KIND_AVG)]
+    theta = rng.standard_normal(19)
+    ws = [theta - rng.standard_normal(19) for _ in range(3)]
+    B0 = np.zeros(19)
+    lr, mu = 0.7, 0.9
+    v = {"target": "update", "momentum": momentum}
+    th, B, info = oracle.outer_step(lay, theta, ws, B0, 1.0, lr, mu, variant=v)
+    delta = oracle.pseudo_gradient_mean(theta, ws)
+    np.testing.assert_allclose(B[:15], delta[:15], atol=1e-15)
+    iso = oracle.iso_correct(delta[:15].reshape(5, 3))[0].reshape(-1)
+    f = (1 + mu) if momentum == "nesterov" else 1.0
+    np.testing.assert_allclose(th[:15], theta[:15] - lr * f * iso, atol=1e-13)
+    th0, B0n, _ = oracle.outer_step(lay, theta, ws, B0, 1.0, lr, 0.0, variant=v)
+    th1, B1n, _ = oracle.outer_step(lay, theta, ws, B0, 1.0, lr, 0.0, variant={"momentum": momentum})
+    np.testing.assert_allclose(th0, th1, atol=1e-14)
+
+
+def test_fast_variant_on_a_flat_spectrum_is_ns5_times_scale():
+    # flat spectrum c Q0: RMS = mean = c and NS5(c Q0) = p^5(1/sqrt(r)) Q0
+    rng = np.random.default_rng(16)
+    Q0, _ = np.linalg.qr(rng.standard_normal((8, 5)))
+    c = 0.3
+    a, b, cc = oracle.NS5_COEFFS
+    x = 1 / np.sqrt(5)
+    for _ in range(5):
+        x = a * x + b * x ** 3 + cc * x ** 5
+    D, f, Q = oracle.correct_matrix(c * Q0, 1.5, "ns5", "rms")
+    np.testing.assert_allclose(f, c, rtol=1e-13)
+    np.testing.assert_allclose(D, 1.5 * c * x * Q0, atol=1e-13)
+
+
+def _variant_pins_pass():
+    try:
+        test_newton_schulz5_acts_on_singular_values((7, 4))
+        test_rms_at_least_mean_equal_iff_flat()
+        test_heavy_ball_matches_torch_sgd()
+        test_fast_variant_on_a_flat_spectrum_is_ns5_times_scale()
+        test_correcting_the_update_first_step_and_mu_zero("nesterov")
+    except AssertionError:
+        return False
+    return True
+
+
+def test_variant_pins_pass_unpatched():
+    assert _variant_pins_pass()
+
+
+@pytest.mark.parametrize("mistake", ["ns5_no_normalise", "ns5_transposed_gram", "rms_over_r",
+                                     "heavy_ball_nesterov_form", "heavy_ball_old_B"])
+def test_planted_variant_mistake_is_caught(monkeypatch, mistake):
+    if mistake == "ns5_no_normalise":
+        def ns(M, coeffs=step.NS5_COEFFS, steps=step.NS5_STEPS):
+            a, b, c = coeffs
+            X = np.asarray(M, dtype=np.float64)
+            for _ in range(steps):
+                A = X.T @ X
+                X = a * X + b * (X @ A) + c * (X @ (A @ A))
+            return X
+        monkeypatch.setattr(step, "newton_schulz5", ns)
+        monkeypatch.setattr(oracle, "newton_schulz5", ns)
+    elif mistake == "ns5_transposed_gram":
+        def ns(M, coeffs=step.NS5_COEFFS, steps=step.NS5_STEPS):
+            a, b, c = coeffs
+            M = np.asarray(M, dtype=np.float64)
+            X = M / np.linalg.norm(M)
+            for _ in range(steps):
+                A = X @ X.T                      # wrong side: only defined for square X
+                if A.shape[0] != X.shape[1]:
+                    raise AssertionError("shape")
+                X = a * X + b * (X @ A) + c * (X @ (A @ A))
+            return X
+        monkeypatch.setattr(step, "newton_schulz5", ns)
+        monkeypatch.setattr(oracle, "newton_schulz5", ns)
+    elif mistake == "rms_over_r":
+        def rms(M):
+            M = np.asarray(M, dtype=np.float64)
+            return float(np.linalg.norm(M)) / min(M.shape)
+        monkeypatch.setattr(step, "rms_singular_value", rms)
+        monkeypatch.setattr(oracle, "rms_singular_value", rms)
+    elif mistake == "heavy_ball_nesterov_form":
+        monkeypatch.setattr(step, "heavy_ball_update", step.nesterov_update)
+        monkeypatch.setattr(oracle, "heavy_ball_update", step.nesterov_update)
+    elif mistake == "heavy_ball_old_B":
+        def hb(theta, B, D, lr, mu):
+            return theta - lr * (mu * B), mu * B + D
+        monkeypatch.setattr(step, "heavy_ball_update", hb)
+        monkeypatch.setattr(oracle, "heavy_ball_update", hb)
+    assert not _variant_pins_pass()
