@@ -111,7 +111,7 @@ def finish_bytes(layout):
     return sum(20 * r * c for (_, r, c, kind) in layout if kind == 0)
 
 
-def cpu_baseline(cfg, theta, workers, mom, budget_s):
+def cpu_baseline(cfg, theta, workers, mom, budget_s, variant=None):
     """The float64 oracle timed on the host on a bounded sample of the step:
     all 1-D tensors plus one tensor of each 2-D shape, extrapolated to the whole
     step by the count of each shape."""
@@ -136,7 +136,8 @@ def cpu_baseline(cfg, theta, workers, mom, budget_s):
             off, r, c, kind = cfg.layout[i]
             sl = slice(off, off + r * c)
             ws = [w for w in workers[:, sl].cpu().numpy()]
-            oracle.outer_step([(0, r, c, kind)], th[sl], ws, mo[sl], cfg.alpha, cfg.outer_lr, cfg.mu)
+            oracle.outer_step([(0, r, c, kind)], th[sl], ws, mo[sl], cfg.alpha, cfg.outer_lr, cfg.mu,
+                              variant=variant)
         dt = time.time() - t0
         total += dt * (len(idx) / len(sel))
         timed.append("%s x%d" % ("1-D" if key == ("1d",) else "%dx%d" % key[:2], len(sel)))
@@ -145,9 +146,11 @@ def cpu_baseline(cfg, theta, workers, mom, budget_s):
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": total * 1e3, "unit": "ms per outer step (extrapolated)",
             "cores": threads if J.BACKEND == "c" else 1, "kind": "oracle",
-            "sample": "float64 oracle (one-sided Jacobi SVD, %s sweeps) on %s of the workload's "
+            "sample": "float64 oracle (%s) on %s of the workload's "
                       "tensors, each shape's time scaled by its count; host has %d cores" %
-                      (J.BACKEND, ", ".join(timed), len(os.sched_getaffinity(0)))}
+                      ("five Newton-Schulz steps in numpy" if variant else
+                       "one-sided Jacobi SVD, %s sweeps" % J.BACKEND, ", ".join(timed),
+                       len(os.sched_getaffinity(0)))}
 
 
 def main():
@@ -163,6 +166,9 @@ def main():
                     help="arithmetic of the polar iteration's matrix products")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (reference for HBM counters)")
+    ap.add_argument("--variant", choices=["exact", "fast"], default="exact",
+                    help="exact: Algorithm 2 (converged polar factor, mean singular value); fast: "
+                         "Section 4.3 (five Newton-Schulz steps, RMS of the singular values)")
     ap.add_argument("--ell-fast", type=float, default=0.0,
                     help="short-schedule bound (0: library default; negative: one phase)")
     args = ap.parse_args()
@@ -187,7 +193,8 @@ def main():
     theta0 = theta.clone()
     prec = {"mixed": iso.ISOLOCO_PREC_MIXED, "bf16x3": iso.ISOLOCO_PREC_BF16X3,
             "bf16x6": iso.ISOLOCO_PREC_BF16X6, "fp32": iso.ISOLOCO_PREC_FP32}[args.precision]
-    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast),
+    vopts = dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS) if args.variant == "fast" else {}
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, **vopts),
                            device=dev)
     sched, n_short = plan.schedule_split()
     n_polar = len(sched)
@@ -263,7 +270,7 @@ def main():
     gbytes = gemm_bytes_per_step(cfg.layout, st)
     mt = MEASURED_TRAFFIC
     measured = (mt["sources_sha256"] == sources_sha256() and mt["workload"] == args.workload
-                and mt["precision"] == args.precision)
+                and mt["precision"] == args.precision and args.variant == "exact")
 
     out = {
         "metric": "ms per IsoLoCo outer step",
@@ -281,6 +288,7 @@ def main():
                 "every step restores theta and B = 0 so that it sees fresh pseudo-gradients",
         "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
                    "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
+                   "variant": args.variant,
                    "polar_steps": n_polar, "short_phase_steps": n_short, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
         "roofline": {"bound": "mfma", "kernel": "gemm_%s_kernel (Gram, polynomial and update products)" %
                      ("f32" if args.precision == "fp32" else "bf16"), "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
@@ -306,7 +314,8 @@ def main():
         "matrices_by_steps": {str(k): v for k, v in sorted(steps_hist.items())},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget,
+                                           {"orth": "ns5", "scale": "rms"} if args.variant == "fast" else None)
     plan.close()
     print(json.dumps(out), flush=True)
 

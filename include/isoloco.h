@@ -90,11 +90,30 @@ typedef struct {
                         products split every fp32 operand into 2 (bf16x3: 3 bf16 MFMA
                         products, about 2^-16 relative error) or 3 (bf16x6: 6 products,
                         about fp32 accuracy) bfloat16 parts and accumulate in fp32.
-                        MIXED (default): bf16x6 for the first 3 steps, then bf16x3       */
+                        MIXED (default): bf16x6 for the update products of the first
+                        3 steps, bf16x3 for every other product                          */
   float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
                         whose Q^T Q is then the identity to 5e-5 stops there, the others run the
                         continuation that reaches [ell0, 1] (default 1e-4; a negative value
                         runs the single schedule for [ell0, 1])                                */
+  /* Variants of the step that the paper studies (all 0: Algorithm 2). */
+  int32_t orth;      /* ISOLOCO_ORTH_POLAR: Q = U V^T, the converged polar factor (Algorithm 2);
+                        ISOLOCO_ORTH_NS5: the fast variant's five Newton-Schulz steps of the
+                        Muon quintic (3.4445, -4.7750, 2.0315) on Delta / ||Delta||_F
+                        (Section 4.3); ell0, tol, ell_fast do not apply, and the residual
+                        of check is reported without the not-converged flag                */
+  int32_t scale;     /* ISOLOCO_SCALE_MEAN: sigma_bar = <Q, Delta>_F / r, the mean singular
+                        value (Algorithm 2; needs ORTH_POLAR); ISOLOCO_SCALE_RMS:
+                        ||Delta||_F / sqrt(r) (Section 4.3); ISOLOCO_SCALE_SPECTRAL:
+                        sqrt(rows / cols), Muon's sqrt(fan_out / fan_in) (Appendix B)      */
+  int32_t momentum;  /* ISOLOCO_MOMENTUM_NESTEROV: B <- mu B + D, theta <- theta - lr (D + mu B)
+                        (Algorithm 2); ISOLOCO_MOMENTUM_HEAVY_BALL: B <- mu B + D,
+                        theta <- theta - lr B (Section 4.5's ablation)                      */
+  int32_t target;    /* ISOLOCO_TARGET_DELTA: correct Delta, then the momentum step
+                        (Algorithm 2); ISOLOCO_TARGET_UPDATE: B <- mu B + Delta first, then
+                        correct the update (Delta + mu B, or B with HEAVY_BALL) and step
+                        theta <- theta - lr D (Section 4.5's ablation).  AVG tensors always
+                        take the uncorrected step of the chosen momentum                   */
 } isoloco_options;
 
 #define ISOLOCO_PREC_MIXED 0
@@ -102,9 +121,20 @@ typedef struct {
 #define ISOLOCO_PREC_BF16X3 2
 #define ISOLOCO_PREC_BF16X6 3
 
+#define ISOLOCO_ORTH_POLAR 0
+#define ISOLOCO_ORTH_NS5 1
+#define ISOLOCO_SCALE_MEAN 0
+#define ISOLOCO_SCALE_RMS 1
+#define ISOLOCO_SCALE_SPECTRAL 2
+#define ISOLOCO_MOMENTUM_NESTEROV 0
+#define ISOLOCO_MOMENTUM_HEAVY_BALL 1
+#define ISOLOCO_TARGET_DELTA 0
+#define ISOLOCO_TARGET_UPDATE 1
+
 /* Per-tensor results of the last isoloco_aggregate() on a plan. */
 typedef struct {
-  float sigma_bar;  /* mean singular value of Delta_l (ISO tensors; 0 for AVG)            */
+  float sigma_bar;  /* the scale of the correction (ISO tensors; 0 for AVG): the mean
+                       singular value of Delta_l by default, else as the scale option says */
   float fro_norm;   /* ||Delta_l||_F                                                        */
   float orth_resid; /* ||Q^T Q - I||_F / sqrt(r) on the short side (ISO, if checked; else -1) */
   int32_t steps;    /* polar iteration steps taken (ISO tensors): the short schedule's length

@@ -28,6 +28,15 @@ ISOLOCO_PREC_MIXED = 0
 ISOLOCO_PREC_FP32 = 1
 ISOLOCO_PREC_BF16X3 = 2
 ISOLOCO_PREC_BF16X6 = 3
+ISOLOCO_ORTH_POLAR = 0
+ISOLOCO_ORTH_NS5 = 1
+ISOLOCO_SCALE_MEAN = 0
+ISOLOCO_SCALE_RMS = 1
+ISOLOCO_SCALE_SPECTRAL = 2
+ISOLOCO_MOMENTUM_NESTEROV = 0
+ISOLOCO_MOMENTUM_HEAVY_BALL = 1
+ISOLOCO_TARGET_DELTA = 0
+ISOLOCO_TARGET_UPDATE = 1
 ISOLOCO_FLAG_NONFINITE = 1
 ISOLOCO_FLAG_ZERO = 2
 ISOLOCO_FLAG_NOT_CONVERGED = 4
@@ -46,7 +55,9 @@ class isoloco_tensor(ctypes.Structure):
 
 class isoloco_options(ctypes.Structure):
     _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
-                ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float)]
+                ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float),
+                ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
+                ("target", ctypes.c_int32)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):

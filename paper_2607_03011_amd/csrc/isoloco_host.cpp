@@ -84,6 +84,10 @@ int step_arith(int precision, int k, int product) {
   }
 }
 constexpr double kSafety = 1.02;
+// The fast variant's iteration: the quintic of the Muon optimizer's reference
+// implementation, p(x) = 3.4445 x - 4.7750 x^3 + 2.0315 x^5, five times.
+constexpr double kNs5Coeffs[3] = {3.4445, -4.7750, 2.0315};
+constexpr int kNs5Steps = 5;
 
 bool solve4(double M[4][5], double out[4]) {
   for (int col = 0; col < 4; ++col) {
@@ -593,6 +597,17 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.check != 1 && o.check != -1) return fail(ISOLOCO_ERR_INVALID_ARG, "check must be 1 or -1");
   if (o.precision < ISOLOCO_PREC_MIXED || o.precision > ISOLOCO_PREC_BF16X6)
     return fail(ISOLOCO_ERR_INVALID_ARG, "unknown precision %d", o.precision);
+  if (o.orth < ISOLOCO_ORTH_POLAR || o.orth > ISOLOCO_ORTH_NS5)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown orth %d", o.orth);
+  if (o.scale < ISOLOCO_SCALE_MEAN || o.scale > ISOLOCO_SCALE_SPECTRAL)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown scale %d", o.scale);
+  if (o.momentum < ISOLOCO_MOMENTUM_NESTEROV || o.momentum > ISOLOCO_MOMENTUM_HEAVY_BALL)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown momentum %d", o.momentum);
+  if (o.target < ISOLOCO_TARGET_DELTA || o.target > ISOLOCO_TARGET_UPDATE)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown target %d", o.target);
+  if (o.orth == ISOLOCO_ORTH_NS5 && o.scale == ISOLOCO_SCALE_MEAN)
+    return fail(ISOLOCO_ERR_INVALID_ARG,
+                "the Newton-Schulz variant gives no singular values: use SCALE_RMS or SCALE_SPECTRAL");
 
   std::vector<std::pair<int64_t, int64_t>> spans;
   for (int32_t i = 0; i < n_tensors; ++i) {
@@ -626,7 +641,13 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     // Two phases: a short schedule that assumes sigma_min >= ell_fast, after
     // which every matrix whose Q^T Q is already the identity stops; the others
     // continue with the schedule for what the short one made of [ell0, 1].
-    if (o.ell_fast > o.ell0) {
+    if (o.orth == ISOLOCO_ORTH_NS5) {
+      // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
+      // quintic (Section 4.3; the paper's own coefficients are not printed)
+      p->sched.clear();
+      for (int k = 0; k < kNs5Steps; ++k) p->sched.insert(p->sched.end(), kNs5Coeffs, kNs5Coeffs + 3);
+      p->n_short = kNs5Steps;
+    } else if (o.ell_fast > o.ell0) {
       p->sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
       p->n_short = (int)p->sched.size() / 3;
       double lb = o.ell0;
@@ -730,6 +751,10 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   a.alpha = alpha;
   a.lr = outer_lr;
   a.mu = mu;
+  a.heavy_ball = plan->opts.momentum == ISOLOCO_MOMENTUM_HEAVY_BALL;
+  a.target_update = plan->opts.target == ISOLOCO_TARGET_UPDATE;
+  a.scale = plan->opts.scale;
+  const bool ns5 = plan->opts.orth == ISOLOCO_ORTH_NS5;
 
   plan->ev_used = 0;
   auto timed = [&](int phase, auto&& launch) -> hipError_t {
@@ -751,9 +776,10 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     const int Sa = plan->n_short;
     const bool two = Sa < S;
     const int buf_short = (Sa - 1) & 1, buf_total = (S - 1) & 1;
-    if ((e = timed(kPhOther, [&] { return launch_fro(t, S, buf_total, st); })) != hipSuccess)
+    if ((e = timed(kPhOther, [&] { return launch_fro(t, S, buf_total, ns5 ? 1 : 0, st); })) != hipSuccess)
       return hip_fail(e, "fro launch");
     NormArgs na{};
+    na.flag_unconverged = ns5 ? 0 : 1;
     na.steps_short = Sa;
     na.steps_total = S;
     na.buf_short = buf_short;
@@ -783,7 +809,8 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       ps.arith = step_arith(plan->opts.precision, k, kProdGram);
       // the first Gram of the second phase was formed by the switch check
       if (!(two && k == Sa) && (e = gram(ps)) != hipSuccess) return hip_fail(e, "Gram launch");
-      if (k == 0 && (e = norm(kNormFirst, 0)) != hipSuccess) return hip_fail(e, "norm launch");
+      // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
+      if (k == 0 && !ns5 && (e = norm(kNormFirst, 0)) != hipSuccess) return hip_fail(e, "norm launch");
       PolarStep pp = ps, pu = ps;
       pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
       pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
@@ -807,7 +834,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       if ((e = gram(pc)) != hipSuccess || (e = norm(kNormFinal, pc.only_active)) != hipSuccess)
         return hip_fail(e, "check launch");
     }
-    if ((e = timed(kPhOther, [&] { return launch_trace(t, st); })) != hipSuccess ||
+    if ((e = timed(kPhOther, [&] { return launch_scale(t, a, st); })) != hipSuccess ||
         (e = timed(kPhFinish, [&] { return launch_finish(t, a, st); })) != hipSuccess)
       return hip_fail(e, "finish launch");
   }

@@ -50,6 +50,9 @@ struct StepArgs {
   int K;
   int worker_dtype;  // 0 float32, 1 bfloat16
   float alpha, lr, mu;
+  int heavy_ball;     // 1: theta <- theta - lr B (standard momentum); 0: Nesterov
+  int target_update;  // 1: B <- mu B + Delta first and the update is corrected
+  int scale;          // 0: mean singular value, 1: RMS, 2: sqrt(rows / cols)
 };
 
 // Arithmetic of one batched-product launch.
@@ -77,17 +80,20 @@ struct NormArgs {
   int steps_short, steps_total;  // schedule lengths
   int buf_short, buf_total;      // X buffer holding the result after each phase
   float tol_switch;              // residual below which a matrix stops after the short schedule
+  int flag_unconverged;          // final check: flag residuals above 1e-3 (not for a fixed-length variant)
 };
 
 hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
 // also initialises the per-matrix iteration state (active, qbuf, steps)
-hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStream_t st);
+// fixed_g: the first step uses g = 1 (no Gram-norm scaling)
+hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fixed_g, hipStream_t st);
 // mode: 0 Gram, 1 polynomial, 2 update
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st);
 hipError_t launch_split_sums(const DevTables& t, int only_active, hipStream_t st);
 hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st);
-// the polar factor of matrix m is in t.x[scalars[m].qbuf]
-hipError_t launch_trace(const DevTables& t, hipStream_t st);
+// the polar factor of matrix m is in t.x[scalars[m].qbuf]; the scale of each
+// correction (a.scale: its mean singular value from <Q, Delta>, or a closed form)
+hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st);
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st);
 
 }  // namespace isoloco

@@ -97,7 +97,7 @@ template <int WDT>
 __global__ void __launch_bounds__(kStreamThreads)
 reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
               float* __restrict__ mom, float* __restrict__ delta, double* __restrict__ part_sq,
-              WorkerPtrs w, int K, float inv_k, float lr, float mu) {
+              WorkerPtrs w, int K, float inv_k, float lr, float mu, int heavy_ball, int target_update) {
   using WL = WorkerLoad<WDT>;
   constexpr int V = WL::kVec;
   __shared__ double red[4];
@@ -136,6 +136,20 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
       for (int q = 0; q < V; ++q) acc[q] *= inv_k;
       if (iso) {
         float* dst = delta + c.ws + (int64_t)v * V;
+        if (target_update) {
+          // B <- mu B + Delta now; the polar input is the update itself
+#pragma unroll
+          for (int q = 0; q < V; q += 4) {
+            floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + q);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float bn = mu * b4[r] + acc[q + r];
+              b4[r] = bn;
+              acc[q + r] = heavy_ball ? bn : acc[q + r] + mu * bn;
+            }
+            *reinterpret_cast<floatx4*>(mom + e + q) = b4;
+          }
+        }
 #pragma unroll
         for (int q = 0; q < V; q += 4) {
           floatx4 o = {acc[q], acc[q + 1], acc[q + 2], acc[q + 3]};
@@ -153,7 +167,7 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
             const float d = acc[q + r];
             const float bn = mu * b4[r] + d;
             b4[r] = bn;
-            t4[r] = th[q + r] - lr * (d + mu * bn);
+            t4[r] = th[q + r] - lr * (heavy_ball ? bn : d + mu * bn);
           }
           *reinterpret_cast<floatx4*>(mom + e + q) = b4;
           *reinterpret_cast<floatx4*>(theta + e + q) = t4;
@@ -169,12 +183,17 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
     for (int k = 0; k < K; ++k) acc += th - WL::one(w.p[k], e);
     acc *= inv_k;
     if (iso) {
+      if (target_update) {
+        const float bn = mu * mom[e] + acc;
+        mom[e] = bn;
+        acc = heavy_ball ? bn : acc + mu * bn;
+      }
       delta[c.ws + i] = acc;
       sq += (double)acc * acc;
     } else {
       const float bn = mu * mom[e] + acc;
       mom[e] = bn;
-      theta[e] = th - lr * (acc + mu * bn);
+      theta[e] = th - lr * (heavy_ball ? bn : acc + mu * bn);
     }
   }
   if (iso) {
@@ -194,7 +213,7 @@ __device__ __forceinline__ double wave_sum_range(const double* part, int begin, 
 // ||Delta||_F per matrix (one wavefront per matrix).
 __global__ void __launch_bounds__(64)
 fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
-           MatScalars* __restrict__ sc, int n_mat, int steps_total, int buf_total) {
+           MatScalars* __restrict__ sc, int n_mat, int steps_total, int buf_total, int fixed_g) {
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
   const double s = wave_sum_range(part_sq, mi.chunk_begin, mi.chunk_end);
@@ -205,7 +224,7 @@ fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
   if (!isfinite(s)) o.flags |= 1;
   else if (s == 0.0) o.flags |= 2;
   o.inv_fro = (o.flags == 0) ? (float)(1.0 / sqrt(s)) : 0.f;
-  o.gscale = 0.f;
+  o.gscale = (fixed_g && o.flags == 0) ? 1.f : 0.f;  // else set from the first Gram
   o.sigma_bar = 0.f;
   o.resid = -1.f;
   o.steps = steps_total;
@@ -1005,7 +1024,7 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
     o.active = go_on ? 1 : 0;
     o.steps = go_on ? a.steps_total : a.steps_short;
     o.qbuf = go_on ? a.buf_total : a.buf_short;
-  } else if (!(o.resid <= 1e-3f) && o.flags == 0) {
+  } else if (a.flag_unconverged && !(o.resid <= 1e-3f) && o.flags == 0) {
     o.flags |= 4;
   }
 }
@@ -1034,24 +1053,31 @@ trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc
   if (threadIdx.x == 0) part_tr[blockIdx.x] = s;
 }
 
+// The scale of each correction.  mode 0: <Q, Delta>_F / r, the mean singular
+// value (from the trace partials); 1: ||Delta||_F / sqrt(r), their RMS;
+// 2: sqrt(rows / cols) of the tensor as stored (Muon's sqrt(fan_out / fan_in)).
 __global__ void __launch_bounds__(64)
 sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
-             MatScalars* __restrict__ sc, int n_mat) {
+             MatScalars* __restrict__ sc, int n_mat, int mode) {
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
-  const double s = wave_sum_range(part_tr, mi.chunk_begin, mi.chunk_end);
+  const double s = mode == 0 ? wave_sum_range(part_tr, mi.chunk_begin, mi.chunk_end) : 0.0;
   if (threadIdx.x != 0) return;
   MatScalars& o = sc[m];
   if (o.flags & 1) o.sigma_bar = __builtin_nanf("");
   else if (o.flags & 2) o.sigma_bar = 0.f;
-  else o.sigma_bar = (float)(s / mi.n);
+  else if (mode == 0) o.sigma_bar = (float)(s / mi.n);
+  else if (mode == 1) o.sigma_bar = (float)((double)o.fro / sqrt((double)mi.n));
+  else o.sigma_bar = (float)(mi.trans ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
 }
 
-// D = alpha sigma_bar Q;  B <- mu B + D;  theta <- theta - lr (D + mu B).
+// D = alpha sigma_bar Q;  B <- mu B + D;  theta <- theta - lr (D + mu B)
+// (heavy_ball: theta <- theta - lr B; target_update: B was updated by the
+// reduction and theta <- theta - lr D).
 __global__ void __launch_bounds__(kStreamThreads)
 finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
               const float* __restrict__ x0, const float* __restrict__ x1, float* __restrict__ theta,
-              float* __restrict__ mom, float alpha, float lr, float mu) {
+              float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball, int target_update) {
   const Chunk c = chunks[blockIdx.x];
   const MatScalars s = sc[c.mat];
   const float* q = s.qbuf ? x1 : x0;
@@ -1063,16 +1089,21 @@ finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ s
     for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
       const int64_t e = c.src + 4 * v;
       const floatx4 qq = *reinterpret_cast<const floatx4*>(q + c.ws + 4 * v);
-      floatx4 b = *reinterpret_cast<const floatx4*>(mom + e);
       floatx4 t = *reinterpret_cast<const floatx4*>(theta + e);
+      if (target_update) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float d = f * qq[r];
-        const float bn = mu * b[r] + d;
-        b[r] = bn;
-        t[r] = t[r] - lr * (d + mu * bn);
+        for (int r = 0; r < 4; ++r) t[r] = t[r] - lr * (f * qq[r]);
+      } else {
+        floatx4 b = *reinterpret_cast<const floatx4*>(mom + e);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = f * qq[r];
+          const float bn = mu * b[r] + d;
+          b[r] = bn;
+          t[r] = t[r] - lr * (heavy_ball ? bn : d + mu * bn);
+        }
+        *reinterpret_cast<floatx4*>(mom + e) = b;
       }
-      *reinterpret_cast<floatx4*>(mom + e) = b;
       *reinterpret_cast<floatx4*>(theta + e) = t;
     }
     done = nv * 4;
@@ -1080,9 +1111,13 @@ finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ s
   for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
     const int64_t e = c.src + i;
     const float d = f * q[c.ws + i];
-    const float bn = mu * mom[e] + d;
-    mom[e] = bn;
-    theta[e] = theta[e] - lr * (d + mu * bn);
+    if (target_update) {
+      theta[e] = theta[e] - lr * d;
+    } else {
+      const float bn = mu * mom[e] + d;
+      mom[e] = bn;
+      theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
+    }
   }
 }
 
@@ -1095,17 +1130,19 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st) 
   const float inv_k = 1.0f / (float)a.K;
   if (a.worker_dtype == 0)
     hipLaunchKernelGGL(reduce_kernel<0>, dim3(t.n_chunks), dim3(kStreamThreads), 0, st, t.chunks,
-                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu);
+                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu, a.heavy_ball,
+                       a.target_update);
   else
     hipLaunchKernelGGL(reduce_kernel<1>, dim3(t.n_chunks), dim3(kStreamThreads), 0, st, t.chunks,
-                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu);
+                       a.theta, a.mom, t.delta, t.part_sq, a.workers, a.K, inv_k, a.lr, a.mu, a.heavy_ball,
+                       a.target_update);
   return hipGetLastError();
 }
 
-hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, hipStream_t st) {
+hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fixed_g, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
   hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat,
-                     steps_total, buf_total);
+                     steps_total, buf_total, fixed_g);
   return hipGetLastError();
 }
 
@@ -1216,18 +1253,20 @@ hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_trace(const DevTables& t, hipStream_t st) {
+hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
-                     t.x[0], t.x[1], t.delta, t.part_tr);
-  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat);
+  if (a.scale == 0)
+    hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+                       t.x[0], t.x[1], t.delta, t.part_tr);
+  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat,
+                     a.scale);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
   hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
-                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu);
+                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update);
   return hipGetLastError();
 }
 

@@ -36,14 +36,24 @@ def workers_host(workers):
 
 
 def _oracle_one(args):
-    (off, rows, cols, kind), theta, ws, B, alpha, lr, mu = args
+    (off, rows, cols, kind), theta, ws, B, alpha, lr, mu, variant = args
     lay = [(0, rows, cols, kind)]
-    th, b, info = oracle.outer_step(lay, theta, ws, B, alpha, lr, mu)
+    th, b, info = oracle.outer_step(lay, theta, ws, B, alpha, lr, mu, variant=variant)
     sb = info[0].get("sigma_bar", 0.0)
     return th, b, sb
 
 
-def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, processes=1):
+# plan option values of the oracle's variant keys
+VARIANT_OPTS = {"orth": {"svd": 0, "ns5": 1}, "scale": {"mean": 0, "rms": 1, "spectral": 2},
+                "momentum": {"nesterov": 0, "heavy_ball": 1}, "target": {"delta": 0, "update": 1}}
+
+
+def variant_opts(variant):
+    """isoloco_options fields for an oracle variant dict."""
+    return {k: VARIANT_OPTS[k][v] for k, v in (variant or {}).items()}
+
+
+def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, processes=1, variant=None):
     """Oracle outer step evaluated tensor by tensor (the tensors of the step are
     independent), optionally on a subset.  Runs in this process by default (the
     compiled Jacobi loop is itself multi-threaded; processes > 1 forks, which is
@@ -54,7 +64,7 @@ def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, pro
     for i in idx:
         off, rows, cols, kind = layout[i]
         sl = slice(off, off + rows * cols)
-        jobs.append(((off, rows, cols, kind), theta[sl], [w[sl] for w in workers], B[sl], alpha, lr, mu))
+        jobs.append(((off, rows, cols, kind), theta[sl], [w[sl] for w in workers], B[sl], alpha, lr, mu, variant))
     if processes == 1 or len(jobs) <= 1:
         res = [_oracle_one(j) for j in jobs]
     else:

@@ -58,7 +58,8 @@ def test_plan_rejects(layout, n, K, dtype, err):
 
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
                                   dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
-                                  dict(ell_fast=float("nan"))])
+                                  dict(ell_fast=float("nan")), dict(orth=2), dict(scale=3), dict(momentum=-1),
+                                  dict(target=2), dict(orth=1), dict(orth=1, scale=0)])
 def test_plan_rejects_options(opts):
     with pytest.raises(iso.IsoLoCoError) as ei:
         iso.isoloco_plan(LAY, 8256, 4, 0, opts)
@@ -179,3 +180,20 @@ def test_big_layout_plans_quickly():
         assert ws >= 3 * 4 * n2d
         assert ws < 3 * 4 * n2d * 1.5 + (1 << 30)
         iso.isoloco_plan_destroy(h)
+
+
+@pytest.mark.parametrize("scale", [1, 2])
+def test_fast_variant_schedule(scale):
+    # the fast variant is five steps of the Muon quintic, one phase
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(orth=1, scale=scale))
+    sched, ns = iso.isoloco_schedule(h, with_split=True)
+    iso.isoloco_plan_destroy(h)
+    assert ns == len(sched) == 5
+    for co in sched:
+        assert tuple(co) == (3.4445, -4.7750, 2.0315)
+
+
+def test_variant_options_accepted():
+    for o in [dict(scale=1), dict(scale=2), dict(momentum=1), dict(target=1), dict(target=1, momentum=1),
+              dict(orth=1, scale=1, momentum=1, target=1)]:
+        iso.isoloco_plan_destroy(iso.isoloco_plan(LAY, 8256, 4, 0, o))

@@ -10,7 +10,7 @@ recovered from the momentum (B_1 = alpha sigma_bar Q when B_0 = 0) and
 import numpy as np
 import pytest
 
-from _helpers import KIND_AVG, KIND_ISO, oracle_per_tensor, relF, workers_host
+from _helpers import KIND_AVG, KIND_ISO, oracle_per_tensor, relF, variant_opts, workers_host
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -43,7 +43,12 @@ def _host_slices(theta, workers, mom, layout, select):
 
 
 def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select=None, check_q=True,
-                     theta=None, mom=None, plan=None, opts=None, return_inputs=False):
+                     theta=None, mom=None, plan=None, opts=None, return_inputs=False, variant=None):
+    if variant:
+        opts = dict(opts or {}, **variant_opts(variant))
+        # Q = B / (alpha * scale) is orthonormal only for the exact polar factor
+        # corrected before a Nesterov or heavy-ball step of B
+        check_q = check_q and variant.get("orth", "svd") == "svd" and variant.get("target", "delta") == "delta"
     from workload import ReplicaGenerator
     dev = torch.device("cuda", 0)
     gen = ReplicaGenerator(cfg, seed=seed, device=dev)
@@ -66,7 +71,8 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
         off, rows, cols, kind = cfg.layout[i]
         sl = slice(off, off + rows * cols)
         th0, wh, b0 = host[i]
-        th_r, b_r, sb_r = oracle_per_tensor([(0, rows, cols, kind)], th0, wh, b0, alpha, lr, mu)[0]
+        th_r, b_r, sb_r = oracle_per_tensor([(0, rows, cols, kind)], th0, wh, b0, alpha, lr, mu,
+                                            variant=variant)[0]
         th = theta[sl].double().cpu().numpy()
         b = mom[sl].double().cpu().numpy()
         e_th = relF(th, th_r)
@@ -151,6 +157,38 @@ def test_big_tiles_with_remainders(iso, precision):
     from workload import custom_layout
     lay, n = custom_layout(BIG_MIXED, align=4)
     _run_and_compare(iso, _cfg(lay, n, K=3), opts=dict(precision=precision))
+
+
+# The paper's variants of the step (Section 4.3's fast path, Appendix B's
+# spectral scale, Section 4.5's standard momentum and update target), each
+# against the oracle's same variant over two steps (the second one starts
+# from a nonzero momentum).
+VARIANTS = [
+    ("fast", {"orth": "ns5", "scale": "rms"}),
+    ("fast_spectral", {"orth": "ns5", "scale": "spectral"}),
+    ("polar_rms", {"scale": "rms"}),
+    ("polar_spectral", {"scale": "spectral"}),
+    ("heavy_ball", {"momentum": "heavy_ball"}),
+    ("target_update", {"target": "update"}),
+    ("target_update_heavy_ball", {"target": "update", "momentum": "heavy_ball"}),
+]
+
+
+@pytest.mark.parametrize("name,variant", VARIANTS, ids=[v[0] for v in VARIANTS])
+def test_variants_two_steps(iso, name, variant):
+    from workload import custom_layout
+    lay, n = custom_layout(RAGGED, align=4)
+    cfg = _cfg(lay, n, K=3)
+    theta, mom, st = _run_and_compare(iso, cfg, variant=variant)
+    _run_and_compare(iso, cfg, step=2, theta=theta, mom=mom, variant=variant)
+    if variant.get("orth") == "ns5":
+        assert all(s.steps == 5 for s, t in zip(st, lay) if t[3] == KIND_ISO)
+
+
+@pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
+def test_fast_variant_full_block(iso, precision):
+    from workload import CONFIGS
+    _run_and_compare(iso, CONFIGS[1], opts=dict(precision=precision), variant={"orth": "ns5", "scale": "rms"})
 
 
 def test_ragged_multi_tile_bf16(iso):
