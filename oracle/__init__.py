@@ -18,8 +18,9 @@ Contents
                  (Algorithm 2's last three assignments); and the variants
                  the paper studies: the fast five-step Newton-Schulz with the
                  RMS scale (Section 4.3), Muon's spectral scale (Appendix B),
-                 standard momentum and correcting the momentum update
-                 instead of the pseudo-gradient (Section 4.5).
+                 standard momentum, correcting the momentum update instead
+                 of the pseudo-gradient, and clipping only the singular
+                 values above or below their mean (Section 4.5).
 
 Every function is pinned by ``tests/test_oracle_pins.py`` against values fixed
 by the mathematics (closed forms, invariants, library routines, brute force)
@@ -32,6 +33,7 @@ from .isoloco_step import (  # noqa: F401
     NS5_COEFFS,
     NS5_STEPS,
     VARIANT_DEFAULT,
+    clip_correct,
     correct_matrix,
     decode_bf16,
     heavy_ball_update,

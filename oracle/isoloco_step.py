@@ -150,6 +150,25 @@ def correct_matrix(M, alpha=1.0, orth="svd", scale="mean"):
     return alpha * f * Q, f, Q
 
 
+def clip_correct(M, alpha=1.0, clip="high"):
+    """Section 4.5's directional variants of the correction: with
+    M = U diag(sigma) V^T and sigma_bar the mean singular value, "high" sets
+    only the singular values above the mean to the mean (sigma <- min(sigma,
+    sigma_bar)), "low" only those below it (sigma <- max(sigma, sigma_bar));
+    U and V are kept.  Returns (alpha * U diag(sigma') V^T, sigma_bar)."""
+    M = np.asarray(M, dtype=np.float64)
+    U, s, Vt = np.linalg.svd(M, full_matrices=False)
+    r = min(M.shape)
+    sbar = float(s.sum()) / r if r > 0 else 0.0
+    if clip == "high":
+        s2 = np.minimum(s, sbar)
+    elif clip == "low":
+        s2 = np.maximum(s, sbar)
+    else:
+        raise ValueError("unknown clip %r" % (clip,))
+    return alpha * (U * s2) @ Vt, sbar
+
+
 def heavy_ball_update(theta, B, D, lr, mu):
     """Standard (non-Nesterov) momentum, the ablation of Section 4.5:
     B <- mu B + D;  theta <- theta - lr * B.  Returns (theta_new, B_new)."""
@@ -166,7 +185,7 @@ def nesterov_update(theta, B, D, lr, mu):
     return theta - lr * P, B_new
 
 
-VARIANT_DEFAULT = {"orth": "svd", "scale": "mean", "momentum": "nesterov", "target": "delta"}
+VARIANT_DEFAULT = {"orth": "svd", "scale": "mean", "momentum": "nesterov", "target": "delta", "clip": "none"}
 
 
 def outer_step(layout, theta, workers, momentum, alpha=1.0, lr=0.7, mu=0.9, variant=None):
@@ -187,6 +206,8 @@ def outer_step(layout, theta, workers, momentum, alpha=1.0, lr=0.7, mu=0.9, vari
                 (Section 4.5's ablation): B <- mu B + Delta, then the
                 correction of P = Delta + mu B (Nesterov) or of B (heavy
                 ball) is the step, theta <- theta - lr * D.
+      clip      "none" | "high" | "low"  -- Section 4.5's directional
+                variants (see clip_correct); they replace orth and scale.
     AVG tensors always take the uncorrected momentum step of their kind.
 
     Returns (theta_new, momentum_new, info) in float64, where info[l] holds
@@ -222,10 +243,14 @@ def outer_step(layout, theta, workers, momentum, alpha=1.0, lr=0.7, mu=0.9, vari
             B_new[sl] = mu * B64[sl] + d
             W = d + mu * B_new[sl] if v["momentum"] == "nesterov" else B_new[sl]
         W2 = W.reshape(rows, cols)
-        D2, f, Q = correct_matrix(W2, alpha, v["orth"], v["scale"])
-        entry = {"sigma_bar": f, "Q": Q, "D": D2, "delta": W2}
-        if v["orth"] == "svd":
-            entry["sigma"] = np.linalg.svd(W2, compute_uv=False)
+        if v["clip"] != "none":
+            D2, f = clip_correct(W2, alpha, v["clip"])
+            entry = {"sigma_bar": f, "D": D2, "delta": W2}
+        else:
+            D2, f, Q = correct_matrix(W2, alpha, v["orth"], v["scale"])
+            entry = {"sigma_bar": f, "Q": Q, "D": D2, "delta": W2}
+            if v["orth"] == "svd":
+                entry["sigma"] = np.linalg.svd(W2, compute_uv=False)
         info.append(entry)
         D = D2.reshape(-1)
         if v["target"] == "delta":

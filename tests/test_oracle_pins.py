@@ -499,6 +499,8 @@ def _variant_pins_pass():
         test_heavy_ball_matches_torch_sgd()
         test_fast_variant_on_a_flat_spectrum_is_ns5_times_scale()
         test_correcting_the_update_first_step_and_mu_zero("nesterov")
+        test_clip_variants_on_a_known_spectrum("high")
+        test_clip_variants_on_a_known_spectrum("low")
     except AssertionError:
         return False
     return True
@@ -509,7 +511,8 @@ def test_variant_pins_pass_unpatched():
 
 
 @pytest.mark.parametrize("mistake", ["ns5_no_normalise", "ns5_transposed_gram", "rms_over_r",
-                                     "heavy_ball_nesterov_form", "heavy_ball_old_B"])
+                                     "heavy_ball_nesterov_form", "heavy_ball_old_B", "clip_swapped",
+                                     "clip_to_rms"])
 def test_planted_variant_mistake_is_caught(monkeypatch, mistake):
     if mistake == "ns5_no_normalise":
         def ns(M, coeffs=step.NS5_COEFFS, steps=step.NS5_STEPS):
@@ -543,9 +546,45 @@ def test_planted_variant_mistake_is_caught(monkeypatch, mistake):
     elif mistake == "heavy_ball_nesterov_form":
         monkeypatch.setattr(step, "heavy_ball_update", step.nesterov_update)
         monkeypatch.setattr(oracle, "heavy_ball_update", step.nesterov_update)
+    elif mistake == "clip_swapped":
+        orig_clip = step.clip_correct
+        def clip(M, alpha=1.0, clip="high"):
+            return orig_clip(M, alpha, "low" if clip == "high" else "high")
+        monkeypatch.setattr(step, "clip_correct", clip)
+        monkeypatch.setattr(oracle, "clip_correct", clip)
+    elif mistake == "clip_to_rms":
+        def clip(M, alpha=1.0, clip="high"):
+            U, s, Vt = np.linalg.svd(np.asarray(M, dtype=np.float64), full_matrices=False)
+            sb = float(np.sqrt(np.mean(s ** 2)))
+            s2 = np.minimum(s, sb) if clip == "high" else np.maximum(s, sb)
+            return alpha * (U * s2) @ Vt, sb
+        monkeypatch.setattr(step, "clip_correct", clip)
+        monkeypatch.setattr(oracle, "clip_correct", clip)
     elif mistake == "heavy_ball_old_B":
         def hb(theta, B, D, lr, mu):
             return theta - lr * (mu * B), mu * B + D
         monkeypatch.setattr(step, "heavy_ball_update", hb)
         monkeypatch.setattr(oracle, "heavy_ball_update", hb)
     assert not _variant_pins_pass()
+
+
+@pytest.mark.parametrize("clip", ["high", "low"])
+def test_clip_variants_on_a_known_spectrum(clip):
+    # U diag(s) V^T with s = (4, 2, 1, 1): mean 2, high -> (2, 2, 1, 1), low -> (4, 2, 2, 2)
+    rng = np.random.default_rng(17)
+    s = np.array([4.0, 2.0, 1.0, 1.0])
+    M, U, V = _svd_of_spectrum(6, 4, s, rng)
+    D, sbar = oracle.clip_correct(M, 1.5, clip)
+    assert abs(sbar - 2.0) < 1e-13
+    want = np.array([2.0, 2.0, 1.0, 1.0]) if clip == "high" else np.array([4.0, 2.0, 2.0, 2.0])
+    np.testing.assert_allclose(D, 1.5 * (U * want) @ V.T, atol=1e-13)
+    # both clips together give the full flattening; the sum of the two is M + mean * Q
+    Dh, _ = oracle.clip_correct(M, 1.0, "high")
+    Dl, _ = oracle.clip_correct(M, 1.0, "low")
+    np.testing.assert_allclose(Dh + Dl, M + 2.0 * polar_factor(M)[0], atol=1e-12)
+    # through outer_step (wide orientation too)
+    lay = [(0, 4, 6, step.KIND_ISO)]
+    theta = np.zeros(24)
+    ws = [-M.T.reshape(-1)]
+    th, B, info = oracle.outer_step(lay, theta, ws, np.zeros(24), 1.0, 1.0, 0.0, variant={"clip": clip})
+    np.testing.assert_allclose(-th.reshape(4, 6), ((U * want) @ V.T).T, atol=1e-12)
