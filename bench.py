@@ -148,7 +148,8 @@ def cpu_baseline(cfg, theta, workers, mom, budget_s, variant=None):
             "cores": threads if J.BACKEND == "c" else 1, "kind": "oracle",
             "sample": "float64 oracle (%s) on %s of the workload's "
                       "tensors, each shape's time scaled by its count; host has %d cores" %
-                      ("five Newton-Schulz steps in numpy" if variant else
+                      ("five Newton-Schulz steps in numpy" if variant and variant.get("orth") == "ns5" else
+                       "LAPACK SVD (numpy)" if variant and "clip" in variant else
                        "one-sided Jacobi SVD, %s sweeps" % J.BACKEND, ", ".join(timed),
                        len(os.sched_getaffinity(0)))}
 
@@ -166,9 +167,10 @@ def main():
                     help="arithmetic of the polar iteration's matrix products")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (reference for HBM counters)")
-    ap.add_argument("--variant", choices=["exact", "fast"], default="exact",
+    ap.add_argument("--variant", choices=["exact", "fast", "clip_high", "clip_low"], default="exact",
                     help="exact: Algorithm 2 (converged polar factor, mean singular value); fast: "
-                         "Section 4.3 (five Newton-Schulz steps, RMS of the singular values)")
+                         "Section 4.3 (five Newton-Schulz steps, RMS of the singular values); clip_high / "
+                         "clip_low: Section 4.5 (only the singular values above / below the mean set to it)")
     ap.add_argument("--ell-fast", type=float, default=0.0,
                     help="short-schedule bound (0: library default; negative: one phase)")
     args = ap.parse_args()
@@ -193,7 +195,8 @@ def main():
     theta0 = theta.clone()
     prec = {"mixed": iso.ISOLOCO_PREC_MIXED, "bf16x3": iso.ISOLOCO_PREC_BF16X3,
             "bf16x6": iso.ISOLOCO_PREC_BF16X6, "fp32": iso.ISOLOCO_PREC_FP32}[args.precision]
-    vopts = dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS) if args.variant == "fast" else {}
+    vopts = {"exact": {}, "fast": dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS),
+             "clip_high": dict(clip=iso.ISOLOCO_CLIP_HIGH), "clip_low": dict(clip=iso.ISOLOCO_CLIP_LOW)}[args.variant]
     plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, **vopts),
                            device=dev)
     sched, n_short = plan.schedule_split()
@@ -314,8 +317,9 @@ def main():
         "matrices_by_steps": {str(k): v for k, v in sorted(steps_hist.items())},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget,
-                                           {"orth": "ns5", "scale": "rms"} if args.variant == "fast" else None)
+        ovar = {"exact": None, "fast": {"orth": "ns5", "scale": "rms"}, "clip_high": {"clip": "high"},
+                "clip_low": {"clip": "low"}}[args.variant]
+        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget, ovar)
     plan.close()
     print(json.dumps(out), flush=True)
 

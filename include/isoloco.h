@@ -114,6 +114,11 @@ typedef struct {
                         correct the update (Delta + mu B, or B with HEAVY_BALL) and step
                         theta <- theta - lr D (Section 4.5's ablation).  AVG tensors always
                         take the uncorrected step of the chosen momentum                   */
+  int32_t clip;      /* ISOLOCO_CLIP_NONE: flatten the whole spectrum to its mean (Algorithm 2);
+                        ISOLOCO_CLIP_HIGH / ISOLOCO_CLIP_LOW: set only the singular values
+                        above / below the mean to the mean, keeping U, V and the other
+                        singular values (Section 4.5).  Needs ORTH_POLAR and SCALE_MEAN; a
+                        second polar iteration runs on Delta - sigma_bar Q                 */
 } isoloco_options;
 
 #define ISOLOCO_PREC_MIXED 0
@@ -130,6 +135,9 @@ typedef struct {
 #define ISOLOCO_MOMENTUM_HEAVY_BALL 1
 #define ISOLOCO_TARGET_DELTA 0
 #define ISOLOCO_TARGET_UPDATE 1
+#define ISOLOCO_CLIP_NONE 0
+#define ISOLOCO_CLIP_HIGH 1
+#define ISOLOCO_CLIP_LOW 2
 
 /* Per-tensor results of the last isoloco_aggregate() on a plan. */
 typedef struct {

@@ -37,6 +37,9 @@ ISOLOCO_MOMENTUM_NESTEROV = 0
 ISOLOCO_MOMENTUM_HEAVY_BALL = 1
 ISOLOCO_TARGET_DELTA = 0
 ISOLOCO_TARGET_UPDATE = 1
+ISOLOCO_CLIP_NONE = 0
+ISOLOCO_CLIP_HIGH = 1
+ISOLOCO_CLIP_LOW = 2
 ISOLOCO_FLAG_NONFINITE = 1
 ISOLOCO_FLAG_ZERO = 2
 ISOLOCO_FLAG_NOT_CONVERGED = 4
@@ -57,7 +60,7 @@ class isoloco_options(ctypes.Structure):
     _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
                 ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float),
                 ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
-                ("target", ctypes.c_int32)]
+                ("target", ctypes.c_int32), ("clip", ctypes.c_int32)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):

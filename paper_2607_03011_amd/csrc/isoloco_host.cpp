@@ -318,6 +318,7 @@ struct isoloco_plan_s {
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
   size_t off_pnorm = 0;
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
+  size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
   size_t off_poly = 0, off_gpart = 0, total = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -511,6 +512,9 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_delta = take((size_t)p->n2d * sizeof(float));
   p->off_x0 = take((size_t)p->n2d * sizeof(float));
   p->off_x1 = take((size_t)p->n2d * sizeof(float));
+  const bool clip = p->opts.clip != ISOLOCO_CLIP_NONE;
+  p->off_x2 = take(clip ? (size_t)p->n2d * sizeof(float) : 0);
+  p->off_sc2 = take(clip ? p->mats.size() * sizeof(MatScalars) : 0);
   p->off_gram = take((size_t)p->nsq * sizeof(float));
   p->off_poly = take((size_t)p->nsq * sizeof(float));
   p->off_gpart = take((size_t)p->npart * sizeof(float));
@@ -547,6 +551,8 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.delta = reinterpret_cast<float*>(w + p->off_delta);
   t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
   t.x[1] = reinterpret_cast<float*>(w + p->off_x1);
+  t.x2 = reinterpret_cast<float*>(w + p->off_x2);
+  t.scalars2 = reinterpret_cast<MatScalars*>(w + p->off_sc2);
   t.gram = reinterpret_cast<float*>(w + p->off_gram);
   t.poly = reinterpret_cast<float*>(w + p->off_poly);
   t.gpart = reinterpret_cast<float*>(w + p->off_gpart);
@@ -605,6 +611,10 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     return fail(ISOLOCO_ERR_INVALID_ARG, "unknown momentum %d", o.momentum);
   if (o.target < ISOLOCO_TARGET_DELTA || o.target > ISOLOCO_TARGET_UPDATE)
     return fail(ISOLOCO_ERR_INVALID_ARG, "unknown target %d", o.target);
+  if (o.clip < ISOLOCO_CLIP_NONE || o.clip > ISOLOCO_CLIP_LOW)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "unknown clip %d", o.clip);
+  if (o.clip != ISOLOCO_CLIP_NONE && (o.orth != ISOLOCO_ORTH_POLAR || o.scale != ISOLOCO_SCALE_MEAN))
+    return fail(ISOLOCO_ERR_INVALID_ARG, "the clip variants need ORTH_POLAR and SCALE_MEAN");
   if (o.orth == ISOLOCO_ORTH_NS5 && o.scale == ISOLOCO_SCALE_MEAN)
     return fail(ISOLOCO_ERR_INVALID_ARG,
                 "the Newton-Schulz variant gives no singular values: use SCALE_RMS or SCALE_SPECTRAL");
@@ -754,6 +764,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   a.heavy_ball = plan->opts.momentum == ISOLOCO_MOMENTUM_HEAVY_BALL;
   a.target_update = plan->opts.target == ISOLOCO_TARGET_UPDATE;
   a.scale = plan->opts.scale;
+  a.clip = plan->opts.clip;
   const bool ns5 = plan->opts.orth == ISOLOCO_ORTH_NS5;
 
   plan->ev_used = 0;
@@ -776,66 +787,104 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     const int Sa = plan->n_short;
     const bool two = Sa < S;
     const int buf_short = (Sa - 1) & 1, buf_total = (S - 1) & 1;
-    if ((e = timed(kPhOther, [&] { return launch_fro(t, S, buf_total, ns5 ? 1 : 0, st); })) != hipSuccess)
-      return hip_fail(e, "fro launch");
-    NormArgs na{};
-    na.flag_unconverged = ns5 ? 0 : 1;
-    na.steps_short = Sa;
-    na.steps_total = S;
-    na.buf_short = buf_short;
-    na.buf_total = buf_total;
-    na.tol_switch = kSwitchTol;
-    auto gram = [&](const PolarStep& ps) -> hipError_t {
-      hipError_t r = timed(kPhGram, [&] { return launch_gemm(t, 0, ps, st); });
-      if (r == hipSuccess && t.n_split)
-        r = timed(kPhOther, [&] { return launch_split_sums(t, ps.only_active, st); });
-      return r;
-    };
-    auto norm = [&](int mode, int only_active) -> hipError_t {
-      na.mode = mode;
-      na.only_active = only_active;
-      return timed(kPhOther, [&] { return launch_gram_norm(t, na, st); });
-    };
-    const float* xin = t.delta;
-    for (int k = 0; k < S; ++k) {
-      PolarStep ps{};
-      ps.xin = xin;
-      ps.xout = t.x[k & 1];
-      ps.ca = (float)plan->sched[3 * k];
-      ps.cb = (float)plan->sched[3 * k + 1];
-      ps.cc = (float)plan->sched[3 * k + 2];
-      ps.first = (k == 0);
-      ps.only_active = (k >= Sa);
-      ps.arith = step_arith(plan->opts.precision, k, kProdGram);
-      // the first Gram of the second phase was formed by the switch check
-      if (!(two && k == Sa) && (e = gram(ps)) != hipSuccess) return hip_fail(e, "Gram launch");
-      // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
-      if (k == 0 && !ns5 && (e = norm(kNormFirst, 0)) != hipSuccess) return hip_fail(e, "norm launch");
-      PolarStep pp = ps, pu = ps;
-      pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
-      pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
-      if ((e = timed(kPhPoly, [&] { return launch_gemm(t, 1, pp, st); })) != hipSuccess ||
-          (e = timed(kPhUpdate, [&] { return launch_gemm(t, 2, pu, st); })) != hipSuccess)
-        return hip_fail(e, "polar step launch");
-      xin = ps.xout;
-      if (two && k == Sa - 1) {
+    const char* what = "";
+    // The polar iteration on the matrices in tt.delta (state in tt.scalars;
+    // the chunk partials of their squared norms in tt.part_sq); the factor of
+    // matrix m ends in tt.x[scalars[m].qbuf].
+    auto polar = [&](const DevTables& tt, bool check) -> hipError_t {
+      hipError_t r;
+      what = "fro launch";
+      if ((r = timed(kPhOther, [&] { return launch_fro(tt, S, buf_total, ns5 ? 1 : 0, st); })) != hipSuccess)
+        return r;
+      NormArgs na{};
+      na.flag_unconverged = ns5 ? 0 : 1;
+      na.steps_short = Sa;
+      na.steps_total = S;
+      na.buf_short = buf_short;
+      na.buf_total = buf_total;
+      na.tol_switch = kSwitchTol;
+      auto gram = [&](const PolarStep& ps) -> hipError_t {
+        hipError_t q = timed(kPhGram, [&] { return launch_gemm(tt, 0, ps, st); });
+        if (q == hipSuccess && tt.n_split)
+          q = timed(kPhOther, [&] { return launch_split_sums(tt, ps.only_active, st); });
+        return q;
+      };
+      auto norm = [&](int mode, int only_active) -> hipError_t {
+        na.mode = mode;
+        na.only_active = only_active;
+        return timed(kPhOther, [&] { return launch_gram_norm(tt, na, st); });
+      };
+      const float* xin = tt.delta;
+      for (int k = 0; k < S; ++k) {
+        PolarStep ps{};
+        ps.xin = xin;
+        ps.xout = tt.x[k & 1];
+        ps.ca = (float)plan->sched[3 * k];
+        ps.cb = (float)plan->sched[3 * k + 1];
+        ps.cc = (float)plan->sched[3 * k + 2];
+        ps.first = (k == 0);
+        ps.only_active = (k >= Sa);
+        ps.arith = step_arith(plan->opts.precision, k, kProdGram);
+        what = "polar step launch";
+        // the first Gram of the second phase was formed by the switch check
+        if (!(two && k == Sa) && (r = gram(ps)) != hipSuccess) return r;
+        // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
+        if (k == 0 && !ns5 && (r = norm(kNormFirst, 0)) != hipSuccess) return r;
+        PolarStep pp = ps, pu = ps;
+        pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
+        pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
+        if ((r = timed(kPhPoly, [&] { return launch_gemm(tt, 1, pp, st); })) != hipSuccess ||
+            (r = timed(kPhUpdate, [&] { return launch_gemm(tt, 2, pu, st); })) != hipSuccess)
+          return r;
+        xin = ps.xout;
+        if (two && k == Sa - 1) {
+          PolarStep pc{};
+          pc.xin = xin;
+          pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
+          what = "switch check launch";
+          if ((r = gram(pc)) != hipSuccess || (r = norm(kNormSwitch, 0)) != hipSuccess) return r;
+        }
+      }
+      if (check) {
         PolarStep pc{};
         pc.xin = xin;
-        pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
-        if ((e = gram(pc)) != hipSuccess || (e = norm(kNormSwitch, 0)) != hipSuccess)
-          return hip_fail(e, "switch check launch");
+        pc.only_active = two ? 1 : 0;
+        pc.arith = step_arith(plan->opts.precision, S, kProdGram);
+        what = "check launch";
+        if ((r = gram(pc)) != hipSuccess || (r = norm(kNormFinal, pc.only_active)) != hipSuccess) return r;
       }
-    }
-    if (plan->opts.check == 1) {
+      return hipSuccess;
+    };
+    if ((e = polar(t, plan->opts.check == 1)) != hipSuccess) return hip_fail(e, what);
+    if ((e = timed(kPhOther, [&] { return launch_scale(t, a, st); })) != hipSuccess)
+      return hip_fail(e, "scale launch");
+    if (a.clip) {
+      // E = Delta - sigma_bar Q, its polar factor Q2 (a second iteration), then
+      // |E| = Q (Q2^T E): the finish forms U diag(min or max(sigma, sigma_bar)) V^T
+      // as (E -+ |E|) / 2 + sigma_bar Q
+      DevTables t2 = t;
+      t2.scalars = t.scalars2;
+      if ((e = timed(kPhOther, [&] { return launch_clip_prep(t, st); })) != hipSuccess)
+        return hip_fail(e, "clip launch");
+      if ((e = polar(t2, false)) != hipSuccess) return hip_fail(e, what);
       PolarStep pc{};
-      pc.xin = xin;
-      pc.only_active = two ? 1 : 0;
+      pc.xin = t.x[0];
+      pc.xin_alt = t.x[1];
+      pc.bin = t.delta;
       pc.arith = step_arith(plan->opts.precision, S, kProdGram);
-      if ((e = gram(pc)) != hipSuccess || (e = norm(kNormFinal, pc.only_active)) != hipSuccess)
-        return hip_fail(e, "check launch");
+      hipError_t r = timed(kPhGram, [&] { return launch_gemm(t2, 0, pc, st); });
+      if (r == hipSuccess && t.n_split) r = timed(kPhOther, [&] { return launch_split_sums(t2, 0, st); });
+      if (r != hipSuccess) return hip_fail(r, "clip product launch");
+      DevTables t3 = t2;
+      t3.poly = t.gram;  // the update product reads Q2^T E as its right factor
+      PolarStep pu{};
+      pu.xin = t.x2;
+      pu.xout = t.x[0];
+      pu.arith = step_arith(plan->opts.precision, S, kProdUpdate);
+      if ((e = timed(kPhUpdate, [&] { return launch_gemm(t3, 2, pu, st); })) != hipSuccess)
+        return hip_fail(e, "clip product launch");
     }
-    if ((e = timed(kPhOther, [&] { return launch_scale(t, a, st); })) != hipSuccess ||
-        (e = timed(kPhFinish, [&] { return launch_finish(t, a, st); })) != hipSuccess)
+    if ((e = timed(kPhFinish, [&] { return launch_finish(t, a, st); })) != hipSuccess)
       return hip_fail(e, "finish launch");
   }
   plan->last_stream = st;

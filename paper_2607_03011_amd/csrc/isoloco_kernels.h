@@ -34,6 +34,8 @@ struct DevTables {
   double* part_norm;  // n_mat x kNormSlices partials of the Gram norms
   float* delta;
   float* x[2];
+  float* x2;              // clip variants: copy of the polar factor Q (else unused)
+  MatScalars* scalars2;   // clip variants: state of the second polar iteration
   float* gram;
   float* poly;
   float* gpart;
@@ -50,6 +52,7 @@ struct StepArgs {
   int K;
   int worker_dtype;  // 0 float32, 1 bfloat16
   float alpha, lr, mu;
+  int clip;           // 0: none; 1: clip_high; 2: clip_low (see launch_clip_prep)
   int heavy_ball;     // 1: theta <- theta - lr B (standard momentum); 0: Nesterov
   int target_update;  // 1: B <- mu B + Delta first and the update is corrected
   int scale;          // 0: mean singular value, 1: RMS, 2: sqrt(rows / cols)
@@ -60,6 +63,8 @@ enum Arith { kArithBf16x3 = 0, kArithBf16x6 = 1, kArithFp32 = 2 };
 
 struct PolarStep {
   const float* xin;
+  const float* xin_alt;  // if set, matrix m reads X from xin_alt when its qbuf is 1 (Gram mode)
+  const float* bin;      // if set, the Gram's second operand (same layout as X): X^T B
   float* xout;
   float ca, cb, cc;
   int first;
@@ -95,5 +100,9 @@ hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t s
 // correction (a.scale: its mean singular value from <Q, Delta>, or a closed form)
 hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st);
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st);
+// Clip variants (U diag(min or max(sigma, sigma_bar)) V^T): E = Delta - sigma_bar Q
+// replaces Delta in t.delta, Q is copied to t.x2, and the chunk partials of
+// ||E||^2 are left in t.part_sq for a second polar iteration (on E)
+hipError_t launch_clip_prep(const DevTables& t, hipStream_t st);
 
 }  // namespace isoloco

@@ -321,6 +321,8 @@ struct GemmArgs {
   const Task* tasks;
   const MatScalars* sc;
   const float* xin;   // Gram/Update: X input buffer (Delta at step 0)
+  const float* xin_alt;  // Gram: if set, matrices whose qbuf is 1 read X here
+  const float* bin;      // Gram: if set, the second operand B (C = X^T B)
   float* xout;        // Update: X output buffer
   float* gram;        // n x n Gram buffers (Gram output, Poly input)
   float* poly;        // n x n polynomial buffers (Poly output, Update input)
@@ -360,11 +362,12 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     s.gs = q.gscale;
   }
   if (MODE == kGram) {
-    const float* x = g.xin + mi.ws_off;
+    const float* x = ((g.xin_alt && g.sc[task.mat].qbuf) ? g.xin_alt : g.xin) + mi.ws_off;
     s.k_begin = task.ks * mi.kchunk;
     s.k_end = min(m, s.k_begin + mi.kchunk);
     s.A = {x, s.sr, s.sc, s.k_end, n, !mi.trans, vec, s.xscale};
     s.B = s.A;
+    if (g.bin) s.B.base = g.bin + mi.ws_off;
     s.M = n;
     s.N = n;
   } else if (MODE == kPoly) {
@@ -1077,12 +1080,33 @@ sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_t
 __global__ void __launch_bounds__(kStreamThreads)
 finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
               const float* __restrict__ x0, const float* __restrict__ x1, float* __restrict__ theta,
-              float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball, int target_update) {
+              float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball, int target_update,
+              int clip, const float* __restrict__ ebuf, const float* __restrict__ qcopy) {
   const Chunk c = chunks[blockIdx.x];
   const MatScalars s = sc[c.mat];
   const float* q = s.qbuf ? x1 : x0;
   float f = alpha * s.sigma_bar;
   if (s.flags & 2) f = 0.f;
+  if (clip) {
+    // clip_high: D = alpha ((E - |E|) / 2 + sigma_bar Q), clip_low: (E + |E|) / 2,
+    // with E = Delta - sigma_bar Q (ebuf), |E| = Q (Q2^T E) (x0), Q copied to qcopy
+    const float sg = clip == 1 ? -0.5f : 0.5f;
+    const float sb = s.sigma_bar;
+    const float al = (s.flags & 2) ? 0.f : alpha;
+    for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
+      const int64_t e = c.src + i;
+      const float ev = ebuf[c.ws + i];
+      const float d = al * (0.5f * ev + sg * x0[c.ws + i] + sb * qcopy[c.ws + i]);
+      if (target_update) {
+        theta[e] = theta[e] - lr * d;
+      } else {
+        const float bn = mu * mom[e] + d;
+        mom[e] = bn;
+        theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
+      }
+    }
+    return;
+  }
   int done = 0;
   if (c.vec) {
     const int nv = c.count / 4;
@@ -1119,6 +1143,29 @@ finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ s
       theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
     }
   }
+}
+
+// Clip variants, first half: E = Delta - sigma_bar Q in place of Delta, Q
+// copied aside, and the chunk partials of ||E||^2 for the second iteration.
+__global__ void __launch_bounds__(kStreamThreads)
+clip_prep_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
+                 const float* __restrict__ x1, float* __restrict__ delta, float* __restrict__ qcopy,
+                 double* __restrict__ part_sq) {
+  __shared__ double red[4];
+  const Chunk c = chunks[blockIdx.x];
+  const MatScalars s = sc[c.mat];
+  const float* q = s.qbuf ? x1 : x0;
+  const float sb = s.flags ? 0.f : s.sigma_bar;
+  double sq = 0.0;
+  for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
+    const float qv = q[c.ws + i];
+    const float ev = delta[c.ws + i] - sb * qv;
+    delta[c.ws + i] = ev;
+    qcopy[c.ws + i] = qv;
+    sq += (double)ev * ev;
+  }
+  sq = block_sum256(sq, red);
+  if (threadIdx.x == 0) part_sq[blockIdx.x] = sq;
 }
 
 // ---------------------------------------------------------------------------
@@ -1217,6 +1264,8 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.mats = t.mats;
   g.sc = t.scalars;
   g.xin = p.xin;
+  g.xin_alt = p.xin_alt;
+  g.bin = p.bin;
   g.xout = p.xout;
   g.gram = t.gram;
   g.poly = t.poly;
@@ -1266,8 +1315,18 @@ hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
   hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
-                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update);
+                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update, a.clip,
+                     t.delta, t.x2);
   return hipGetLastError();
 }
 
+}  // namespace isoloco
+
+namespace isoloco {
+hipError_t launch_clip_prep(const DevTables& t, hipStream_t st) {
+  if (t.n_iso_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(clip_prep_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+                     t.x[0], t.x[1], t.delta, t.x2, t.part_sq);
+  return hipGetLastError();
+}
 }  // namespace isoloco

@@ -45,7 +45,8 @@ def _oracle_one(args):
 
 # plan option values of the oracle's variant keys
 VARIANT_OPTS = {"orth": {"svd": 0, "ns5": 1}, "scale": {"mean": 0, "rms": 1, "spectral": 2},
-                "momentum": {"nesterov": 0, "heavy_ball": 1}, "target": {"delta": 0, "update": 1}}
+                "momentum": {"nesterov": 0, "heavy_ball": 1}, "target": {"delta": 0, "update": 1},
+                "clip": {"none": 0, "high": 1, "low": 2}}
 
 
 def variant_opts(variant):

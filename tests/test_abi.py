@@ -59,7 +59,8 @@ def test_plan_rejects(layout, n, K, dtype, err):
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
                                   dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
                                   dict(ell_fast=float("nan")), dict(orth=2), dict(scale=3), dict(momentum=-1),
-                                  dict(target=2), dict(orth=1), dict(orth=1, scale=0)])
+                                  dict(target=2), dict(orth=1), dict(orth=1, scale=0), dict(clip=3),
+                                  dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1)])
 def test_plan_rejects_options(opts):
     with pytest.raises(iso.IsoLoCoError) as ei:
         iso.isoloco_plan(LAY, 8256, 4, 0, opts)
@@ -195,5 +196,5 @@ def test_fast_variant_schedule(scale):
 
 def test_variant_options_accepted():
     for o in [dict(scale=1), dict(scale=2), dict(momentum=1), dict(target=1), dict(target=1, momentum=1),
-              dict(orth=1, scale=1, momentum=1, target=1)]:
+              dict(orth=1, scale=1, momentum=1, target=1), dict(clip=1), dict(clip=2, momentum=1, target=1)]:
         iso.isoloco_plan_destroy(iso.isoloco_plan(LAY, 8256, 4, 0, o))

@@ -48,7 +48,8 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
         opts = dict(opts or {}, **variant_opts(variant))
         # Q = B / (alpha * scale) is orthonormal only for the exact polar factor
         # corrected before a Nesterov or heavy-ball step of B
-        check_q = check_q and variant.get("orth", "svd") == "svd" and variant.get("target", "delta") == "delta"
+        check_q = (check_q and variant.get("orth", "svd") == "svd" and variant.get("target", "delta") == "delta"
+                   and variant.get("clip", "none") == "none")
     from workload import ReplicaGenerator
     dev = torch.device("cuda", 0)
     gen = ReplicaGenerator(cfg, seed=seed, device=dev)
@@ -171,6 +172,9 @@ VARIANTS = [
     ("heavy_ball", {"momentum": "heavy_ball"}),
     ("target_update", {"target": "update"}),
     ("target_update_heavy_ball", {"target": "update", "momentum": "heavy_ball"}),
+    ("clip_high", {"clip": "high"}),
+    ("clip_low", {"clip": "low"}),
+    ("clip_high_heavy_ball_update", {"clip": "high", "momentum": "heavy_ball", "target": "update"}),
 ]
 
 
@@ -183,6 +187,12 @@ def test_variants_two_steps(iso, name, variant):
     _run_and_compare(iso, cfg, step=2, theta=theta, mom=mom, variant=variant)
     if variant.get("orth") == "ns5":
         assert all(s.steps == 5 for s, t in zip(st, lay) if t[3] == KIND_ISO)
+
+
+@pytest.mark.parametrize("clip", ["high", "low"])
+def test_clip_full_block(iso, clip):
+    from workload import CONFIGS
+    _run_and_compare(iso, CONFIGS[1], variant={"clip": clip})
 
 
 @pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
