@@ -16,6 +16,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -235,10 +237,12 @@ def main():
     launches = {"gemm": 0}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    step_ms = []
     for _ in range(args.steps):
         restore()
         plan.aggregate(theta, workers, mom, cfg.alpha, cfg.outer_lr, cfg.mu)
         tm = plan.timing()
+        step_ms.append(tm.total_ms)
         for k in acc:
             acc[k] += getattr(tm, k)
         launches["gemm"] += tm.gram_launches + tm.poly_launches + tm.update_launches
@@ -312,6 +316,7 @@ def main():
                             "traffic": mt["finish_bytes_per_launch"] if measured else None,
                             "bytes_per_launch": fbytes, "ms": round(per["finish_ms"], 4)},
         "phases_ms": {k: round(v, 4) for k, v in per.items()},
+        "library_ms_p10_p50_p90": [round(float(x), 4) for x in np.percentile(step_ms, [10, 50, 90])],
         "input_restore_ms": round(restore_ms, 4),
         "max_orth_resid": resid,
         "matrices_by_steps": {str(k): v for k, v in sorted(steps_hist.items())},
