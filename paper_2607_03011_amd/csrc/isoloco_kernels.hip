@@ -448,9 +448,37 @@ __device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup
 // acc[a][b][r] holds C(i, j) with
 //   i = i0 + wm*32*NA + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32
 // (the 32 x 32 accumulator layout of the fp32 and bf16 MFMA instructions).
-template <int MODE, int NA = 2, int WNC = 2>
+template <int MODE, int NA = 2, int WNC = 2, bool SWAP = false, bool VEC = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
                                               const floatx16 (&acc)[NA][2]) {
+  if (MODE == kUpdate && VEC) {
+    // Interior update tile: 16-byte stores.  Row-major X' (SWAP, transposed
+    // accumulators): lane holds X'(i, j .. j+3); wide-stored X' (i contiguous):
+    // lane holds X'(i .. i+3, j).
+    float* xo = g.xout + s.mi.ws_off;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave / WNC, wn = wave % WNC;
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const floatx4 v = {acc[a][b][4 * grp], acc[a][b][4 * grp + 1], acc[a][b][4 * grp + 2],
+                             acc[a][b][4 * grp + 3]};
+          const int off4 = 8 * grp + 4 * (lane >> 5);
+          if (SWAP) {
+            const int i = s.i0 + wm * 32 * NA + a * 32 + (lane & 31);
+            const int j = s.j0 + wn * 64 + b * 32 + off4;
+            *reinterpret_cast<floatx4*>(xo + (int64_t)i * s.sr + j) = v;
+          } else {
+            const int i = s.i0 + wm * 32 * NA + a * 32 + off4;
+            const int j = s.j0 + wn * 64 + b * 32 + (lane & 31);
+            *reinterpret_cast<floatx4*>(xo + i + (int64_t)j * s.sc) = v;
+          }
+        }
+    return;
+  }
   const MatInfo& mi = s.mi;
   const int n = mi.n;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -749,7 +777,9 @@ __device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[
 // One k16 substep of a wave's (32 NA) x 64 tile: read the operand fragments
 // of the NS planes from LDS and issue the part products (smallest order
 // first).  WNC waves span the block's columns (wm = wave / WNC, wn = wave % WNC).
-template <int NS, int NA = 2, int WNC = 2, int ROWS = kBM>
+// SWAP: issue each product as B A instead of A B, so that the accumulators
+// hold the transposed 32 x 32 blocks (4 consecutive output columns per lane).
+template <int NS, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false>
 __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], const __bf16 (*Bp)[ROWS][kLdsK],
                                              int kk, floatx16 (&acc)[NA][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -776,7 +806,8 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], co
       for (int ord = NS - 1; ord >= 0; --ord)
 #pragma unroll
         for (int pa = ord; pa >= 0; --pa)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
+          acc[a][b] = SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b][ord - pa], av[a][pa], acc[a][b], 0, 0, 0)
+                           : __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
 }
 
 // bf16x3 (NS = 2) double-buffers the LDS slabs: while the products of slab s
@@ -793,6 +824,8 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
   // only X operands carry a scale (Gram: both, Update: A)
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
+  // interior update tiles of row-major X' accumulate transposed blocks (16-byte stores)
+  constexpr bool kSwap = MODE == kUpdate && LAYOUT == kFastT0;
   const GemmSetup s = gemm_setup<MODE>(g, task);
   floatx16 acc[2][2];
   gemm_acc_init<MODE>(g, s, acc);
@@ -821,17 +854,17 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
     __syncthreads();
     int sl = 0;
     for (; sl + 2 < nslab; sl += 2) {
-      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
       store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
       store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
       __syncthreads();
-      mfma_substep<NS>(Ap[1], Bp[1], 0, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 0, acc);
       store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
       store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
-      mfma_substep<NS>(Ap[1], Bp[1], 16, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
       __syncthreads();
@@ -839,15 +872,15 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
     // one or two slabs remain: slab sl in buffer 0, slab sl + 1 in (ra1, rb1)
     int last = 0;
     if (sl + 1 < nslab) {
-      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
       store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
       store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
       __syncthreads();
       last = 1;
     }
-    mfma_substep<NS>(Ap[last], Bp[last], 0, acc);
-    mfma_substep<NS>(Ap[last], Bp[last], 16, acc);
+    mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 0, acc);
+    mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 16, acc);
   } else {
     for (int sl = 0; sl < nslab; ++sl) {
       __syncthreads();
@@ -857,12 +890,12 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
       const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
       load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
       load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
-      mfma_substep<NS>(Ap[0], Bp[0], 0, acc);
-      mfma_substep<NS>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
     }
   }
   }
-  gemm_epilogue<MODE>(g, s, task, acc);
+  gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc);
 }
 
 // The interior tiles of row-major (T0) and wide-stored (T1) matrices share one
@@ -900,6 +933,8 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
                                               __bf16 (*Bp)[NS][kBig][kLdsK]) {
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
+  // update tiles of row-major X' accumulate transposed blocks (16-byte stores)
+  constexpr bool kSwap = MODE == kUpdate && LAYOUT == kFastT0;
   const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
   floatx16 acc[4][2];
   gemm_acc_init<MODE, 4, 4>(g, s, acc);
@@ -919,17 +954,17 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
       __syncthreads();
       for (int sl = 0; sl + 1 < nslab; ++sl) {
         const int cur = sl & 1;
-        mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 0, acc);
+        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 0, acc);
         store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
         store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
-        mfma_substep<NS, 4, 4, kBig>(Ap[cur], Bp[cur], 16, acc);
+        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 16, acc);
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
         __syncthreads();
       }
       const int last = (nslab - 1) & 1;
-      mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 0, acc);
-      mfma_substep<NS, 4, 4, kBig>(Ap[last], Bp[last], 16, acc);
+      mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 0, acc);
+      mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 16, acc);
     } else {
       for (int sl = 0; sl < nslab; ++sl) {
         __syncthreads();
@@ -938,12 +973,12 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
         __syncthreads();
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 1), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 1), s.j0, rb);
-        mfma_substep<NS, 4, 4, kBig>(Ap[0], Bp[0], 0, acc);
-        mfma_substep<NS, 4, 4, kBig>(Ap[0], Bp[0], 16, acc);
+        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 0, acc);
+        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 16, acc);
       }
     }
   }
-  gemm_epilogue<MODE, 4, 4>(g, s, task, acc);
+  gemm_epilogue<MODE, 4, 4, kSwap, true>(g, s, task, acc);
 }
 
 template <int MODE, int NS, int LAYOUT, bool SCALED>
