@@ -231,6 +231,8 @@ constexpr int kXcds = 8;
 // evenly, and these phases ran slower than on 128 x 128 tiles; the update
 // (9 to 375 tiles per matrix) uses them.
 constexpr bool kBigGram = false;
+// Most K slices of a split Gram (see plan_matrices).
+constexpr int64_t kMaxKSlices = 6;
 
 std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<Task>& in, bool by_slice) {
   struct Group {
@@ -351,14 +353,14 @@ void plan_matrices(isoloco_plan_s* p) {
     mi.sq_off = sq;
     mi.vec = (mi.m % 4 == 0 && mi.n % 4 == 0) ? 1 : 0;
     mi.tensor = (int32_t)t;
-    const int64_t tiles = (mi.n + kBM - 1) / kBM;
-    // Split the Gram's K dimension when the matrix has few output tiles and
-    // a long K, so that no single tile dominates the launch.
+    // Split the Gram's K dimension of a tall matrix (few output tiles, long
+    // K) so that no single tile dominates the launch.  Every slice writes an
+    // n x n partial that is read back once, so the count stays small: six
+    // slices measured fastest for the 32000 x 768 embedding (four leave the
+    // launch's tail too long, eight and more add partial traffic).
     int ks = 1;
-    if (mi.m >= 4 * mi.n && mi.m > 4096) {
-      ks = (int)std::min<int64_t>((1024 + tiles * tiles - 1) / (tiles * tiles), (mi.m + 1023) / 1024);
-      ks = std::max(ks, 1);
-    }
+    if (mi.m >= 4 * mi.n && mi.m > 4096)
+      ks = (int)std::min<int64_t>(kMaxKSlices, (mi.m + 1023) / 1024);
     int64_t kchunk = (mi.m + ks - 1) / ks;
     kchunk = (kchunk + 31) / 32 * 32;  // whole K slabs of both product kernels
     ks = (int)((mi.m + kchunk - 1) / kchunk);
