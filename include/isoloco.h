@@ -30,7 +30,9 @@
  * Asynchrony.  isoloco_aggregate() only enqueues work on the caller's HIP
  * stream and returns; buffers must stay valid until the stream passes that
  * point.  One plan must not be used by two streams at once; distinct plans
- * are independent.
+ * are independent.  The call issues kernel launches only (no host
+ * synchronisation, memset or allocation), so it may be captured in a HIP
+ * graph; every replay then repeats the step on the same buffers.
  *
  * Errors.  Every function returns an isoloco_status; no C++ exception crosses
  * this boundary.  A call that fails validation enqueues nothing.  The last

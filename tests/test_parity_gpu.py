@@ -444,3 +444,54 @@ def test_single_phase_schedule(iso, precision):
     from workload import custom_layout
     lay, n = custom_layout(RAGGED, align=4)
     _run_and_compare(iso, _cfg(lay, n, K=3), seed=9, opts=dict(ell_fast=-1.0, precision=precision))
+
+
+@pytest.mark.parametrize("variant", [None, {"clip": "high"}], ids=["exact", "clip_high"])
+def test_graph_capture_replays(iso, variant):
+    """The step only enqueues kernels on the caller's stream (no host sync, no
+    memset, no allocation), so it can be captured in a HIP graph: every replay,
+    with eager steps and synchronisations in between, must equal the eager
+    result bit for bit."""
+    from workload import ReplicaGenerator, custom_layout
+    lay, n = custom_layout(RAGGED + [(520, 130, KIND_ISO)], align=4)
+    cfg = _cfg(lay, n, K=3)
+    dev = torch.device("cuda", 0)
+    gen = ReplicaGenerator(cfg, seed=12, device=dev)
+    theta0, _ = gen.init_state()
+    workers = gen.workers(theta0, 1)
+    opts = variant_opts(variant) if variant else None
+    plan = iso.IsoLoCoPlan(lay, n, 3, iso.ISOLOCO_F32, opts=opts, device=dev)
+
+    def eager():
+        t, m = theta0.clone(), torch.zeros_like(theta0)
+        plan.aggregate(t, workers, m, 1.0, 0.7, 0.9)
+        torch.cuda.synchronize()
+        return t, m
+
+    t_ref, m_ref = eager()
+    theta, mom = theta0.clone(), torch.zeros_like(theta0)
+
+    def body():
+        theta.copy_(theta0)
+        mom.zero_()
+        plan.aggregate(theta, workers, mom, 1.0, 0.7, 0.9)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        body()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        body()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        print("replay %d" % rep, flush=True)
+        assert torch.equal(theta, t_ref) and torch.equal(mom, m_ref), rep
+        t_e, m_e = eager()
+        assert torch.equal(t_e, t_ref) and torch.equal(m_e, m_ref), rep
+    del graph
+    plan.close()
