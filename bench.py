@@ -28,8 +28,8 @@ PEAK_BF16_MFMA_TFS = 2500.0  # MI355X dense bf16 matrix, TFLOP/s
 
 # Part products per fp32 product for each precision mode: (update products of
 # the first 3 steps, every other product).  Mixed runs the early updates in
-# bf16x6 and everything else in bf16x3.
-PARTS = {"mixed": (6, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
+# bf16x5 and everything else in bf16x3.
+PARTS = {"mixed": (5, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
 X6_STEPS = 3
 
 
@@ -41,7 +41,7 @@ def gemm_flops_per_step(layout, stats, check, precision):
     polynomial A A (n (n+1) n) and the update X P (2 m n^2).  A matrix that took
     s steps forms s + 1 Grams with the check (the last one measures Q^T Q), s
     polynomials and s updates.  Split-bf16 products issue one MFMA product per
-    part product (3 or 6)."""
+    part product (3, 5 or 6)."""
     early, late = PARTS[precision]
     f = 0
     fm = 0

@@ -92,8 +92,9 @@ typedef struct {
                         products split every fp32 operand into 2 (bf16x3: 3 bf16 MFMA
                         products, about 2^-16 relative error) or 3 (bf16x6: 6 products,
                         about fp32 accuracy) bfloat16 parts and accumulate in fp32.
-                        MIXED (default): bf16x6 for the update products of the first
-                        3 steps, bf16x3 for every other product                          */
+                        MIXED (default): the update products X P of the first 3 steps
+                        in bf16x5 (X in 3 parts, P in 2: 5 products, about the accuracy
+                        of bf16x6 for this product), bf16x3 for every other product      */
   float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
                         whose Q^T Q is then the identity to 5e-5 stops there, the others run the
                         continuation that reaches [ell0, 1] (default 1e-4; a negative value

@@ -65,13 +65,17 @@ constexpr double kCushion = 0.1;
 // within about half this value of the exact one)
 constexpr float kSwitchTol = 5e-5f;
 // In the mixed precision mode the update products of the first kX6Steps steps
-// use bf16x6, everything else bf16x3.  Those early updates X' = X P' carry
-// the large coefficients of the steps that amplify the small singular values
-// (P' holds a I + b A + c A^2 with |a| + |b| + |c| far above |p|), so their
-// rounding in the directions of small singular values is amplified the most;
-// the Gram and polynomial products of the same steps are as accurate in
-// bf16x3 (emulation of the iteration on spectra down to 1e-6: the same error
-// as bf16x6 updates with bf16x6 everywhere, within 5%).
+// use bf16x5 (X in 3 bf16 parts, P' in 2), everything else bf16x3.  Those
+// early updates X' = X P' carry the large coefficients of the steps that
+// amplify the small singular values (P' holds a I + b A + c A^2 with
+// |a| + |b| + |c| far above |p|), so the rounding of X, which reaches the
+// directions of small singular values at the size of the largest ones, is
+// amplified the most; the rounding of P' reaches each direction in
+// proportion to its singular value and needs no third part, and the Gram and
+// polynomial products of the same steps are as accurate in bf16x3
+// (emulation of the iteration on spectra down to 1e-6: the same error as
+// bf16x6 everywhere, within 5%; a third part for P' instead of X loses a
+// factor 10).
 constexpr int kX6Steps = 3;
 enum Product { kProdGram = 0, kProdPoly = 1, kProdUpdate = 2 };
 
@@ -80,7 +84,7 @@ int step_arith(int precision, int k, int product) {
     case ISOLOCO_PREC_FP32: return kArithFp32;
     case ISOLOCO_PREC_BF16X3: return kArithBf16x3;
     case ISOLOCO_PREC_BF16X6: return kArithBf16x6;
-    default: return (product == kProdUpdate && k < kX6Steps) ? kArithBf16x6 : kArithBf16x3;
+    default: return (product == kProdUpdate && k < kX6Steps) ? kArithBf16x5 : kArithBf16x3;
   }
 }
 constexpr double kSafety = 1.02;

@@ -59,7 +59,7 @@ struct StepArgs {
 };
 
 // Arithmetic of one batched-product launch.
-enum Arith { kArithBf16x3 = 0, kArithBf16x6 = 1, kArithFp32 = 2 };
+enum Arith { kArithBf16x3 = 0, kArithBf16x6 = 1, kArithFp32 = 2, kArithBf16x5 = 3 };
 
 struct PolarStep {
   const float* xin;

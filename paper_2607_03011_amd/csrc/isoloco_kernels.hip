@@ -587,16 +587,17 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Split-bfloat16 main loop (bf16x3 and bf16x6)
+// Split-bfloat16 main loop (bf16x3, bf16x5 and bf16x6)
 // ---------------------------------------------------------------------------
 //
 // Each fp32 operand x is split into NS bfloat16 parts, x = x0 + x1 (+ x2) + r,
 // x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1), round to nearest
 // even, so |r| <= 2^-16 |x| for NS = 2 and 2^-24 |x| for NS = 3.  The product
-// sum_k a_k b_k is accumulated in fp32 over the part products whose order
-// (a_i b_j with i + j < NS) is kept:
-//   NS = 2 (bf16x3):  a1 b0 + a0 b1 + a0 b0
-//   NS = 3 (bf16x6):  a2 b0 + a1 b1 + a0 b2 + a1 b0 + a0 b1 + a0 b0
+// sum_k a_k b_k is accumulated in fp32 over the part products of order
+// i + j <= 2 that both splits provide:
+//   bf16x3 (2 + 2 parts):  a1 b0 + a0 b1 + a0 b0
+//   bf16x5 (3 + 2 parts):  a2 b0 + a1 b1 + a1 b0 + a0 b1 + a0 b0
+//   bf16x6 (3 + 3 parts):  a2 b0 + a1 b1 + a0 b2 + a1 b0 + a0 b1 + a0 b0
 // on v_mfma_f32_32x32x16_bf16.  K is staged in slabs of 32: fp32 global loads
 // into registers (next slab in flight during the current slab's products),
 // split, and stored to LDS as NS bf16 planes per operand in [row][k] order, so
@@ -774,53 +775,78 @@ __device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[
   else slab32_store<NS, SCALED, ROWS>(r, planes, scale);
 }
 
+// Split-bf16 arithmetic with NP part products per fp32 product: NP = 3
+// (bf16x3: both operands in 2 parts, products of part orders 0 + 0, 0 + 1,
+// 1 + 0), NP = 6 (bf16x6: 3 parts each, all orders up to 2) and NP = 5 (left
+// operand in 3 parts, right operand in 2: the orders up to 2 without the
+// right operand's third part).  NP = 5 serves the update X' = X P': a
+// rounding error of X enters every direction of X' with the size of X's
+// largest singular values, while an error of P' enters the component of
+// each singular direction in proportion to its singular value, so the left
+// factor needs the third part and the right factor does not.
+template <int NP>
+struct SplitParts {
+  static_assert(NP == 3 || NP == 5 || NP == 6, "bf16x3, bf16x5 or bf16x6");
+  static constexpr int a = NP == 3 ? 2 : 3;   // planes of the left operand
+  static constexpr int b = NP == 6 ? 3 : 2;   // planes of the right operand
+  static constexpr int nb = NP == 3 ? 2 : 1;  // LDS buffers (double-buffered bf16x3)
+};
+
 // One k16 substep of a wave's (32 NA) x 64 tile: read the operand fragments
-// of the NS planes from LDS and issue the part products (smallest order
-// first).  WNC waves span the block's columns (wm = wave / WNC, wn = wave % WNC).
-// SWAP: issue each product as B A instead of A B, so that the accumulators
-// hold the transposed 32 x 32 blocks (4 consecutive output columns per lane).
-template <int NS, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false>
+// of the NSA / NSB planes from LDS and issue the part products (smallest
+// order first).  WNC waves span the block's columns (wm = wave / WNC,
+// wn = wave % WNC).  SWAP: issue each product as B A instead of A B, so that
+// the accumulators hold the transposed 32 x 32 blocks (4 consecutive output
+// columns per lane).
+template <int NSA, int NSB, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false>
 __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], const __bf16 (*Bp)[ROWS][kLdsK],
                                              int kk, floatx16 (&acc)[NA][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WNC, wn = wave % WNC;
   const int kc = kk + 8 * (lane >> 5);
-  bf16x8 av[NA][NS], bv[2][NS];
+  constexpr int kMaxOrd = (NSA > NSB ? NSA : NSB) - 1;
+  bf16x8 av[NA][NSA], bv[2][NSB];
 #pragma unroll
   for (int a = 0; a < NA; ++a) {
     const int row = wm * 32 * NA + a * 32 + (lane & 31);
 #pragma unroll
-    for (int p = 0; p < NS; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
+    for (int p = 0; p < NSA; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
   }
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int row = wn * 64 + b * 32 + (lane & 31);
 #pragma unroll
-    for (int p = 0; p < NS; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
+    for (int p = 0; p < NSB; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
   }
 #pragma unroll
   for (int a = 0; a < NA; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int ord = NS - 1; ord >= 0; --ord)
+      for (int ord = kMaxOrd; ord >= 0; --ord)
 #pragma unroll
-        for (int pa = ord; pa >= 0; --pa)
-          acc[a][b] = SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b][ord - pa], av[a][pa], acc[a][b], 0, 0, 0)
-                           : __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][ord - pa], acc[a][b], 0, 0, 0);
+        for (int pa = ord; pa >= 0; --pa) {
+          const int pb = ord - pa;
+          if (pa >= NSA || pb >= NSB) continue;
+          acc[a][b] = SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b][pb], av[a][pa], acc[a][b], 0, 0, 0)
+                           : __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][pb], acc[a][b], 0, 0, 0);
+        }
 }
 
-// bf16x3 (NS = 2) double-buffers the LDS slabs: while the products of slab s
+// bf16x3 (NP = 3) double-buffers the LDS slabs: while the products of slab s
 // run from one buffer, slab s + 1 is split and stored into the other and the
 // global loads of slab s + 2 are in flight; one barrier per slab, and the
 // steady-state loop body is a single basic block (the look-ahead slab index
 // is clamped to the last slab instead of branching), so that the compiler can
-// interleave the split arithmetic with the matrix products.  bf16x6 (NS = 3)
-// needs 1.5x the LDS per buffer and keeps a single buffer with two barriers.
+// interleave the split arithmetic with the matrix products.  bf16x5 and
+// bf16x6 need 1.25x and 1.5x the LDS per buffer and keep a single buffer
+// with two barriers.
 // SCALED: the X operands are multiplied by the first step's 1/||Delta||_F.
-template <int MODE, int NS, int LAYOUT, bool SCALED, int NB>
-__device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[NS][kBM][kLdsK],
-                                          __bf16 (*Bp)[NS][kBN][kLdsK]) {
+template <int MODE, int NP, int LAYOUT, bool SCALED>
+__device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
+                                          __bf16 (*Ap)[SplitParts<NP>::a][kBM][kLdsK],
+                                          __bf16 (*Bp)[SplitParts<NP>::b][kBN][kLdsK]) {
+  constexpr int kNa = SplitParts<NP>::a, kNb = SplitParts<NP>::b, NB = SplitParts<NP>::nb;
   // only X operands carry a scale (Gram: both, Update: A)
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
@@ -847,24 +873,24 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
     Slab32 ra1, rb1;
     load_operand<MODE, LAYOUT, true>(s.A, kat(1), s.i0, ra1);
     load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
-    store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
-    store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
+    store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
+    store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
     load_operand<MODE, LAYOUT, true>(s.A, kat(2), s.i0, ra);
     load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
     __syncthreads();
     int sl = 0;
     for (; sl + 2 < nslab; sl += 2) {
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
-      store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
       __syncthreads();
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 0, acc);
-      store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 16, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 0, acc);
+      store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
       load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
       __syncthreads();
@@ -872,26 +898,26 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
     // one or two slabs remain: slab sl in buffer 0, slab sl + 1 in (ra1, rb1)
     int last = 0;
     if (sl + 1 < nslab) {
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
-      store_operand<MODE, LAYOUT, true, NS, SA>(ra1, Ap[1], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
       __syncthreads();
       last = 1;
     }
-    mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 0, acc);
-    mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 16, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 0, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 16, acc);
   } else {
     for (int sl = 0; sl < nslab; ++sl) {
       __syncthreads();
-      store_operand<MODE, LAYOUT, true, NS, SA>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
       __syncthreads();
       const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
       load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
       load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
-      mfma_substep<NS, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
     }
   }
   }
@@ -901,18 +927,18 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task, _
 // The interior tiles of row-major (T0) and wide-stored (T1) matrices share one
 // launch (kFastAny picks the loaders per task), so that neither layout class
 // forms a launch of its own with a ragged tail.
-template <int MODE, int NS, int LAYOUT, bool SCALED>
+template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
-  constexpr int NB = NS == 2 ? 2 : 1;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBM][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBN][kLdsK];
+  constexpr int NB = SplitParts<NP>::nb;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][SplitParts<NP>::a][kBM][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][SplitParts<NP>::b][kBN][kLdsK];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   if constexpr (LAYOUT == kFastAny) {
-    if (g.mats[task.mat].trans) bf16_tile<MODE, NS, kFastT1, SCALED, NB>(g, task, Ap, Bp);
-    else bf16_tile<MODE, NS, kFastT0, SCALED, NB>(g, task, Ap, Bp);
+    if (g.mats[task.mat].trans) bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
+    else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
   } else {
-    bf16_tile<MODE, NS, LAYOUT, SCALED, NB>(g, task, Ap, Bp);
+    bf16_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
   }
 }
 
@@ -923,14 +949,16 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
 // LDS (2 buffers x 2 planes x 512 rows x 80 bytes: the whole 160 KB of the
 // CU) with one slab in flight in registers (issued after the split of the
 // previous one, landing during the second half of the current slab's
-// products); bf16x6 keeps one buffer of 3 planes (120 KB) and two barriers
-// per slab.
+// products); bf16x5 and bf16x6 keep one buffer of 3 + 2 or 3 + 3 planes
+// (100 or 120 KB) and two barriers per slab.
 constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 
-template <int MODE, int NS, int LAYOUT, bool SCALED, int NB>
-__device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task, __bf16 (*Ap)[NS][kBig][kLdsK],
-                                              __bf16 (*Bp)[NS][kBig][kLdsK]) {
+template <int MODE, int NP, int LAYOUT, bool SCALED>
+__device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task,
+                                              __bf16 (*Ap)[SplitParts<NP>::a][kBig][kLdsK],
+                                              __bf16 (*Bp)[SplitParts<NP>::b][kBig][kLdsK]) {
+  constexpr int kNa = SplitParts<NP>::a, kNb = SplitParts<NP>::b, NB = SplitParts<NP>::nb;
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
   // update tiles of row-major X' accumulate transposed blocks (16-byte stores)
@@ -947,52 +975,52 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
     load_operand<MODE, LAYOUT, true, kBig>(s.A, s.k_begin, s.i0, ra);
     load_operand<MODE, LAYOUT, false, kBig>(s.B, s.k_begin, s.j0, rb);
     if constexpr (NB == 2) {
-      store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[0], s.B.scale);
       load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
       load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
       __syncthreads();
       for (int sl = 0; sl + 1 < nslab; ++sl) {
         const int cur = sl & 1;
-        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 0, acc);
-        store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
-        store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
-        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 16, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 0, acc);
+        store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
+        store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 16, acc);
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
         __syncthreads();
       }
       const int last = (nslab - 1) & 1;
-      mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 0, acc);
-      mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 16, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 0, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 16, acc);
     } else {
       for (int sl = 0; sl < nslab; ++sl) {
         __syncthreads();
-        store_operand<MODE, LAYOUT, true, NS, SA, kBig>(ra, Ap[0], s.A.scale);
-        store_operand<MODE, LAYOUT, false, NS, SB, kBig>(rb, Bp[0], s.B.scale);
+        store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[0], s.A.scale);
+        store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[0], s.B.scale);
         __syncthreads();
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 1), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 1), s.j0, rb);
-        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 0, acc);
-        mfma_substep<NS, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 16, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 0, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 16, acc);
       }
     }
   }
   gemm_epilogue<MODE, 4, 4, kSwap, true>(g, s, task, acc);
 }
 
-template <int MODE, int NS, int LAYOUT, bool SCALED>
+template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
-  constexpr int NB = NS == 2 ? 2 : 1;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][NS][kBig][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][NS][kBig][kLdsK];
+  constexpr int NB = SplitParts<NP>::nb;
+  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][SplitParts<NP>::a][kBig][kLdsK];
+  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][SplitParts<NP>::b][kBig][kLdsK];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   if constexpr (LAYOUT == kFastAny) {
-    if (g.mats[task.mat].trans) bf16_big_tile<MODE, NS, kFastT1, SCALED, NB>(g, task, Ap, Bp);
-    else bf16_big_tile<MODE, NS, kFastT0, SCALED, NB>(g, task, Ap, Bp);
+    if (g.mats[task.mat].trans) bf16_big_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
+    else bf16_big_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
   } else {
-    bf16_big_tile<MODE, NS, LAYOUT, SCALED, NB>(g, task, Ap, Bp);
+    bf16_big_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
   }
 }
 
@@ -1228,7 +1256,7 @@ hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fi
   return hipGetLastError();
 }
 
-template <int MODE, int NS, bool SCALED>
+template <int MODE, int NP, bool SCALED>
 static void launch_bf16_segments(const Task* tasks, const int* off, const int* cnt, const GemmArgs& g0,
                                  hipStream_t st) {
   GemmArgs g = g0;
@@ -1237,47 +1265,47 @@ static void launch_bf16_segments(const Task* tasks, const int* off, const int* c
   // wide-stored tiles (then each has a launch of its own)
   if (cnt[0] && cnt[1]) {
     g.tasks = tasks + off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
   } else if (cnt[0]) {
     g.tasks = tasks + off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastAny, SCALED>), dim3(cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastAny, SCALED>), dim3(cnt[0]), block, 0, st, g);
   }
   if (cnt[1]) {
     g.tasks = tasks + off[1];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kFastT1, SCALED>), dim3(cnt[1]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastT1, SCALED>), dim3(cnt[1]), block, 0, st, g);
   }
   if (cnt[2]) {
     g.tasks = tasks + off[2];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NS, kGeneric, SCALED>), dim3(cnt[2]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kGeneric, SCALED>), dim3(cnt[2]), block, 0, st, g);
   }
 }
 
 // The 256 x 256 interior tiles, then the 128 x 128 tiles left over (for lists
 // without 256 x 256 tiles this is the plain 128 x 128 cover).
-template <int MODE, int NS, bool SCALED>
+template <int MODE, int NP, bool SCALED>
 static void launch_big_cover(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kBigThreads);
   if (L.big_cnt[0] && L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
   } else if (L.big_cnt[0]) {
     g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
   }
   if (L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[1];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NS, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
   }
-  launch_bf16_segments<MODE, NS, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
+  launch_bf16_segments<MODE, NP, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
 }
 
 // The first step's X operands carry the 1/||Delta||_F pre-scaling (Poly reads
 // only Gram outputs and never does).
-template <int MODE, int NS>
+template <int MODE, int NP>
 static void launch_bf16(const TaskList& L, const GemmArgs& g, hipStream_t st) {
-  if (MODE != kPoly && g.first) launch_big_cover<MODE, NS, MODE != kPoly>(L, g, st);
-  else launch_big_cover<MODE, NS, false>(L, g, st);
+  if (MODE != kPoly && g.first) launch_big_cover<MODE, NP, MODE != kPoly>(L, g, st);
+  else launch_big_cover<MODE, NP, false>(L, g, st);
 }
 
 template <int MODE>
@@ -1288,9 +1316,11 @@ static void launch_mode(const TaskList& L, const GemmArgs& g0, int arith, hipStr
     const int n = L.seg_cnt[0] + L.seg_cnt[1] + L.seg_cnt[2];
     if (n) hipLaunchKernelGGL(gemm_f32_kernel<MODE>, dim3(n), dim3(kGemmThreads), 0, st, g);
   } else if (arith == kArithBf16x6) {
-    launch_bf16<MODE, 3>(L, g0, st);
+    launch_bf16<MODE, 6>(L, g0, st);
+  } else if (MODE == kUpdate && arith == kArithBf16x5) {
+    launch_bf16<MODE, 5>(L, g0, st);
   } else {
-    launch_bf16<MODE, 2>(L, g0, st);
+    launch_bf16<MODE, 3>(L, g0, st);
   }
 }
 
