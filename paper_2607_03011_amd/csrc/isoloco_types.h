@@ -18,15 +18,17 @@ constexpr int kMaxWorkers = 128;
 
 // One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
 // element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
-// where (sr, sc) = (n, 1) if the tensor is stored with rows >= cols, and
-// (1, m) if it is stored wide (rows < cols, kept in its own row-major layout).
+// where (sr, sc) = (n, 1) for a tensor stored with rows > cols, and (1, m)
+// (column-major) for one stored wide (rows < cols, kept in its own row-major
+// layout) or square (its row-major bytes read column-major are its
+// transpose, whose polar factor is the transposed one: the same bytes).
 struct MatInfo {
   int64_t ws_off;    // element offset in the Delta / X buffers (64-element aligned)
   int64_t src_off;   // element offset in theta / momentum / workers
   int64_t sq_off;    // element offset of this matrix's n x n buffers (Gram, polynomial)
   int64_t part_off;  // element offset of the split-K Gram partials (ksplit * n * n)
   int32_t m, n;      // tall shape
-  int32_t trans;     // 1 if stored wide (rows < cols)
+  int32_t trans;     // 1: column-major in tall coordinates (stored wide or square)
   int32_t ksplit;    // number of K slices of the Gram product (1 = no split)
   int32_t kchunk;    // rows of X per K slice (multiple of kBK)
   int32_t vec;       // 1 if m and n are multiples of 4 (vector loads allowed)
