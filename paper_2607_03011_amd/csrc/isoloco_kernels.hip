@@ -334,7 +334,7 @@ struct GemmArgs {
 
 // Operands, output bounds and K range of one task.
 //   Gram:    C(i, j) = sum_k X[k][i] X[k][j]   over the task's K slice (C is n x n)
-//   Poly:    C(i, j) = sum_k A[k][i] A[k][j]   (A symmetric, so this is A A)
+//   Poly:    C(i, j) = sum_k A[i][k] A[j][k]   (A symmetric, so this is A A)
 //   Update:  C(i, j) = sum_k X[i][k] P[k][j]   (C is m x n, tall coordinates)
 struct GemmSetup {
   MatInfo mi;
@@ -372,7 +372,9 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     s.N = n;
   } else if (MODE == kPoly) {
     const float* a = g.gram + mi.sq_off;
-    s.A = {a, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
+    // A is symmetric (its diagonal tiles to rounding), so the operand A[k][i]
+    // is read as A[i][k]: k-contiguous rows, the faster loads
+    s.A = {a, 1, (int64_t)n, n, n, false, (n & 3) == 0, 1.f};
     s.B = s.A;
     s.M = n;
     s.N = n;
@@ -694,13 +696,14 @@ __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, S
 enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2, kFastAny = 3 };
 
 // Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
-// k-contiguous for wide storage (T1).  Poly: A[k][i], always i-contiguous.
-// Update: A = X[i][k] (k-contiguous for T0, i-contiguous for T1), B = P[k][j].
-// k-contiguous interior operands use the row mapping of the registers.
+// k-contiguous for column-major storage (T1).  Poly: A[k][i] read as A[i][k]
+// (symmetric), k-contiguous.  Update: A = X[i][k] (k-contiguous for T0,
+// i-contiguous for T1), B = P[k][j], i-contiguous.  k-contiguous interior
+// operands use the row mapping of the registers.
 template <int MODE, int LAYOUT, bool IS_A>
 struct OperandLayout {
   static constexpr bool icontig =
-      MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? true : (IS_A ? (LAYOUT == kFastT1) : true);
+      MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? false : (IS_A ? (LAYOUT == kFastT1) : true);
   static constexpr bool rowmap = LAYOUT != kGeneric && !icontig;
 };
 
