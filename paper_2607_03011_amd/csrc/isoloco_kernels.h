@@ -104,5 +104,9 @@ hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st);
 // replaces Delta in t.delta, Q is copied to t.x2, and the chunk partials of
 // ||E||^2 are left in t.part_sq for a second polar iteration (on E)
 hipError_t launch_clip_prep(const DevTables& t, hipStream_t st);
+// Clip variants, the correction D = alpha ((E -+ |E|) / 2 + sigma_bar Q) into
+// t.delta from E (t.delta), |E| (t.x[0]) and Q (t.x2); a.clip 1: high, 2: low.
+// The write-back then reads D from t.delta.
+hipError_t launch_clip_compose(const DevTables& t, const StepArgs& a, hipStream_t st);
 
 }  // namespace isoloco

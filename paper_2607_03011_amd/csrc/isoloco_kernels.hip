@@ -24,6 +24,7 @@ typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -71,6 +72,7 @@ struct WorkerLoad<0> {
   __device__ static __forceinline__ float one(const void* p, int64_t i) {
     return static_cast<const float*>(p)[i];
   }
+  __device__ static __forceinline__ void quad(const void* p, int64_t i, float* out) { vec(p, i, out); }
 };
 
 template <>
@@ -88,7 +90,93 @@ struct WorkerLoad<1> {
   __device__ static __forceinline__ float one(const void* p, int64_t i) {
     return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
   }
+  // four elements (8 bytes)
+  __device__ static __forceinline__ void quad(const void* p, int64_t i, float* out) {
+    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(static_cast<const uint16_t*>(p) + i));
+    out[0] = __uint_as_float(v[0] << 16);
+    out[1] = __uint_as_float(v[0] & 0xffff0000u);
+    out[2] = __uint_as_float(v[1] << 16);
+    out[3] = __uint_as_float(v[1] & 0xffff0000u);
+  }
 };
+
+// Workspace index of element i of a chunk (tiles: column by column).
+__device__ __forceinline__ int64_t chunk_ws(const Chunk& c, int i) {
+  return c.rows ? c.ws + (int64_t)(i / c.rows) * c.ws_ld + i % c.rows : c.ws + i;
+}
+
+// LDS staging of one tile between the stored (row-major) and the workspace
+// (column-major) layouts; the padded row keeps the column reads spread over
+// the banks.
+typedef float TileLds[kTileRows][kTileCols + 1];
+
+// Delta of a tile of a tall row-major tensor, written column-major: each
+// thread reduces 4 consecutive stored elements of a row (a wave covers two
+// rows of 128 columns), the tile goes through LDS, and each thread writes 4
+// consecutive rows of a column (eight threads per 128-byte column segment).
+// Returns the thread's share of sum Delta^2.
+template <int WDT>
+__device__ __forceinline__ double reduce_tile(const Chunk& c, const float* __restrict__ theta,
+                                              float* __restrict__ mom, float* __restrict__ delta,
+                                              const WorkerPtrs& w, int K, float inv_k, float mu, int heavy_ball,
+                                              int target_update, TileLds& tl) {
+  using WL = WorkerLoad<WDT>;
+  const int TR = c.rows, TC = c.cols;
+  double sq = 0.0;
+  for (int it = threadIdx.x; it < TR * (kTileCols / 4); it += kStreamThreads) {
+    const int rr = it / (kTileCols / 4), col = 4 * (it % (kTileCols / 4));
+    if (col >= TC) continue;
+    const int64_t e = c.src + (int64_t)rr * c.src_ld + col;
+    const int nq = min(4, TC - col);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f}, th[4] = {0.f, 0.f, 0.f, 0.f};
+    if (c.vec) {
+      const floatx4 t4 = *reinterpret_cast<const floatx4*>(theta + e);
+      th[0] = t4[0]; th[1] = t4[1]; th[2] = t4[2]; th[3] = t4[3];
+#pragma unroll 1
+      for (int k0 = 0; k0 < K; k0 += 8) {
+        float wv[8][4];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (k0 + j < K) WL::quad(w.p[k0 + j], e, wv[j]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (k0 + j < K) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[q] += th[q] - wv[j][q];
+          }
+      }
+    } else {
+      for (int q = 0; q < nq; ++q) {
+        th[q] = theta[e + q];
+        for (int k = 0; k < K; ++k) acc[q] += th[q] - WL::one(w.p[k], e + q);
+      }
+    }
+    for (int q = 0; q < nq; ++q) {
+      float a = acc[q] * inv_k;
+      if (target_update) {
+        // B <- mu B + Delta now; the polar input is the update itself
+        const float bn = mu * mom[e + q] + a;
+        mom[e + q] = bn;
+        a = heavy_ball ? bn : a + mu * bn;
+      }
+      tl[rr][col + q] = a;
+      sq += (double)a * a;
+    }
+  }
+  __syncthreads();
+  for (int it = threadIdx.x; it < TC * (kTileRows / 4); it += kStreamThreads) {
+    const int cc = it / (kTileRows / 4), r = 4 * (it % (kTileRows / 4));
+    if (r >= TR) continue;
+    float* dst = delta + c.ws + (int64_t)cc * c.ws_ld + r;
+    if (c.vec) {
+      const floatx4 o = {tl[r][cc], tl[r + 1][cc], tl[r + 2][cc], tl[r + 3][cc]};
+      *reinterpret_cast<floatx4*>(dst) = o;
+    } else {
+      for (int q = 0; q < 4 && r + q < TR; ++q) dst[q] = tl[r + q][cc];
+    }
+  }
+  return sq;
+}
 
 // Per element: Delta = (1/K) sum_k (theta - theta_k).  2-D (ISO) chunks store
 // Delta in the workspace and add Delta^2 to the chunk's partial; AVG chunks run
@@ -101,11 +189,16 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
   using WL = WorkerLoad<WDT>;
   constexpr int V = WL::kVec;
   __shared__ double red[4];
+  __shared__ TileLds tl;
   const Chunk c = chunks[blockIdx.x];
   const bool iso = c.mat >= 0;
   double sq = 0.0;
   int done = 0;
-  if (c.vec) {
+  if (c.rows) {
+    // a tile of a tall row-major tensor (always corrected): Delta column-major
+    sq = reduce_tile<WDT>(c, theta, mom, delta, w, K, inv_k, mu, heavy_ball, target_update, tl);
+    done = c.count;
+  } else if (c.vec) {
     const int nv = c.count / V;
     for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
       const int64_t e = c.src + (int64_t)v * V;
@@ -1098,7 +1191,9 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
   }
 }
 
-// <Q, Delta>_F partial per chunk of a corrected matrix.
+// <Q, Delta>_F partial per chunk of a corrected matrix (both in the
+// workspace layout: chunk_ws maps the chunk's elements; groups of 4 are
+// contiguous when c.vec).
 __global__ void __launch_bounds__(kStreamThreads)
 trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
              const float* __restrict__ x1, const float* __restrict__ delta, double* __restrict__ part_tr) {
@@ -1110,14 +1205,17 @@ trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc
   if (c.vec) {
     const int nv = c.count / 4;
     for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
-      const floatx4 a = *reinterpret_cast<const floatx4*>(q + c.ws + 4 * v);
-      const floatx4 d = *reinterpret_cast<const floatx4*>(delta + c.ws + 4 * v);
+      const int64_t o = chunk_ws(c, 4 * v);
+      const floatx4 a = *reinterpret_cast<const floatx4*>(q + o);
+      const floatx4 d = *reinterpret_cast<const floatx4*>(delta + o);
       s += (double)a[0] * d[0] + (double)a[1] * d[1] + (double)a[2] * d[2] + (double)a[3] * d[3];
     }
     done = nv * 4;
   }
-  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads)
-    s += (double)q[c.ws + i] * delta[c.ws + i];
+  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
+    const int64_t o = chunk_ws(c, i);
+    s += (double)q[o] * delta[o];
+  }
   s = block_sum256(s, red);
   if (threadIdx.x == 0) part_tr[blockIdx.x] = s;
 }
@@ -1137,38 +1235,80 @@ sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_t
   else if (o.flags & 2) o.sigma_bar = 0.f;
   else if (mode == 0) o.sigma_bar = (float)(s / mi.n);
   else if (mode == 1) o.sigma_bar = (float)((double)o.fro / sqrt((double)mi.n));
-  else o.sigma_bar = (float)(mi.trans ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
+  else o.sigma_bar = (float)(mi.wide ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
 }
 
-// D = alpha sigma_bar Q;  B <- mu B + D;  theta <- theta - lr (D + mu B)
+// One element of the write-back: D = f p;  B <- mu B + D;  theta <- theta - lr (D + mu B)
 // (heavy_ball: theta <- theta - lr B; target_update: B was updated by the
 // reduction and theta <- theta - lr D).
+__device__ __forceinline__ void finish_one(float* __restrict__ theta, float* __restrict__ mom, int64_t e, float d,
+                                           float lr, float mu, int heavy_ball, int target_update) {
+  if (target_update) {
+    theta[e] = theta[e] - lr * d;
+  } else {
+    const float bn = mu * mom[e] + d;
+    mom[e] = bn;
+    theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
+  }
+}
+
+__device__ __forceinline__ void finish_quad(float* __restrict__ theta, float* __restrict__ mom, int64_t e,
+                                            const floatx4& d, float lr, float mu, int heavy_ball, int target_update) {
+  floatx4 t = *reinterpret_cast<const floatx4*>(theta + e);
+  if (target_update) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) t[r] = t[r] - lr * d[r];
+  } else {
+    floatx4 b = *reinterpret_cast<const floatx4*>(mom + e);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float bn = mu * b[r] + d[r];
+      b[r] = bn;
+      t[r] = t[r] - lr * (heavy_ball ? bn : d[r] + mu * bn);
+    }
+    *reinterpret_cast<floatx4*>(mom + e) = b;
+  }
+  *reinterpret_cast<floatx4*>(theta + e) = t;
+}
+
+// The write-back of the corrected tensors (Algorithm 2): D = f P with P = Q
+// and f = alpha sigma_bar (clip variants: P is their correction, already
+// scaled, and f = 1).  A tile chunk reads its column-major P through LDS.
 __global__ void __launch_bounds__(kStreamThreads)
 finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
-              const float* __restrict__ x0, const float* __restrict__ x1, float* __restrict__ theta,
-              float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball, int target_update,
-              int clip, const float* __restrict__ ebuf, const float* __restrict__ qcopy) {
+              const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ dclip,
+              float* __restrict__ theta, float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball,
+              int target_update, int clip) {
+  __shared__ TileLds tl;
   const Chunk c = chunks[blockIdx.x];
   const MatScalars s = sc[c.mat];
-  const float* q = s.qbuf ? x1 : x0;
-  float f = alpha * s.sigma_bar;
+  const float* q = clip ? dclip : (s.qbuf ? x1 : x0);
+  float f = clip ? 1.f : alpha * s.sigma_bar;
   if (s.flags & 2) f = 0.f;
-  if (clip) {
-    // clip_high: D = alpha ((E - |E|) / 2 + sigma_bar Q), clip_low: (E + |E|) / 2,
-    // with E = Delta - sigma_bar Q (ebuf), |E| = Q (Q2^T E) (x0), Q copied to qcopy
-    const float sg = clip == 1 ? -0.5f : 0.5f;
-    const float sb = s.sigma_bar;
-    const float al = (s.flags & 2) ? 0.f : alpha;
-    for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
-      const int64_t e = c.src + i;
-      const float ev = ebuf[c.ws + i];
-      const float d = al * (0.5f * ev + sg * x0[c.ws + i] + sb * qcopy[c.ws + i]);
-      if (target_update) {
-        theta[e] = theta[e] - lr * d;
+  if (c.rows) {
+    const int TR = c.rows, TC = c.cols;
+    for (int it = threadIdx.x; it < TC * (kTileRows / 4); it += kStreamThreads) {
+      const int cc = it / (kTileRows / 4), r = 4 * (it % (kTileRows / 4));
+      if (r >= TR) continue;
+      const float* src = q + c.ws + (int64_t)cc * c.ws_ld + r;
+      if (c.vec) {
+        const floatx4 v = *reinterpret_cast<const floatx4*>(src);
+        tl[r][cc] = v[0]; tl[r + 1][cc] = v[1]; tl[r + 2][cc] = v[2]; tl[r + 3][cc] = v[3];
       } else {
-        const float bn = mu * mom[e] + d;
-        mom[e] = bn;
-        theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
+        for (int k = 0; k < 4 && r + k < TR; ++k) tl[r + k][cc] = src[k];
+      }
+    }
+    __syncthreads();
+    for (int it = threadIdx.x; it < TR * (kTileCols / 4); it += kStreamThreads) {
+      const int rr = it / (kTileCols / 4), col = 4 * (it % (kTileCols / 4));
+      if (col >= TC) continue;
+      const int64_t e = c.src + (int64_t)rr * c.src_ld + col;
+      if (c.vec) {
+        const floatx4 d = {f * tl[rr][col], f * tl[rr][col + 1], f * tl[rr][col + 2], f * tl[rr][col + 3]};
+        finish_quad(theta, mom, e, d, lr, mu, heavy_ball, target_update);
+      } else {
+        for (int k = 0; k < 4 && col + k < TC; ++k)
+          finish_one(theta, mom, e + k, f * tl[rr][col + k], lr, mu, heavy_ball, target_update);
       }
     }
     return;
@@ -1177,42 +1317,18 @@ finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ s
   if (c.vec) {
     const int nv = c.count / 4;
     for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
-      const int64_t e = c.src + 4 * v;
       const floatx4 qq = *reinterpret_cast<const floatx4*>(q + c.ws + 4 * v);
-      floatx4 t = *reinterpret_cast<const floatx4*>(theta + e);
-      if (target_update) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) t[r] = t[r] - lr * (f * qq[r]);
-      } else {
-        floatx4 b = *reinterpret_cast<const floatx4*>(mom + e);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float d = f * qq[r];
-          const float bn = mu * b[r] + d;
-          b[r] = bn;
-          t[r] = t[r] - lr * (heavy_ball ? bn : d + mu * bn);
-        }
-        *reinterpret_cast<floatx4*>(mom + e) = b;
-      }
-      *reinterpret_cast<floatx4*>(theta + e) = t;
+      finish_quad(theta, mom, c.src + 4 * v, f * qq, lr, mu, heavy_ball, target_update);
     }
     done = nv * 4;
   }
-  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
-    const int64_t e = c.src + i;
-    const float d = f * q[c.ws + i];
-    if (target_update) {
-      theta[e] = theta[e] - lr * d;
-    } else {
-      const float bn = mu * mom[e] + d;
-      mom[e] = bn;
-      theta[e] = theta[e] - lr * (heavy_ball ? bn : d + mu * bn);
-    }
-  }
+  for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads)
+    finish_one(theta, mom, c.src + i, f * q[c.ws + i], lr, mu, heavy_ball, target_update);
 }
 
 // Clip variants, first half: E = Delta - sigma_bar Q in place of Delta, Q
-// copied aside, and the chunk partials of ||E||^2 for the second iteration.
+// copied aside, and the chunk partials of ||E||^2 for the second iteration
+// (all in the workspace layout).
 __global__ void __launch_bounds__(kStreamThreads)
 clip_prep_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
                  const float* __restrict__ x1, float* __restrict__ delta, float* __restrict__ qcopy,
@@ -1224,14 +1340,33 @@ clip_prep_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict_
   const float sb = s.flags ? 0.f : s.sigma_bar;
   double sq = 0.0;
   for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
-    const float qv = q[c.ws + i];
-    const float ev = delta[c.ws + i] - sb * qv;
-    delta[c.ws + i] = ev;
-    qcopy[c.ws + i] = qv;
+    const int64_t o = chunk_ws(c, i);
+    const float qv = q[o];
+    const float ev = delta[o] - sb * qv;
+    delta[o] = ev;
+    qcopy[o] = qv;
     sq += (double)ev * ev;
   }
   sq = block_sum256(sq, red);
   if (threadIdx.x == 0) part_sq[blockIdx.x] = sq;
+}
+
+// Clip variants, the correction in the workspace layout, in place of E:
+// clip_high D = alpha ((E - |E|) / 2 + sigma_bar Q), clip_low alpha ((E + |E|) / 2
+// + sigma_bar Q), with E = Delta - sigma_bar Q (delta), |E| = Q (Q2^T E) (x0)
+// and Q (qcopy).
+__global__ void __launch_bounds__(kStreamThreads)
+clip_compose_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
+                    const float* __restrict__ qcopy, float* __restrict__ delta, float alpha, int clip) {
+  const Chunk c = chunks[blockIdx.x];
+  const MatScalars s = sc[c.mat];
+  const float sg = clip == 1 ? -0.5f : 0.5f;
+  const float sb = s.sigma_bar;
+  const float al = (s.flags & 2) ? 0.f : alpha;
+  for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
+    const int64_t o = chunk_ws(c, i);
+    delta[o] = al * (0.5f * delta[o] + sg * x0[o] + sb * qcopy[o]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1383,8 +1518,15 @@ hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (t.n_iso_chunks == 0) return hipSuccess;
   hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
-                     t.x[0], t.x[1], a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update, a.clip,
-                     t.delta, t.x2);
+                     t.x[0], t.x[1], t.delta, a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update,
+                     a.clip);
+  return hipGetLastError();
+}
+
+hipError_t launch_clip_compose(const DevTables& t, const StepArgs& a, hipStream_t st) {
+  if (t.n_iso_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(clip_compose_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+                     t.x[0], t.x2, t.delta, a.alpha, a.clip);
   return hipGetLastError();
 }
 

@@ -18,34 +18,46 @@ constexpr int kMaxWorkers = 128;
 
 // One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
 // element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
-// where (sr, sc) = (n, 1) for a tensor stored with rows > cols, and (1, m)
-// (column-major) for one stored wide (rows < cols, kept in its own row-major
-// layout) or square (its row-major bytes read column-major are its
-// transpose, whose polar factor is the transposed one: the same bytes).
+// with (sr, sc) = (n, 1) if trans == 0 and (1, m) (column-major) if trans ==
+// 1, which the planner sets for every matrix: a tensor stored wide is then in
+// its own row-major layout, a square one in its row-major bytes (read
+// column-major they are its transpose, whose polar factor is the transposed
+// one: the same bytes), and a tall one (rows > cols) is transposed tile by
+// tile by the streaming kernels.
 struct MatInfo {
   int64_t ws_off;    // element offset in the Delta / X buffers (64-element aligned)
   int64_t src_off;   // element offset in theta / momentum / workers
   int64_t sq_off;    // element offset of this matrix's n x n buffers (Gram, polynomial)
   int64_t part_off;  // element offset of the split-K Gram partials (ksplit * n * n)
   int32_t m, n;      // tall shape
-  int32_t trans;     // 1: column-major in tall coordinates (stored wide or square)
+  int32_t trans;     // 1: column-major in tall coordinates
   int32_t ksplit;    // number of K slices of the Gram product (1 = no split)
   int32_t kchunk;    // rows of X per K slice (multiple of kBK)
   int32_t vec;       // 1 if m and n are multiples of 4 (vector loads allowed)
   int32_t tensor;    // index in the caller's layout
   int32_t chunk_begin, chunk_end;  // range of this matrix in the chunk table
-  int32_t pad0;
+  int32_t wide;      // 1 if the tensor is stored wide (rows < cols)
 };
 
-// A contiguous run of at most kChunk elements of one tensor.
+// Work item of the streaming kernels: at most kChunk elements of one tensor.
+// rows == 0: a contiguous run, element i at src + i (stored) and ws + i
+// (workspace).  rows > 0: a rows x cols tile (rows <= kTileRows, cols <=
+// kTileCols) of a tall tensor stored row-major and iterated column-major:
+// element (r, c) of the tile at src + r * src_ld + c as stored and at
+// ws + c * ws_ld + r in the workspace.
 struct Chunk {
   int64_t src;    // first element, index into theta / momentum / workers
   int64_t ws;     // first element in the workspace buffers (-1 for AVG tensors)
   int32_t count;  // elements
   int32_t mat;    // matrix index, or -1 for AVG tensors
-  int32_t vec;    // 1 if src (and ws) allow 16-byte vector access of every stream
+  int32_t vec;    // 1 if every stream allows 16-byte vector access (runs: from src and ws;
+                  // tiles: rows, cols, src_ld and ws_ld multiples of 4 and aligned starts)
+  int32_t rows, cols;     // tile shape (rows == 0: a contiguous run)
+  int32_t src_ld, ws_ld;  // tile strides: the tensor's columns, the iterate's rows
   int32_t pad;
 };
+constexpr int kTileRows = 32;
+constexpr int kTileCols = 128;
 
 // Per-matrix scalars kept in the workspace.
 struct MatScalars {
