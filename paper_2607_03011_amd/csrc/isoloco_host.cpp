@@ -441,10 +441,12 @@ void plan_matrices(isoloco_plan_s* p) {
   p->npart = part;
 
   // Work lists, longest tasks first, each in three segments (interior tiles of
-  // row-major matrices, interior tiles of wide-stored matrices, ragged tiles),
-  // each segment reordered for the XCD round robin of the dispatcher.  Next to
-  // this cover by 128 x 128 tiles, the bf16x3 steps use interior 256 x 256
-  // tiles where a matrix has them and 128 x 128 tiles for the rest.
+  // row-major iterates, interior tiles of column-major iterates, ragged
+  // tiles), each segment reordered for the XCD round robin of the dispatcher.
+  // Next to this cover by 128 x 128 tiles, the split-bf16 kernels use
+  // interior 256 x 256 tiles where a matrix has them and 128 x 128 tiles for
+  // the rest.  (The planner makes every iterate column-major; the kernels
+  // take either layout, per task in the shared segment 0.)
   std::vector<Task> seg[3], big[2], rem[3];
   auto flush = [&](TaskListHost& L, bool by_slice) {
     L.tasks.clear();
@@ -462,12 +464,12 @@ void plan_matrices(isoloco_plan_s* p) {
   // The interior kernels address a matrix with 32-bit byte offsets: matrices
   // of 2^29 elements or more take the generic kernel.
   auto fast_ok = [](const MatInfo& M) { return M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29); };
-  // Interior tiles of wide-stored matrices go to segment 1 of the update
-  // list (a launch of their own) and share segment 0 with the row-major ones
-  // in the Gram and polynomial lists (one launch; the kernel picks the
-  // loaders per task): the choices measured fastest (one Gram launch: 0.1 ms
-  // per outer step faster on the 109.5M workload; one update launch: 0.5 ms
-  // slower).
+  // Interior tiles of column-major iterates go to segment 1 of the update
+  // list (a launch of their own) and share segment 0 with row-major ones in
+  // the Gram and polynomial lists (one launch; the kernel picks the loaders
+  // per task).  With row-major and column-major iterates mixed, these were
+  // the choices measured fastest (one Gram launch: 0.1 ms per outer step
+  // faster on the 109.5M workload; one update launch: 0.5 ms slower).
   bool split_layouts = false;
   auto segment = [&](const MatInfo& M, bool interior) {
     return !(interior && fast_ok(M)) ? 2 : (split_layouts && M.trans ? 1 : 0);
