@@ -929,6 +929,47 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], co
         }
 }
 
+// Interior update tile of a column-major X': the accumulators of each
+// 32-column block go through the wave's own LDS region (columns padded to
+// 32 NA + 4 floats), so that every store instruction writes whole columns
+// of the wave's 32 NA rows -- full 128-byte lines -- instead of 32-byte
+// pieces of 32 columns.
+template <int NA>
+__host__ __device__ constexpr int stage_floats(int waves) { return waves * 32 * (32 * NA + 4); }
+
+template <int NA, int WNC>
+__device__ __forceinline__ void store_update_colmajor(const GemmArgs& g, const GemmSetup& s,
+                                                      const floatx16 (&acc)[NA][2], float* stage) {
+  constexpr int RW = 32 * NA;     // rows of the wave's tile
+  constexpr int LD = RW + 4;      // padded LDS column
+  constexpr int LPC = RW / 4;     // lanes per column in a store
+  constexpr int CPI = 64 / LPC;   // columns per store instruction
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WNC, wn = wave % WNC;
+  float* ws = stage + wave * 32 * LD;
+  float* xo = g.xout + s.mi.ws_off;
+  __syncthreads();  // every wave is done with the operand planes
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const floatx4 v = {acc[a][b][4 * grp], acc[a][b][4 * grp + 1], acc[a][b][4 * grp + 2],
+                           acc[a][b][4 * grp + 3]};
+        *reinterpret_cast<floatx4*>(ws + (lane & 31) * LD + a * 32 + 8 * grp + 4 * (lane >> 5)) = v;
+      }
+    // the wave reads back only what it wrote: LDS accesses of a wave stay in order
+#pragma unroll
+    for (int q = 0; q < 32 / CPI; ++q) {
+      const int j = q * CPI + lane / LPC, i = 4 * (lane % LPC);
+      const floatx4 v = *reinterpret_cast<const floatx4*>(ws + j * LD + i);
+      const int64_t gi = s.i0 + wm * RW + i, gj = s.j0 + wn * 64 + b * 32 + j;
+      *reinterpret_cast<floatx4*>(xo + gi + gj * s.sc) = v;
+    }
+  }
+}
+
 // bf16x3 (NP = 3) double-buffers the LDS slabs: while the products of slab s
 // run from one buffer, slab s + 1 is split and stored into the other and the
 // global loads of slab s + 2 are in flight; one barrier per slab, and the
@@ -1017,7 +1058,10 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
     }
   }
   }
-  gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc);
+  if constexpr (MODE == kUpdate && LAYOUT == kFastT1)
+    store_update_colmajor<2, 2>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
+  else
+    gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc);
 }
 
 // The interior tiles of row-major (T0) and wide-stored (T1) matrices share one
@@ -1026,15 +1070,29 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
 template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
   constexpr int NB = SplitParts<NP>::nb;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][SplitParts<NP>::a][kBM][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][SplitParts<NP>::b][kBN][kLdsK];
+  typedef __bf16 APlanes[SplitParts<NP>::a][kBM][kLdsK];
+  typedef __bf16 BPlanes[SplitParts<NP>::b][kBM][kLdsK];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
-  if constexpr (LAYOUT == kFastAny) {
-    if (g.mats[task.mat].trans) bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
-    else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+  auto run = [&](APlanes* Ap, BPlanes* Bp) {
+    if constexpr (LAYOUT == kFastAny) {
+      if (g.mats[task.mat].trans) bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
+      else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+    } else {
+      bf16_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
+    }
+  };
+  if constexpr (MODE == kUpdate) {
+    // one block for the operand planes and, after the products, the staging
+    // of the output tile
+    constexpr size_t kPlanes = NB * (sizeof(APlanes) + sizeof(BPlanes));
+    constexpr size_t kStage = stage_floats<2>(kGemmThreads / 64) * sizeof(float);
+    __shared__ __attribute__((aligned(16))) char lds[kPlanes > kStage ? kPlanes : kStage];
+    run(reinterpret_cast<APlanes*>(lds), reinterpret_cast<BPlanes*>(lds + NB * sizeof(APlanes)));
   } else {
-    bf16_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
+    __shared__ __attribute__((aligned(16))) APlanes Ap[NB];
+    __shared__ __attribute__((aligned(16))) BPlanes Bp[NB];
+    run(Ap, Bp);
   }
 }
 
@@ -1102,21 +1160,38 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
       }
     }
   }
-  gemm_epilogue<MODE, 4, 4, kSwap, true>(g, s, task, acc);
+  if constexpr (MODE == kUpdate && LAYOUT == kFastT1)
+    store_update_colmajor<4, 4>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
+  else
+    gemm_epilogue<MODE, 4, 4, kSwap, true>(g, s, task, acc);
 }
 
 template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
   constexpr int NB = SplitParts<NP>::nb;
-  __shared__ __attribute__((aligned(16))) __bf16 Ap[NB][SplitParts<NP>::a][kBig][kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 Bp[NB][SplitParts<NP>::b][kBig][kLdsK];
+  typedef __bf16 APlanes[SplitParts<NP>::a][kBig][kLdsK];
+  typedef __bf16 BPlanes[SplitParts<NP>::b][kBig][kLdsK];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
-  if constexpr (LAYOUT == kFastAny) {
-    if (g.mats[task.mat].trans) bf16_big_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
-    else bf16_big_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+  auto run = [&](APlanes* Ap, BPlanes* Bp) {
+    if constexpr (LAYOUT == kFastAny) {
+      if (g.mats[task.mat].trans) bf16_big_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
+      else bf16_big_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+    } else {
+      bf16_big_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
+    }
+  };
+  if constexpr (MODE == kUpdate) {
+    // one block for the operand planes and, after the products, the staging
+    // of the output tile
+    constexpr size_t kPlanes = NB * (sizeof(APlanes) + sizeof(BPlanes));
+    constexpr size_t kStage = stage_floats<4>(kBigThreads / 64) * sizeof(float);
+    __shared__ __attribute__((aligned(16))) char lds[kPlanes > kStage ? kPlanes : kStage];
+    run(reinterpret_cast<APlanes*>(lds), reinterpret_cast<BPlanes*>(lds + NB * sizeof(APlanes)));
   } else {
-    bf16_big_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
+    __shared__ __attribute__((aligned(16))) APlanes Ap[NB];
+    __shared__ __attribute__((aligned(16))) BPlanes Bp[NB];
+    run(Ap, Bp);
   }
 }
 
