@@ -979,7 +979,7 @@ __device__ __forceinline__ void store_update_colmajor(const GemmArgs& g, const G
 // bf16x6 need 1.25x and 1.5x the LDS per buffer and keep a single buffer
 // with two barriers.
 // SCALED: the X operands are multiplied by the first step's 1/||Delta||_F.
-template <int MODE, int NP, int LAYOUT, bool SCALED>
+template <int MODE, int NP, int LAYOUT, bool SCALED, bool SAME = false>
 __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
                                           __bf16 (*Ap)[SplitParts<NP>::a][kBM][kLdsK],
                                           __bf16 (*Bp)[SplitParts<NP>::b][kBN][kLdsK]) {
@@ -990,6 +990,12 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
   // interior update tiles of row-major X' accumulate transposed blocks (16-byte stores)
   constexpr bool kSwap = MODE == kUpdate && LAYOUT == kFastT0;
   const GemmSetup s = gemm_setup<MODE>(g, task);
+  // SAME: a diagonal tile of a symmetric product, whose two operand panels
+  // coincide -- loaded, split and stored once, read as both operands
+  auto bpl = [&](int buf) -> __bf16 (*)[kBN][kLdsK] {
+    if constexpr (SAME) return Ap[buf];
+    else return Bp[buf];
+  };
   floatx16 acc[2][2];
   gemm_acc_init<MODE>(g, s, acc);
 
@@ -998,7 +1004,7 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
   Slab32 ra, rb;
   if (nslab > 0) {
   load_operand<MODE, LAYOUT, true>(s.A, s.k_begin, s.i0, ra);
-  load_operand<MODE, LAYOUT, false>(s.B, s.k_begin, s.j0, rb);
+  if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, s.k_begin, s.j0, rb);
   if (NB == 2) {
     // Registers hold two slabs in flight: at the top of the products of slab
     // sl, slab sl + 1 is in (ra1, rb1) and slab sl + 2 in (ra, rb).  Each
@@ -1009,52 +1015,52 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
     auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
     Slab32 ra1, rb1;
     load_operand<MODE, LAYOUT, true>(s.A, kat(1), s.i0, ra1);
-    load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
+    if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
     store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-    store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
+    if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
     load_operand<MODE, LAYOUT, true>(s.A, kat(2), s.i0, ra);
-    load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
+    if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
     __syncthreads();
     int sl = 0;
     for (; sl + 2 < nslab; sl += 2) {
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
       store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
-      load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
       __syncthreads();
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], bpl(1), 0, acc);
       store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], Bp[1], 16, acc);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], bpl(1), 16, acc);
       load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
-      load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
       __syncthreads();
     }
     // one or two slabs remain: slab sl in buffer 0, slab sl + 1 in (ra1, rb1)
     int last = 0;
     if (sl + 1 < nslab) {
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
       store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
       __syncthreads();
       last = 1;
     }
-    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 0, acc);
-    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], Bp[last], 16, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], bpl(last), 0, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], bpl(last), 16, acc);
   } else {
     for (int sl = 0; sl < nslab; ++sl) {
       __syncthreads();
       store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
       __syncthreads();
       const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
       load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
-      load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 0, acc);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], Bp[0], 16, acc);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
     }
   }
   }
@@ -1076,8 +1082,14 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   auto run = [&](APlanes* Ap, BPlanes* Bp) {
     if constexpr (LAYOUT == kFastAny) {
-      if (g.mats[task.mat].trans) bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
-      else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+      const bool same = MODE != kUpdate && task.tm == task.tn && (MODE == kPoly || !g.bin);
+      if (g.mats[task.mat].trans) {
+        if (same) bf16_tile<MODE, NP, kFastT1, SCALED, MODE != kUpdate>(g, task, Ap, Bp);
+        else bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
+      } else {
+        if (same) bf16_tile<MODE, NP, kFastT0, SCALED, MODE != kUpdate>(g, task, Ap, Bp);
+        else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
+      }
     } else {
       bf16_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
     }
