@@ -2,11 +2,13 @@
 //
 //   reduce        K-way pseudo-gradient mean (Algorithm 1's sign, averaged as in
 //                 Algorithm 2), 16-byte loads, ||Delta||_F^2 partials per chunk
-//                 for the 2-D tensors, and the whole Nesterov step (Algorithm 2)
-//                 for tensors that are not corrected.
+//                 for the 2-D tensors (written in the iterate's column-major
+//                 layout), and the whole Nesterov step (Algorithm 2) for
+//                 tensors that are not corrected.
 //   fro           per-matrix Frobenius norm from the partials (pre-scaling).
 //   gemm          batched, grouped MFMA products (split-bf16 or fp32) for the polar iteration:
-//                 Gram A = X^T X, polynomial P = b A + c A^2, update X <- a X + X P.
+//                 Gram A = X^T X, polynomial P' = g (a I + b g^2 A + c g^4 A^2),
+//                 update X <- X P'.
 //   gram_norm     ||A||_F (first step: normalisation) or ||A - I||_F (check).
 //   trace/sigma   sigma_bar = <Q, Delta>_F / r (mean singular value, Algorithm 2).
 //   finish        fused Nesterov update and write-back of theta and B for the
@@ -548,7 +550,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
                                               const floatx16 (&acc)[NA][2]) {
   if (MODE == kUpdate && VEC) {
     // Interior update tile: 16-byte stores.  Row-major X' (SWAP, transposed
-    // accumulators): lane holds X'(i, j .. j+3); wide-stored X' (i contiguous):
+    // accumulators): lane holds X'(i, j .. j+3); column-major X' (i contiguous):
     // lane holds X'(i .. i+3, j).
     float* xo = g.xout + s.mi.ws_off;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1070,7 +1072,7 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
     gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc);
 }
 
-// The interior tiles of row-major (T0) and wide-stored (T1) matrices share one
+// The interior tiles of row-major (T0) and column-major (T1) iterates share one
 // launch (kFastAny picks the loaders per task), so that neither layout class
 // forms a launch of its own with a ragged tail.
 template <int MODE, int NP, int LAYOUT, bool SCALED>
@@ -1487,7 +1489,7 @@ static void launch_bf16_segments(const Task* tasks, const int* off, const int* c
   GemmArgs g = g0;
   const dim3 block(kGemmThreads);
   // segment 0 holds both storage orders unless segment 1 takes the
-  // wide-stored tiles (then each has a launch of its own)
+  // column-major tiles (then each has a launch of its own)
   if (cnt[0] && cnt[1]) {
     g.tasks = tasks + off[0];
     hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
