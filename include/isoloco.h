@@ -96,8 +96,9 @@ typedef struct {
                         in bf16x5 (X in 3 parts, P in 2: 5 products, about the accuracy
                         of bf16x6 for this product), bf16x3 for every other product      */
   float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
-                        whose Q^T Q is then the identity to 5e-5 stops there, the others run the
-                        continuation that reaches [ell0, 1] (default 1e-4; a negative value
+                        whose Q^T Q is then the identity to 5e-5 stops there; the others run
+                        a continuation that reaches [sqrt(ell_fast ell0), 1], the same test,
+                        and a last one that reaches [ell0, 1] (default 1e-4; a negative value
                         runs the single schedule for [ell0, 1])                                */
   /* Variants of the step that the paper studies (all 0: Algorithm 2). */
   int32_t orth;      /* ISOLOCO_ORTH_POLAR: Q = U V^T, the converged polar factor (Algorithm 2);
@@ -200,6 +201,16 @@ isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out,
  * NULL) the length of the short first phase (= *n_steps for one phase).  Host only. */
 isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps,
                                 int32_t* n_steps, int32_t* n_short);
+
+/* The phases of the schedule: ends[i] is the number of steps done when phase
+ * i ends (increasing; the last equals the schedule length).  Phase 0 is the
+ * short schedule for [ell_fast, 1]; each later phase continues it for a
+ * smaller bound (the geometric mean of ell_fast and ell0, then ell0).  After
+ * every phase but the last, the matrices whose Q^T Q is the identity to the
+ * switch tolerance stop.  Writes at most max_phases entries; *n_phases
+ * receives the count.  Host only. */
+isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t* ends, int32_t max_phases,
+                                       int32_t* n_phases);
 
 /* Per-kernel timing of the last aggregate, measured with HIP events recorded
  * on the aggregate's stream around every launch (enable first; the events

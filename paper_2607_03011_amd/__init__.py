@@ -13,8 +13,9 @@ __all__ = [
     "ISOLOCO_F32", "ISOLOCO_BF16", "ISOLOCO_KIND_ISO", "ISOLOCO_KIND_AVG",
     "IsoLoCoError", "isoloco_tensor", "isoloco_options", "isoloco_tensor_stats",
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
-    "isoloco_get_stats", "isoloco_schedule", "isoloco_plan_destroy", "isoloco_status_string",
-    "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing", "isoloco_timing",
+    "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
+    "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
+    "isoloco_timing",
     "IsoLoCoPlan", "LIB_PATH", "EXPORTED_SYMBOLS",
 ]
 
@@ -46,8 +47,8 @@ ISOLOCO_FLAG_NOT_CONVERGED = 4
 
 EXPORTED_SYMBOLS = (
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
-    "isoloco_get_stats", "isoloco_schedule", "isoloco_plan_destroy", "isoloco_status_string",
-    "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
+    "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
+    "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
 )
 
 
@@ -83,7 +84,7 @@ class isoloco_timing(ctypes.Structure):
 import torch  # noqa: E402,F401
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libisoloco.so is not built: run `python -m paper_2607_03011_amd.build` "
+    raise ImportError("libisoloco.so is not built: run `python paper_2607_03011_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -99,6 +100,8 @@ _sig = {
     "isoloco_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_tensor_stats), ctypes.c_int32]),
     "isoloco_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
                                         ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
+    "isoloco_schedule_phases": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                               ctypes.POINTER(ctypes.c_int32)]),
     "isoloco_plan_destroy": (ctypes.c_int, [_P]),
     "isoloco_enable_timing": (ctypes.c_int, [_P, ctypes.c_int32]),
     "isoloco_get_timing": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_timing)]),
@@ -106,6 +109,8 @@ _sig = {
     "isoloco_last_error": (ctypes.c_char_p, []),
 }
 for _name, (_res, _args) in _sig.items():
+    if not hasattr(_lib, _name):
+        raise ImportError("libisoloco.so does not export %s: it predates its sources; rebuild it" % _name)
     _f = getattr(_lib, _name)
     _f.restype = _res
     _f.argtypes = _args
@@ -178,6 +183,14 @@ def isoloco_schedule(plan, max_steps=256, with_split=False):
     _check(_lib.isoloco_schedule(plan, buf, max_steps, ctypes.byref(n), ctypes.byref(ns)), "isoloco_schedule")
     sched = [tuple(buf[3 * k: 3 * k + 3]) for k in range(min(n.value, max_steps))]
     return (sched, ns.value) if with_split else sched
+
+
+def isoloco_schedule_phases(plan, max_phases=16):
+    """Steps done at the end of each phase of the schedule (the last is its length)."""
+    buf = (ctypes.c_int32 * max_phases)()
+    n = ctypes.c_int32()
+    _check(_lib.isoloco_schedule_phases(plan, buf, max_phases, ctypes.byref(n)), "isoloco_schedule_phases")
+    return [buf[i] for i in range(min(n.value, max_phases))]
 
 
 def isoloco_enable_timing(plan, enable=True):
@@ -254,6 +267,9 @@ class IsoLoCoPlan:
 
     def schedule_split(self):
         return isoloco_schedule(self.handle, with_split=True)
+
+    def schedule_phases(self):
+        return isoloco_schedule_phases(self.handle)
 
     def close(self):
         if self.handle is not None:

@@ -1,6 +1,6 @@
 """Compile libisoloco.so (host planner + gfx950 HIP kernels) in place.
 
-Usage: ``python -m paper_2607_03011_amd.build`` or ``build()`` from Python.
+Usage: ``python paper_2607_03011_amd/build.py`` or ``__graft_entry__.build()``.
 The library is always rebuilt; tests, the smoke check and the benchmark only
 load what is already built.
 """

@@ -316,8 +316,9 @@ struct isoloco_plan_s {
   int n_iso_chunks = 0;
   TaskListHost gram_list, poly_list, update_list;
   std::vector<int> split_mats, split_n;
-  std::vector<double> sched;  // short schedule followed by its continuation
+  std::vector<double> sched;  // short schedule followed by its continuation phases
   int n_short = 0;            // steps of the short schedule
+  std::vector<int> phase_end; // steps at the end of each phase (the last is the length)
   int64_t n2d = 0;   // elements of one Delta / X buffer
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
   int64_t npart = 0; // elements of the split-K partial buffer
@@ -685,28 +686,36 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     p->dtype = worker_dtype;
     p->opts = o;
     plan_matrices(p);
-    // Two phases: a short schedule that assumes sigma_min >= ell_fast, after
-    // which every matrix whose Q^T Q is already the identity stops; the others
-    // continue with the schedule for what the short one made of [ell0, 1].
+    // Phases: a short schedule that assumes sigma_min >= ell_fast, then
+    // continuations for ever smaller bounds, first the geometric mean of
+    // ell_fast and ell0, then ell0 itself.  After every phase but the last,
+    // each matrix whose Q^T Q is already the identity stops; the others run
+    // the next phase, built for what the phases so far made of its bound.
     if (o.orth == ISOLOCO_ORTH_NS5) {
       // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
       // quintic (Section 4.3; the paper's own coefficients are not printed)
       p->sched.clear();
       for (int k = 0; k < kNs5Steps; ++k) p->sched.insert(p->sched.end(), kNs5Coeffs, kNs5Coeffs + 3);
-      p->n_short = kNs5Steps;
     } else if (o.ell_fast > o.ell0) {
       p->sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
-      p->n_short = (int)p->sched.size() / 3;
-      double lb = o.ell0;
-      for (int k = 0; k < p->n_short; ++k) lb = peval(&p->sched[3 * k], lb);
-      if (p->n_short < o.max_steps && lb < 1.0 - o.tol) {
-        const std::vector<double> rest = build_schedule(lb, o.tol, o.max_steps - p->n_short);
+      p->phase_end.push_back((int)p->sched.size() / 3);
+      const double bounds[2] = {std::sqrt((double)o.ell_fast * o.ell0), o.ell0};
+      for (double b : bounds) {
+        const int done = (int)p->sched.size() / 3;
+        double lb = b;
+        for (int k = 0; k < done; ++k) lb = peval(&p->sched[3 * k], lb);
+        if (done >= o.max_steps || lb >= 1.0 - o.tol) continue;
+        const std::vector<double> rest = build_schedule(lb, o.tol, o.max_steps - done);
+        if (rest.empty()) continue;
         p->sched.insert(p->sched.end(), rest.begin(), rest.end());
+        p->phase_end.push_back((int)p->sched.size() / 3);
       }
     } else {
       p->sched = build_schedule(o.ell0, o.tol, o.max_steps);
-      p->n_short = (int)p->sched.size() / 3;
     }
+    if (p->phase_end.empty() || p->phase_end.back() != (int)p->sched.size() / 3)
+      p->phase_end.push_back((int)p->sched.size() / 3);
+    p->n_short = p->phase_end.front();
     plan_workspace(p);
   } catch (...) {
     delete p;
@@ -821,9 +830,16 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   if (e != hipSuccess) return hip_fail(e, "reduce launch");
   if (t.n_mat > 0) {
     const int S = (int)plan->sched.size() / 3;
-    const int Sa = plan->n_short;
-    const bool two = Sa < S;
-    const int buf_short = (Sa - 1) & 1, buf_total = (S - 1) & 1;
+    const std::vector<int>& ends = plan->phase_end;
+    const int n_ph = (int)ends.size();
+    const bool phased = n_ph > 1;
+    const int buf_total = (S - 1) & 1;
+    // index of the phase that ends after step k, -1 if none but the last does
+    auto ends_phase = [&](int k) {
+      for (int i = 0; i + 1 < n_ph; ++i)
+        if (ends[i] == k + 1) return i;
+      return -1;
+    };
     const char* what = "";
     // The polar iteration on the matrices in tt.delta (state in tt.scalars;
     // the chunk partials of their squared norms in tt.part_sq); the factor of
@@ -835,9 +851,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         return r;
       NormArgs na{};
       na.flag_unconverged = ns5 ? 0 : 1;
-      na.steps_short = Sa;
       na.steps_total = S;
-      na.buf_short = buf_short;
       na.buf_total = buf_total;
       na.tol_switch = kSwitchTol;
       auto gram = [&](const PolarStep& ps) -> hipError_t {
@@ -860,11 +874,11 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         ps.cb = (float)plan->sched[3 * k + 1];
         ps.cc = (float)plan->sched[3 * k + 2];
         ps.first = (k == 0);
-        ps.only_active = (k >= Sa);
+        ps.only_active = (k >= ends[0]);
         ps.arith = step_arith(plan->opts.precision, k, kProdGram);
         what = "polar step launch";
-        // the first Gram of the second phase was formed by the switch check
-        if (!(two && k == Sa) && (r = gram(ps)) != hipSuccess) return r;
+        // the first Gram of a later phase was formed by the switch check
+        if (!(k > 0 && ends_phase(k - 1) >= 0) && (r = gram(ps)) != hipSuccess) return r;
         // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
         if (k == 0 && !ns5 && (r = norm(kNormFirst, 0)) != hipSuccess) return r;
         PolarStep pp = ps, pu = ps;
@@ -874,18 +888,24 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
             (r = timed(kPhUpdate, [&] { return launch_gemm(tt, 2, pu, st); })) != hipSuccess)
           return r;
         xin = ps.xout;
-        if (two && k == Sa - 1) {
+        const int ph = ends_phase(k);
+        if (ph >= 0) {
+          // the matrices still running check Q^T Q = I; those that pass stop
+          // here with the factor in x[k & 1]
           PolarStep pc{};
           pc.xin = xin;
+          pc.only_active = ph > 0;
           pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
+          na.steps_short = k + 1;
+          na.buf_short = k & 1;
           what = "switch check launch";
-          if ((r = gram(pc)) != hipSuccess || (r = norm(kNormSwitch, 0)) != hipSuccess) return r;
+          if ((r = gram(pc)) != hipSuccess || (r = norm(kNormSwitch, pc.only_active)) != hipSuccess) return r;
         }
       }
       if (check) {
         PolarStep pc{};
         pc.xin = xin;
-        pc.only_active = two ? 1 : 0;
+        pc.only_active = phased ? 1 : 0;
         pc.arith = step_arith(plan->opts.precision, S, kProdGram);
         what = "check launch";
         if ((r = gram(pc)) != hipSuccess || (r = norm(kNormFinal, pc.only_active)) != hipSuccess) return r;
@@ -970,6 +990,16 @@ isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max
   if (n_short) *n_short = plan->n_short;
   if (coeffs)
     for (int i = 0; i < 3 * std::min<int>(S, std::max(max_steps, 0)); ++i) coeffs[i] = plan->sched[i];
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t* ends, int32_t max_phases,
+                                       int32_t* n_phases) {
+  if (!plan || !n_phases) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  const int n = (int)plan->phase_end.size();
+  *n_phases = n;
+  if (ends)
+    for (int i = 0; i < std::min<int>(n, std::max(max_phases, 0)); ++i) ends[i] = plan->phase_end[i];
   return ISOLOCO_OK;
 }
 

@@ -76,15 +76,15 @@ struct PolarStep {
 enum NormMode {
   kNormFirst = 0,   // gscale = ||A||_F^(-1/2) of the first step
   kNormFinal = 1,   // final check: resid and the not-converged flag
-  kNormSwitch = 2,  // end of the short schedule: resid; converged matrices stop
+  kNormSwitch = 2,  // end of a phase but the last: resid; converged matrices stop
 };
 
 struct NormArgs {
   int mode;
   int only_active;
-  int steps_short, steps_total;  // schedule lengths
-  int buf_short, buf_total;      // X buffer holding the result after each phase
-  float tol_switch;              // residual below which a matrix stops after the short schedule
+  int steps_short, steps_total;  // steps done at this phase's end, schedule length
+  int buf_short, buf_total;      // X buffer holding the result after this phase, after all
+  float tol_switch;              // residual below which a matrix stops at the phase's end
   int flag_unconverged;          // final check: flag residuals above 1e-3 (not for a fixed-length variant)
 };
 

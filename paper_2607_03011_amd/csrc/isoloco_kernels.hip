@@ -1270,7 +1270,7 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
   }
   o.resid = (float)sqrt(s / mats[m].n);
   if (a.mode == kNormSwitch) {
-    // stop after the short schedule when every singular value is already at 1
+    // stop at the end of this phase when every singular value is already at 1
     const bool go_on = o.flags == 0 && !(o.resid <= a.tol_switch);
     o.active = go_on ? 1 : 0;
     o.steps = go_on ? a.steps_total : a.steps_short;

@@ -145,6 +145,33 @@ def test_two_phase_schedule(ell_fast):
     assert np.abs(_compose(sched[ns:], y) - 1).max() <= 1e-6
 
 
+def test_phases_converge_on_their_bounds():
+    """Default phases: [ell_fast, 1], then [sqrt(ell_fast ell0), 1], then
+    [ell0, 1]; a value that one phase converged stays converged through the
+    phases after it."""
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    sched = iso.isoloco_schedule(h)
+    ends = iso.isoloco_schedule_phases(h)
+    _, ns = iso.isoloco_schedule(h, with_split=True)
+    iso.isoloco_plan_destroy(h)
+    assert len(ends) == 3 and ends[0] == ns and ends[-1] == len(sched)
+    assert ends[0] < ends[1] < ends[2]
+    for e, bound in zip(ends, (1e-4, 1e-7, 1e-10)):
+        x = np.geomspace(bound, 1.0, 100001)
+        assert np.abs(_compose(sched[:e], x) - 1).max() <= 1e-6, (e, bound)
+        y = _compose(sched[:e], np.linspace(0.5, 1.0, 1001))
+        assert np.abs(_compose(sched[e:], y) - 1).max() <= 1e-6, e
+
+
+def test_phases_of_single_and_fixed_schedules():
+    for opts, n in ((dict(ell_fast=-1.0), 1), (dict(orth=1, scale=1), 1), (dict(max_steps=12), 2)):
+        h = iso.isoloco_plan(LAY, 8256, 4, 0, opts)
+        ends = iso.isoloco_schedule_phases(h)
+        S = len(iso.isoloco_schedule(h))
+        iso.isoloco_plan_destroy(h)
+        assert len(ends) == n and ends[-1] == S and ends == sorted(set(ends)), (opts, ends)
+
+
 def test_one_phase_when_ell_fast_negative():
     h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell_fast=-1.0))
     sched, ns = iso.isoloco_schedule(h, with_split=True)

@@ -392,18 +392,65 @@ def _planted(rows, cols, smin, rng):
 def test_two_phase_stops_well_conditioned_matrices_early(iso):
     """With the workload's pseudo-gradients (low rank + noise), a tall matrix
     (sigma_min / ||Delta^T Delta||_F^(1/2) around 1e-2) stops after the short
-    schedule while a square one (sigma_min around 1e-6 of that) runs the
+    schedule while a square one (sigma_min around 1e-6 of that) runs a
     continuation; both match the oracle."""
     from workload import custom_layout
     lay, n = custom_layout([(256, 256, KIND_ISO), (192, 64, KIND_ISO), (64, 1, KIND_AVG)], align=4)
     cfg = _cfg(lay, n, K=4)
     dev = torch.device("cuda", 0)
     plan = iso.IsoLoCoPlan(lay, n, 4, iso.ISOLOCO_F32, device=dev)
-    sched, n_short = plan.schedule_split()
+    ends = plan.schedule_phases()
     _, _, st = _run_and_compare(iso, cfg, seed=4, plan=plan)
-    print("steps", [s.steps for s in st[:2]], "of", n_short, len(sched), flush=True)
-    assert st[0].steps == len(sched)
-    assert st[1].steps == n_short
+    print("steps", [s.steps for s in st[:2]], "phase ends", ends, flush=True)
+    assert st[0].steps in ends[1:]
+    assert st[1].steps == ends[0]
+    plan.close()
+
+
+def _planted_tail(rows, cols, tiny, rng):
+    """rows x cols matrix with singular values spaced geometrically in [1e-2, 1]
+    and one more, far below them, at ``tiny``."""
+    r = min(rows, cols)
+    U, _ = np.linalg.qr(rng.standard_normal((rows, r)))
+    V, _ = np.linalg.qr(rng.standard_normal((cols, r)))
+    return (U * np.concatenate([np.geomspace(1.0, 1e-2, r - 1), [tiny]])) @ V.T
+
+
+def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
+    """Three phases (short schedule for [1e-4, 1], continuations for
+    [1e-7, 1] and [1e-10, 1], bounds on sigma / ||Delta^T Delta||_F^(1/2)):
+    a tall matrix with singular values in [1e-2, 1] stops after the first, a
+    square one in [1e-5, 1] after the second, and a square one whose smallest
+    singular value sits alone near 1.5e-8 (relative) runs all three; each
+    matches the oracle."""
+    from workload import custom_layout
+    lay, n = custom_layout([(192, 64, KIND_ISO), (256, 256, KIND_ISO), (256, 256, KIND_ISO)], align=4)
+    rng = np.random.default_rng(5)
+    delta = np.zeros(n)
+    mats = (_planted(192, 64, 1e-2, rng), _planted(256, 256, 1e-5, rng), _planted_tail(256, 256, 3e-8, rng))
+    for (off, rows, cols, kind), m in zip(lay, mats):
+        delta[off:off + rows * cols] = (m * 1e-3).reshape(-1)
+    dev = torch.device("cuda", 0)
+    theta = torch.zeros(n, dtype=torch.float32, device=dev)
+    mom = torch.zeros_like(theta)
+    w = torch.tensor(-delta, dtype=torch.float32, device=dev).reshape(1, n).contiguous()
+    plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, device=dev)
+    ends = plan.schedule_phases()
+    assert len(ends) == 3
+    print("case: planted tails, phase ends", ends, flush=True)
+    plan.aggregate(theta, w, mom, 1.0, 0.7, 0.9)
+    torch.cuda.synchronize()
+    st = plan.stats()
+    ref = oracle_per_tensor(lay, np.zeros(n, np.float32), [w.cpu().numpy()[0]], np.zeros(n, np.float32),
+                            1.0, 0.7, 0.9)
+    th = theta.cpu().numpy()
+    for i, (th_r, b_r, sb_r) in ref.items():
+        off, rows, cols, kind = lay[i]
+        e = relF(th[off:off + rows * cols], th_r)
+        print("tensor %d steps %d resid %.2e: theta %.2e" % (i, st[i].steps, st[i].orth_resid, e), flush=True)
+        assert e <= TOL and st[i].flags == 0
+        assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
+    assert [s.steps for s in st] == ends
     plan.close()
 
 
