@@ -230,13 +230,11 @@ std::vector<double> build_schedule(double ell0, double tol, int max_steps) {
 // 8 queues are interleaved into one grid.  Short queues are padded with
 // empty tasks (mat = -1), which return at once.
 constexpr int kXcds = 8;
-// 256 x 256 tiles for the symmetric Gram and polynomial products: off.  With
-// 6 such tiles per 768 x 768 matrix there are too few tasks to fill 256 CUs
-// evenly, and these phases ran slower than on 128 x 128 tiles; the update
-// (9 to 375 tiles per matrix) uses them.
-constexpr bool kBigGram = false;
-// Most K slices of a split Gram (see plan_matrices).
-constexpr int64_t kMaxKSlices = 6;
+// The symmetric Gram and polynomial products run on 128 x 128 tiles only
+// (their epilogues index the upper-triangle tiles of that tiling).  With 6
+// tiles of 256 x 256 per 768 x 768 matrix there were too few tasks to fill
+// 256 CUs evenly, and these phases ran slower; the update (9 to 375 such
+// tiles per matrix) uses them.
 
 std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<Task>& in, bool by_slice) {
   struct Group {
@@ -315,7 +313,8 @@ struct isoloco_plan_s {
   std::vector<Chunk> chunks;
   int n_iso_chunks = 0;
   TaskListHost gram_list, poly_list, update_list;
-  std::vector<int> split_mats, split_n;
+  int64_t n_norm = 0;  // Gram-norm partial slots (gram_tiles(n) per matrix)
+  int64_t n_cnt = 0;   // split-K tile counters
   std::vector<double> sched;  // short schedule followed by its continuation phases
   int n_short = 0;            // steps of the short schedule
   std::vector<int> phase_end; // steps at the end of each phase (the last is the length)
@@ -323,7 +322,7 @@ struct isoloco_plan_s {
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
-  size_t off_pnorm = 0;
+  size_t off_pnorm = 0, off_cnt = 0;
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
   size_t off_poly = 0, off_gpart = 0, total = 0;
@@ -375,18 +374,23 @@ void plan_matrices(isoloco_plan_s* p) {
     // launch's tail too long, eight and more add partial traffic).
     int ks = 1;
     if (mi.m >= 4 * mi.n && mi.m > 4096)
-      ks = (int)std::min<int64_t>(kMaxKSlices, (mi.m + 1023) / 1024);
+      ks = (int)std::min<int64_t>(kMaxKSplit, (mi.m + 1023) / 1024);
     int64_t kchunk = (mi.m + ks - 1) / ks;
     kchunk = (kchunk + 31) / 32 * 32;  // whole K slabs of both product kernels
     ks = (int)((mi.m + kchunk - 1) / kchunk);
     mi.ksplit = ks;
     mi.kchunk = (int32_t)kchunk;
     mi.part_off = 0;
+    mi.cnt_off = -1;
     if (ks > 1) {
       mi.part_off = part;
       part += (int64_t)ks * mi.n * mi.n;
       part = (part + 63) / 64 * 64;
+      mi.cnt_off = (int32_t)p->n_cnt;
+      p->n_cnt += gram_tiles(mi.n);
     }
+    mi.norm_off = (int32_t)p->n_norm;
+    p->n_norm += gram_tiles(mi.n);
     const int64_t cnt = (int64_t)mi.m * mi.n;
     mi.chunk_begin = (int32_t)p->chunks.size();
     if (tiled) {
@@ -491,25 +495,25 @@ void plan_matrices(isoloco_plan_s* p) {
   });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM, T2 = M.n / 256;
+    const int T = (M.n + kBM - 1) / kBM;
     // the Gram matrix is symmetric: tiles on and above the diagonal only
     for (int ks = 0; ks < M.ksplit; ++ks) {
       const int64_t kb = (int64_t)ks * M.kchunk, ke = std::min<int64_t>(M.m, kb + M.kchunk);
       const bool kin = (ke - kb) % 32 == 0;
       for (int a = 0; a < T; ++a)
         for (int b = a; b < T; ++b)
-          put(M, (b + 1) * kBM <= M.n && kin, kBigGram && fast_ok(M) && kin && b < 2 * T2, Task{mi, a, b, ks});
+          put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, ks});
     }
   }
   flush(p->gram_list, true);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
   for (int mi : order) {
     const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM, T2 = M.n / 256;
+    const int T = (M.n + kBM - 1) / kBM;
     const bool kin = M.n % 32 == 0;
     for (int a = 0; a < T; ++a)
       for (int b = a; b < T; ++b)
-        put(M, (b + 1) * kBM <= M.n && kin, kBigGram && fast_ok(M) && kin && b < 2 * T2, Task{mi, a, b, 0});
+        put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, 0});
   }
   flush(p->poly_list, false);
   split_layouts = true;
@@ -524,11 +528,6 @@ void plan_matrices(isoloco_plan_s* p) {
             fast_ok(M) && kin && a < 2 * TM2 && b < 2 * TN2, Task{mi, a, b, 0});
   }
   flush(p->update_list, false);
-  for (size_t i = 0; i < p->mats.size(); ++i)
-    if (p->mats[i].ksplit > 1) {
-      p->split_mats.push_back((int)i);
-      p->split_n.push_back(p->mats[i].n);
-    }
 }
 
 void plan_workspace(isoloco_plan_s* p) {
@@ -546,7 +545,8 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_sc = take(p->mats.size() * sizeof(MatScalars));
   p->off_psq = take(p->chunks.size() * sizeof(double));
   p->off_ptr = take(p->chunks.size() * sizeof(double));
-  p->off_pnorm = take(p->mats.size() * kNormSlices * sizeof(double));
+  p->off_pnorm = take((size_t)p->n_norm * sizeof(double));
+  p->off_cnt = take((size_t)p->n_cnt * sizeof(int));
   p->off_delta = take((size_t)p->n2d * sizeof(float));
   p->off_x0 = take((size_t)p->n2d * sizeof(float));
   p->off_x1 = take((size_t)p->n2d * sizeof(float));
@@ -586,6 +586,7 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
   t.part_norm = reinterpret_cast<double*>(w + p->off_pnorm);
+  t.split_cnt = reinterpret_cast<int*>(w + p->off_cnt);
   t.delta = reinterpret_cast<float*>(w + p->off_delta);
   t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
   t.x[1] = reinterpret_cast<float*>(w + p->off_x1);
@@ -597,9 +598,6 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.n_mat = (int)p->mats.size();
   t.n_chunks = (int)p->chunks.size();
   t.n_iso_chunks = p->n_iso_chunks;
-  t.n_split = (int)p->split_mats.size();
-  t.split_mats_host = p->split_mats.data();
-  t.split_n_host = p->split_n.data();
   return t;
 }
 
@@ -756,6 +754,14 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
     e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
     if (e != hipSuccess) return hip_fail(e, "clearing per-matrix scalars");
   }
+  if (plan->n_cnt > 0) {
+    // the split-K Gram tiles count their arrivals here; each launch leaves them at zero
+    e = hipMemset(w + plan->off_cnt, 0, (size_t)plan->n_cnt * sizeof(int));
+    if (e != hipSuccess) return hip_fail(e, "clearing split-K counters");
+  }
+  // done before any stream of the caller's (some may not wait for the null stream)
+  e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   plan->ws = w;
   plan->ws_bytes = bytes;
   plan->device = dev;
@@ -855,10 +861,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       na.buf_total = buf_total;
       na.tol_switch = kSwitchTol;
       auto gram = [&](const PolarStep& ps) -> hipError_t {
-        hipError_t q = timed(kPhGram, [&] { return launch_gemm(tt, 0, ps, st); });
-        if (q == hipSuccess && tt.n_split)
-          q = timed(kPhOther, [&] { return launch_split_sums(tt, ps.only_active, st); });
-        return q;
+        return timed(kPhGram, [&] { return launch_gemm(tt, 0, ps, st); });
       };
       auto norm = [&](int mode, int only_active) -> hipError_t {
         na.mode = mode;
@@ -876,11 +879,12 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         ps.first = (k == 0);
         ps.only_active = (k >= ends[0]);
         ps.arith = step_arith(plan->opts.precision, k, kProdGram);
+        // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
+        ps.norm_mode = (k == 0 && !ns5) ? kNormFirst : -1;
         what = "polar step launch";
         // the first Gram of a later phase was formed by the switch check
         if (!(k > 0 && ends_phase(k - 1) >= 0) && (r = gram(ps)) != hipSuccess) return r;
-        // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
-        if (k == 0 && !ns5 && (r = norm(kNormFirst, 0)) != hipSuccess) return r;
+        if (ps.norm_mode == kNormFirst && (r = norm(kNormFirst, 0)) != hipSuccess) return r;
         PolarStep pp = ps, pu = ps;
         pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
         pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
@@ -896,6 +900,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
           pc.xin = xin;
           pc.only_active = ph > 0;
           pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
+          pc.norm_mode = kNormSwitch;
           na.steps_short = k + 1;
           na.buf_short = k & 1;
           what = "switch check launch";
@@ -907,6 +912,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         pc.xin = xin;
         pc.only_active = phased ? 1 : 0;
         pc.arith = step_arith(plan->opts.precision, S, kProdGram);
+        pc.norm_mode = kNormFinal;
         what = "check launch";
         if ((r = gram(pc)) != hipSuccess || (r = norm(kNormFinal, pc.only_active)) != hipSuccess) return r;
       }
@@ -929,8 +935,8 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       pc.xin_alt = t.x[1];
       pc.bin = t.delta;
       pc.arith = step_arith(plan->opts.precision, S, kProdGram);
+      pc.norm_mode = -1;
       hipError_t r = timed(kPhGram, [&] { return launch_gemm(t2, 0, pc, st); });
-      if (r == hipSuccess && t.n_split) r = timed(kPhOther, [&] { return launch_split_sums(t2, 0, st); });
       if (r != hipSuccess) return hip_fail(r, "clip product launch");
       DevTables t3 = t2;
       t3.poly = t.gram;  // the update product reads Q2^T E as its right factor

@@ -31,7 +31,8 @@ struct DevTables {
   MatScalars* scalars;
   double* part_sq;
   double* part_tr;
-  double* part_norm;  // n_mat x kNormSlices partials of the Gram norms
+  double* part_norm;  // Gram-norm partials, gram_tiles(n) per matrix from MatInfo::norm_off
+  int* split_cnt;     // arrival counters of the split-K Gram tiles (zero between launches)
   float* delta;
   float* x[2];
   float* x2;              // clip variants: copy of the polar factor Q (else unused)
@@ -40,9 +41,6 @@ struct DevTables {
   float* poly;
   float* gpart;
   int n_mat, n_chunks, n_iso_chunks;
-  int n_split;
-  const int* split_mats_host;  // host arrays of length n_split
-  const int* split_n_host;
 };
 
 struct StepArgs {
@@ -70,6 +68,8 @@ struct PolarStep {
   int first;
   int only_active;  // 1: skip matrices whose scalars say active == 0
   int arith;        // Arith
+  int norm_mode = -1;  // Gram only: -1 none, else the NormMode whose tile partials the Gram
+                    // leaves in DevTables::part_norm (kNormFirst: sum A^2, others sum (A - I)^2)
 };
 
 // Gram-norm modes
@@ -94,7 +94,8 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
 hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fixed_g, hipStream_t st);
 // mode: 0 Gram, 1 polynomial, 2 update
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st);
-hipError_t launch_split_sums(const DevTables& t, int only_active, hipStream_t st);
+// per-matrix decisions from the norm partials of the Gram launched before with
+// norm_mode = a.mode
 hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st);
 // the polar factor of matrix m is in t.x[scalars[m].qbuf]; the scale of each
 // correction (a.scale: its mean singular value from <Q, Delta>, or a closed form)

@@ -422,9 +422,12 @@ struct GemmArgs {
   float* gram;        // n x n Gram buffers (Gram output, Poly input)
   float* poly;        // n x n polynomial buffers (Poly output, Update input)
   float* gpart;       // split-K Gram partials
+  int* split_cnt;     // split-K Gram: arrival counter per output tile
+  double* part_norm;  // Gram: per-tile partial sums of squares (norm_mode >= 0)
   float ca, cb, cc;   // step coefficients p(x) = ca x + cb x^3 + cc x^5
   int first;          // 1 on the first step (inputs pre-scaled by 1/||Delta||_F, g applied)
   int only_active;    // 1: tasks of matrices that stopped iterating return at once
+  int norm_mode;      // Gram: -1, or kNormFirst (sum A^2) / other (sum (A - I)^2) per tile
 };
 
 // Operands, output bounds and K range of one task.
@@ -540,6 +543,150 @@ __device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup
     }
 }
 
+// Gram epilogue.  Writes the tile and its mirror image into the n x n Gram
+// buffer and, when the launch asks for it, the tile's share of ||A||_F^2 or
+// ||A - I||_F^2 (twice the tile's sum off the diagonal) into its slot of
+// part_norm, which gram_norm_final_kernel adds up in a fixed order.
+//
+// A split-K matrix first writes this K slice's partial tile into its slice of
+// gpart.  The last of the ksplit workgroups of a tile to arrive (counted by an
+// agent-scope atomic, release before and acquire after it, so that the
+// partials written on other XCDs are visible) adds the slices in slice order,
+// finishes the tile as above and sets the counter back to zero for the next
+// launch.  No workgroup waits for another.  `scratch` is LDS the operand
+// planes no longer need (at least 40 bytes).
+template <int NA, int WNC>
+__device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
+                                              const floatx16 (&acc)[NA][2], void* scratch) {
+  const MatInfo& mi = s.mi;
+  const int n = mi.n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WNC, wn = wave % WNC;
+  const int jl = lane & 31, ib = 4 * (lane >> 5);
+  const int tile = gram_tile_index(n, task.tm, task.tn);
+  double* red = reinterpret_cast<double*>(scratch);
+  int* last = reinterpret_cast<int*>(red + 4);
+  floatx16 v[NA][2];
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) v[a][b] = acc[a][b];
+  if (mi.ksplit > 1) {
+    // partial tiles are stored transposed (C(i, j) at j * n + i), so that the
+    // 4 values a lane holds, C(i .. i+3, j), are one 16-byte access
+    const int64_t nn = (int64_t)n * n;
+    const bool v4 = (n & 3) == 0;
+    const float* part = g.gpart + mi.part_off;
+    float* mine = g.gpart + mi.part_off + (int64_t)task.ks * nn;
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int j = s.j0 + wn * 64 + b * 32 + jl;
+        if (j >= s.N) continue;
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
+          float* o = mine + (int64_t)j * n + ibase;
+          if (v4 && ibase + 3 < s.M) {
+            const floatx4 q = {v[a][b][4 * grp], v[a][b][4 * grp + 1], v[a][b][4 * grp + 2], v[a][b][4 * grp + 3]};
+            *reinterpret_cast<floatx4*>(o) = q;
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (ibase + r < s.M) o[r] = v[a][b][4 * grp + r];
+          }
+        }
+      }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();  // every wave's partial is out, and the operand planes are free
+    int* cnt = g.split_cnt + mi.cnt_off + tile;
+    if (threadIdx.x == 0)
+      *last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == mi.ksplit - 1;
+    __syncthreads();
+    if (!*last) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the slices in slice order; every load of the tile is independent of the
+    // sums, so that they can all be in flight together
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int j = s.j0 + wn * 64 + b * 32 + jl;
+        if (j >= s.N) continue;
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
+          const bool vec = v4 && ibase + 3 < s.M;
+          const floatx4 own = {v[a][b][4 * grp], v[a][b][4 * grp + 1], v[a][b][4 * grp + 2], v[a][b][4 * grp + 3]};
+          floatx4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int k = 0; k < kMaxKSplit; ++k) {
+            if (k >= mi.ksplit) break;
+            floatx4 x = own;
+            if (k != task.ks) {
+              const float* src = part + k * nn + (int64_t)j * n + ibase;
+              if (vec) {
+                x = *reinterpret_cast<const floatx4*>(src);
+              } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) x[r] = ibase + r < s.M ? src[r] : 0.f;
+              }
+            }
+            t = k == 0 ? x : t + x;
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[a][b][4 * grp + r] = t[r];
+        }
+      }
+  }
+  float* out = g.gram + mi.sq_off;
+  const bool diag = task.tm == task.tn;
+  const bool want = g.norm_mode >= 0;
+  const float unit = g.norm_mode == kNormFirst ? 0.f : 1.f;
+  double sq = 0.0;
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int j = s.j0 + wn * 64 + b * 32 + jl;
+      if (j >= s.N) continue;
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
+        floatx4 q;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) q[r] = v[a][b][4 * grp + r];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = ibase + r;
+          if (i >= s.M) continue;
+          out[(int64_t)i * n + j] = q[r];
+          if (want) {
+            const double d = (double)q[r] - (i == j ? unit : 0.f);
+            sq += d * d;
+          }
+        }
+        if (!diag) {
+          float* mo = out + (int64_t)j * n + ibase;
+          if ((n & 3) == 0 && ibase + 3 < s.M) {
+            *reinterpret_cast<floatx4*>(mo) = q;
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (ibase + r < s.M) mo[r] = q[r];
+          }
+        }
+      }
+    }
+  if (want) {
+    __syncthreads();  // the operand planes are free (split tiles passed this point already)
+    sq = block_sum256(sq, red);
+    if (threadIdx.x == 0) g.part_norm[mi.norm_off + tile] = diag ? sq : 2.0 * sq;
+  }
+}
+
 // Epilogue.  A wave owns NA x 2 accumulator tiles of 32 x 32: with WNC waves
 // across the block's columns, wm = wave / WNC and wn = wave % WNC,
 // acc[a][b][r] holds C(i, j) with
@@ -547,7 +694,11 @@ __device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup
 // (the 32 x 32 accumulator layout of the fp32 and bf16 MFMA instructions).
 template <int MODE, int NA = 2, int WNC = 2, bool SWAP = false, bool VEC = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
-                                              const floatx16 (&acc)[NA][2]) {
+                                              const floatx16 (&acc)[NA][2], void* scratch = nullptr) {
+  if constexpr (MODE == kGram) {
+    gram_epilogue<NA, WNC>(g, s, task, acc, scratch);
+    return;
+  }
   if (MODE == kUpdate && VEC) {
     // Interior update tile: 16-byte stores.  Row-major X' (SWAP, transposed
     // accumulators): lane holds X'(i, j .. j+3); column-major X' (i contiguous):
@@ -591,27 +742,20 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
         const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
-        if (MODE == kGram || MODE == kPoly) {
+        if (MODE == kPoly) {
           // symmetric n x n result: only tiles with tm <= tn are computed, and an
-          // off-diagonal tile also writes its mirror image C(j, i) = C(i, j)
-          float* out;
+          // off-diagonal tile also writes its mirror image C(j, i) = C(i, j).
+          // P = g (ca I + cb g^2 A + cc g^4 A^2)  (g = 1 after the first step),
+          // so that the update is the plain product X' = X P; the accumulators
+          // hold rho A + A A (see gemm_acc_init)
+          const float g2 = s.gs * s.gs;
+          const float gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
+          float* out = g.poly + mi.sq_off;
           floatx4 v;
-          if (MODE == kGram) {
-            out = (mi.ksplit > 1) ? g.gpart + mi.part_off + (int64_t)task.ks * n * n : g.gram + mi.sq_off;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = acc[a][b][4 * grp + r];
-          } else {
-            // P = g (ca I + cb g^2 A + cc g^4 A^2)  (g = 1 after the first
-            // step), so that the update is the plain product X' = X P; the
-            // accumulators hold rho A + A A (see gemm_acc_init)
-            const float g2 = s.gs * s.gs;
-            const float gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
-            out = g.poly + mi.sq_off;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int i = ibase + r;
-              v[r] = gamma * acc[a][b][4 * grp + r] + (i == j ? diag : 0.f);
-            }
+          for (int r = 0; r < 4; ++r) {
+            const int i = ibase + r;
+            v[r] = gamma * acc[a][b][4 * grp + r] + (i == j ? diag : 0.f);
           }
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -645,8 +789,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
 // fp32 MFMA main loop (v_mfma_f32_32x32x2f32), K staged in slabs of 16.
 template <int MODE>
 __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
-  __shared__ float As[kBK][kLdsW];
-  __shared__ float Bs[kBK][kLdsW];
+  __shared__ __attribute__((aligned(16))) float As[kBK][kLdsW];
+  __shared__ __attribute__((aligned(16))) float Bs[kBK][kLdsW];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   const GemmSetup s = gemm_setup<MODE>(g, task);
@@ -680,7 +824,7 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
     }
     __syncthreads();
   }
-  gemm_epilogue<MODE>(g, s, task, acc);
+  gemm_epilogue<MODE>(g, s, task, acc, &As[0][0]);
 }
 
 // ---------------------------------------------------------------------------
@@ -1069,7 +1213,7 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
   if constexpr (MODE == kUpdate && LAYOUT == kFastT1)
     store_update_colmajor<2, 2>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
   else
-    gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc);
+    gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc, &Ap[0][0][0][0]);
 }
 
 // The interior tiles of row-major (T0) and column-major (T1) iterates share one
@@ -1209,52 +1353,6 @@ __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs 
   }
 }
 
-// Sum of the split-K Gram partials of one matrix, 4 elements per thread.
-__global__ void __launch_bounds__(256)
-gram_split_sum_kernel(const MatInfo* __restrict__ mats, const MatScalars* __restrict__ sc, int mat,
-                      int only_active, const float* __restrict__ gpart, float* __restrict__ gram) {
-  if (only_active && !sc[mat].active) return;
-  const MatInfo mi = mats[mat];
-  const int64_t nn = (int64_t)mi.n * mi.n;
-  const int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (e >= nn) return;
-  const float* p = gpart + mi.part_off;
-  float* out = gram + mi.sq_off;
-  if (e + 3 < nn && (nn & 3) == 0) {
-    floatx4 s = *reinterpret_cast<const floatx4*>(p + e);
-    for (int k = 1; k < mi.ksplit; ++k) s += *reinterpret_cast<const floatx4*>(p + k * nn + e);
-    *reinterpret_cast<floatx4*>(out + e) = s;
-  } else {
-    for (int q = 0; q < 4 && e + q < nn; ++q) {
-      float s = p[e + q];
-      for (int k = 1; k < mi.ksplit; ++k) s += p[k * nn + e + q];
-      out[e + q] = s;
-    }
-  }
-}
-
-// Partial sums of squares over an n x n buffer: block (x, m) takes rows
-// x, x + kNormSlices, ... of matrix m.  mode 0: sum A^2; mode 1: sum (A - I)^2.
-
-__global__ void __launch_bounds__(256)
-gram_norm_partial_kernel(const MatInfo* __restrict__ mats, const MatScalars* __restrict__ sc,
-                         const float* __restrict__ gram, double* __restrict__ part, int mode, int only_active) {
-  __shared__ double red[4];
-  if (only_active && !sc[blockIdx.y].active) return;
-  const MatInfo mi = mats[blockIdx.y];
-  const int n = mi.n;
-  const float* a = gram + mi.sq_off;
-  double s = 0.0;
-  for (int r = blockIdx.x; r < n; r += kNormSlices)
-    for (int c = threadIdx.x; c < n; c += 256) {
-      double v = a[(int64_t)r * n + c];
-      if (mode != kNormFirst && r == c) v -= 1.0;
-      s += v * v;
-    }
-  s = block_sum256(s, red);
-  if (threadIdx.x == 0) part[(int64_t)blockIdx.y * kNormSlices + blockIdx.x] = s;
-}
-
 // Per-matrix decisions from the norm partials (see NormMode).
 __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part,
                                        MatScalars* __restrict__ sc, int n_mat, NormArgs a) {
@@ -1263,7 +1361,8 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
   MatScalars& o = sc[m];
   if (a.only_active && !o.active) return;
   double s = 0.0;
-  for (int x = 0; x < kNormSlices; ++x) s += part[(int64_t)m * kNormSlices + x];
+  const int nt = gram_tiles(mats[m].n);
+  for (int x = 0; x < nt; ++x) s += part[mats[m].norm_off + x];
   if (a.mode == kNormFirst) {
     o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
     return;
@@ -1513,6 +1612,8 @@ template <int MODE, int NP, bool SCALED>
 static void launch_big_cover(const TaskList& L, const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kBigThreads);
+  // (the planner lists 256 x 256 tiles for the update products only)
+  if constexpr (MODE == kUpdate) {
   if (L.big_cnt[0] && L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[0];
     hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
@@ -1523,6 +1624,7 @@ static void launch_big_cover(const TaskList& L, const GemmArgs& g0, hipStream_t 
   if (L.big_cnt[1]) {
     g.tasks = L.tasks + L.big_off[1];
     hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
+  }
   }
   launch_bf16_segments<MODE, NP, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
 }
@@ -1562,6 +1664,9 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.gram = t.gram;
   g.poly = t.poly;
   g.gpart = t.gpart;
+  g.split_cnt = t.split_cnt;
+  g.part_norm = t.part_norm;
+  g.norm_mode = mode == kGram ? p.norm_mode : -1;
   g.ca = p.ca;
   g.cb = p.cb;
   g.cc = p.cc;
@@ -1574,21 +1679,8 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_split_sums(const DevTables& t, int only_active, hipStream_t st) {
-  for (int i = 0; i < t.n_split; ++i) {
-    const int mat = t.split_mats_host[i];
-    const int64_t nn = (int64_t)t.split_n_host[i] * t.split_n_host[i];
-    const int blocks = (int)((nn / 4 + 255) / 256 + 1);
-    hipLaunchKernelGGL(gram_split_sum_kernel, dim3(blocks), dim3(256), 0, st, t.mats, t.scalars, mat, only_active,
-                       t.gpart, t.gram);
-  }
-  return hipGetLastError();
-}
-
 hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
-  hipLaunchKernelGGL(gram_norm_partial_kernel, dim3(kNormSlices, t.n_mat), dim3(256), 0, st, t.mats, t.scalars,
-                     t.gram, t.part_norm, a.mode, a.only_active);
   hipLaunchKernelGGL(gram_norm_final_kernel, dim3((t.n_mat + 63) / 64), dim3(64), 0, st, t.mats, t.part_norm,
                      t.scalars, t.n_mat, a);
   return hipGetLastError();

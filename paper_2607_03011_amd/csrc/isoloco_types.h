@@ -1,5 +1,6 @@
 // Device-visible tables shared by the host planner and the HIP kernels.
 #pragma once
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace isoloco {
@@ -15,6 +16,9 @@ constexpr int kChunk = 4096;
 constexpr int kStreamThreads = 256;
 
 constexpr int kMaxWorkers = 128;
+
+// Most K slices of a split Gram product.
+constexpr int kMaxKSplit = 6;
 
 // One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
 // element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
@@ -37,7 +41,21 @@ struct MatInfo {
   int32_t tensor;    // index in the caller's layout
   int32_t chunk_begin, chunk_end;  // range of this matrix in the chunk table
   int32_t wide;      // 1 if the tensor is stored wide (rows < cols)
+  int32_t norm_off;  // first of this matrix's gram_tiles(n) Gram-norm partials
+  int32_t cnt_off;   // split-K Gram: first of its gram_tiles(n) arrival counters (-1 if not split)
 };
+
+// Output tiles of a symmetric n x n product that are computed: those on or
+// above the diagonal of the 128 x 128 tiling, tile (tm, tn) with tm <= tn at
+// index gram_tile_index(n, tm, tn).
+__host__ __device__ inline int gram_tiles(int n) {
+  const int T = (n + kBM - 1) / kBM;
+  return T * (T + 1) / 2;
+}
+__host__ __device__ inline int gram_tile_index(int n, int tm, int tn) {
+  const int T = (n + kBM - 1) / kBM;
+  return tm * T - tm * (tm - 1) / 2 + (tn - tm);
+}
 
 // Work item of the streaming kernels: at most kChunk elements of one tensor.
 // rows == 0: a contiguous run, element i at src + i (stored) and ws + i
@@ -71,9 +89,6 @@ struct MatScalars {
   int32_t active;   // 1 while the matrix still iterates (second phase of the schedule)
   int32_t qbuf;     // which X buffer holds the final polar factor
 };
-
-// Partial sums per matrix for the Gram norms (rows r, r + kNormSlices, ...).
-constexpr int kNormSlices = 32;
 
 // Work item of a batched matrix product: one output tile of one matrix.
 struct Task {

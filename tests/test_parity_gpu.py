@@ -153,6 +153,27 @@ BIG_MIXED = [(800, 576, KIND_ISO), (576, 800, KIND_ISO), (1000, 512, KIND_ISO), 
              (300, 260, KIND_ISO), (512, 1024, KIND_ISO), (256, 256, KIND_ISO), (40, 1, KIND_AVG)]
 
 
+# Tall matrices whose Gram is split along K (more than 4096 rows and at least
+# 4x as many rows as columns): ragged last K slices, ragged column tiles,
+# a column count that is not a multiple of 4, a wide-stored one.
+SPLIT_K = [(9000, 200, KIND_ISO), (198, 8200, KIND_ISO), (5000, 128, KIND_ISO), (50, 1, KIND_AVG)]
+
+
+@pytest.mark.parametrize("precision", [0, 1], ids=["mixed", "fp32"])
+def test_split_k_gram(iso, precision):
+    """The K slices of a split Gram tile are added by the last workgroup to
+    finish; its arrival counters are left at zero for the next launch (two
+    steps on one plan)."""
+    from workload import custom_layout
+    lay, n = custom_layout(SPLIT_K, align=4)
+    cfg = _cfg(lay, n, K=2)
+    dev = torch.device("cuda", 0)
+    plan = iso.IsoLoCoPlan(lay, n, 2, iso.ISOLOCO_F32, opts=dict(precision=precision), device=dev)
+    for seed in (12, 13):
+        _run_and_compare(iso, cfg, seed=seed, plan=plan)
+    plan.close()
+
+
 @pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
 def test_big_tiles_with_remainders(iso, precision):
     from workload import custom_layout
