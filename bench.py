@@ -172,6 +172,11 @@ def main():
                     help="exact: Algorithm 2 (converged polar factor, mean singular value); fast: "
                          "Section 4.3 (five Newton-Schulz steps, RMS of the singular values); clip_high / "
                          "clip_low: Section 4.5 (only the singular values above / below the mean set to it)")
+    ap.add_argument("--ell-mid", type=float, nargs=2, default=[0.0, 0.0],
+                    help="bounds of the middle phases of the polar schedule of matrices with m < 2n "
+                         "(0: the library's default, negative: none)")
+    ap.add_argument("--ell-mid-tall", type=float, nargs=2, default=[0.0, 0.0],
+                    help="the same for tall matrices (m >= 2n)")
     ap.add_argument("--ell-fast", type=float, default=0.0,
                     help="short-schedule bound (0: library default; negative: one phase)")
     args = ap.parse_args()
@@ -198,13 +203,14 @@ def main():
             "bf16x6": iso.ISOLOCO_PREC_BF16X6, "fp32": iso.ISOLOCO_PREC_FP32}[args.precision]
     vopts = {"exact": {}, "fast": dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS),
              "clip_high": dict(clip=iso.ISOLOCO_CLIP_HIGH), "clip_low": dict(clip=iso.ISOLOCO_CLIP_LOW)}[args.variant]
-    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, **vopts),
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, ell_mid=tuple(args.ell_mid),
+                                                                       ell_mid_tall=tuple(args.ell_mid_tall), **vopts),
                            device=dev)
-    sched, n_short = plan.schedule_split()
-    n_polar = len(sched)
+    phase_ends = {"square": plan.schedule_phases(tall=0), "tall": plan.schedule_phases(tall=1)}
     stream = torch.cuda.current_stream(dev)
-    print("bench: workload %s, %d params, K=%d, %d polar steps (%d in the short phase), workspace %.2f GB" %
-          (cfg.name, cfg.n_params, cfg.K, n_polar, n_short, plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
+    print("bench: workload %s, %d params, K=%d, polar phases end at %s (m < 2n) and %s (m >= 2n), "
+          "workspace %.2f GB" % (cfg.name, cfg.n_params, cfg.K, phase_ends["square"], phase_ends["tall"],
+                                 plan.ws_bytes / 1e9), file=sys.stderr, flush=True)
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * (1 << 20) // 4
@@ -295,7 +301,7 @@ def main():
         "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
                    "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
                    "variant": args.variant,
-                   "polar_steps": n_polar, "short_phase_steps": n_short, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
+                   "polar_phase_ends": phase_ends, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
         "roofline": {"bound": "mfma", "kernel": "gemm_%s_kernel (Gram, polynomial and update products)" %
                      ("f32" if args.precision == "fp32" else "bf16"), "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(gemm_tfs / peak, 4),

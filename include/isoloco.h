@@ -97,9 +97,9 @@ typedef struct {
                         of bf16x6 for this product), bf16x3 for every other product      */
   float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
                         whose Q^T Q is then the identity to 5e-5 stops there; the others run
-                        a continuation that reaches [sqrt(ell_fast ell0), 1], the same test,
-                        and a last one that reaches [ell0, 1] (default 1e-4; a negative value
-                        runs the single schedule for [ell0, 1])                                */
+                        a continuation that reaches [ell_mid, 1], the same test, and a last
+                        one that reaches [ell0, 1] (default 1e-3; a negative value runs the
+                        single schedule for [ell0, 1])                                         */
   /* Variants of the step that the paper studies (all 0: Algorithm 2). */
   int32_t orth;      /* ISOLOCO_ORTH_POLAR: Q = U V^T, the converged polar factor (Algorithm 2);
                         ISOLOCO_ORTH_NS5: the fast variant's five Newton-Schulz steps of the
@@ -123,6 +123,16 @@ typedef struct {
                         above / below the mean to the mean, keeping U, V and the other
                         singular values (Section 4.5).  Needs ORTH_POLAR and SCALE_MEAN; a
                         second polar iteration runs on Delta - sigma_bar Q                 */
+  float ell_mid[2];  /* bounds of the middle phases (see ell_fast), each followed by the same
+                        test, for matrices with m < 2n (m x n in tall coordinates, m >= n);
+                        ell_mid[0] defaults to 2e-8, ell_mid[1] to none.  A negative bound,
+                        or one not strictly between the bounds before and ell0, is left out
+                        (with both left out, the continuation after the short schedule
+                        reaches [ell0, 1])                                                 */
+  float ell_mid_tall[2]; /* the same for tall matrices (m >= 2n), whose smallest singular
+                        value stays away from zero for noise-like spectra: defaults 1e-4
+                        and 2e-8.  The two classes iterate in the same launches, each with
+                        its own coefficients                                               */
 } isoloco_options;
 
 #define ISOLOCO_PREC_MIXED 0
@@ -195,21 +205,24 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
  * (n_tensors entries, in layout order).  Waits for that aggregate's stream. */
 isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out, int32_t n_tensors);
 
-/* The polynomial schedule of the plan: for step k, p_k(x) = c[3k] x + c[3k+1] x^3 + c[3k+2] x^5
- * (on singular values normalised by ||Delta^T Delta||_F^(1/2)).  Writes at most
- * max_steps triples; *n_steps receives the schedule length and *n_short (if not
- * NULL) the length of the short first phase (= *n_steps for one phase).  Host only. */
-isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps,
+/* The polynomial schedule of one class of matrices (tall = 1: m >= 2n in tall
+ * coordinates, m x n with m >= n; tall = 0: the others): for step k, p_k(x) =
+ * c[3k] x + c[3k+1] x^3 + c[3k+2] x^5 (on singular values normalised by
+ * ||Delta^T Delta||_F^(1/2)).  Writes at most max_steps triples; *n_steps
+ * receives the schedule length and *n_short (if not NULL) the length of the
+ * short first phase (= *n_steps for one phase).  Host only. */
+isoloco_status isoloco_schedule(isoloco_plan_t plan, int32_t tall, double* coeffs, int32_t max_steps,
                                 int32_t* n_steps, int32_t* n_short);
 
-/* The phases of the schedule: ends[i] is the number of steps done when phase
- * i ends (increasing; the last equals the schedule length).  Phase 0 is the
- * short schedule for [ell_fast, 1]; each later phase continues it for a
- * smaller bound (the geometric mean of ell_fast and ell0, then ell0).  After
- * every phase but the last, the matrices whose Q^T Q is the identity to the
- * switch tolerance stop.  Writes at most max_phases entries; *n_phases
- * receives the count.  Host only. */
-isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t* ends, int32_t max_phases,
+/* The phases of one class's schedule (tall as above): ends[i] is the number of
+ * steps done when phase i ends (increasing; the last equals the schedule
+ * length).  Phase 0 is the short schedule for [ell_fast, 1]; each later phase
+ * continues it for a smaller bound (the class's middle bounds, then ell0).
+ * After every phase but the last, the matrices whose Q^T Q is the identity to
+ * the switch tolerance stop.  Both classes iterate in the same launches; a
+ * class whose schedule is shorter stops at its end.  Writes at most max_phases
+ * entries; *n_phases receives the count.  Host only. */
+isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t tall, int32_t* ends, int32_t max_phases,
                                        int32_t* n_phases);
 
 /* Per-kernel timing of the last aggregate, measured with HIP events recorded

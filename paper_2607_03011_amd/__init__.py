@@ -61,7 +61,8 @@ class isoloco_options(ctypes.Structure):
     _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
                 ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float),
                 ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
-                ("target", ctypes.c_int32), ("clip", ctypes.c_int32)]
+                ("target", ctypes.c_int32), ("clip", ctypes.c_int32), ("ell_mid", ctypes.c_float * 2),
+                ("ell_mid_tall", ctypes.c_float * 2)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):
@@ -98,9 +99,9 @@ _sig = {
     "isoloco_aggregate": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), _P, ctypes.c_float,
                                          ctypes.c_float, ctypes.c_float, _P]),
     "isoloco_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_tensor_stats), ctypes.c_int32]),
-    "isoloco_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
+    "isoloco_schedule": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
                                         ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
-    "isoloco_schedule_phases": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+    "isoloco_schedule_phases": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                                ctypes.POINTER(ctypes.c_int32)]),
     "isoloco_plan_destroy": (ctypes.c_int, [_P]),
     "isoloco_enable_timing": (ctypes.c_int, [_P, ctypes.c_int32]),
@@ -174,22 +175,25 @@ def isoloco_get_stats(plan, n_tensors):
     return [arr[i] for i in range(n_tensors)]
 
 
-def isoloco_schedule(plan, max_steps=256, with_split=False):
-    """List of (a, b, c) per step; with_split=True also returns the length of
-    the short first phase."""
+def isoloco_schedule(plan, max_steps=256, with_split=False, tall=0):
+    """List of (a, b, c) per step of the square-ish (tall=0) or tall (tall=1)
+    matrices' schedule; with_split=True also returns the length of the short
+    first phase."""
     buf = (ctypes.c_double * (3 * max_steps))()
     n = ctypes.c_int32()
     ns = ctypes.c_int32()
-    _check(_lib.isoloco_schedule(plan, buf, max_steps, ctypes.byref(n), ctypes.byref(ns)), "isoloco_schedule")
+    _check(_lib.isoloco_schedule(plan, int(tall), buf, max_steps, ctypes.byref(n), ctypes.byref(ns)),
+           "isoloco_schedule")
     sched = [tuple(buf[3 * k: 3 * k + 3]) for k in range(min(n.value, max_steps))]
     return (sched, ns.value) if with_split else sched
 
 
-def isoloco_schedule_phases(plan, max_phases=16):
-    """Steps done at the end of each phase of the schedule (the last is its length)."""
+def isoloco_schedule_phases(plan, max_phases=16, tall=0):
+    """Steps done at the end of each phase of a class's schedule (the last is its length)."""
     buf = (ctypes.c_int32 * max_phases)()
     n = ctypes.c_int32()
-    _check(_lib.isoloco_schedule_phases(plan, buf, max_phases, ctypes.byref(n)), "isoloco_schedule_phases")
+    _check(_lib.isoloco_schedule_phases(plan, int(tall), buf, max_phases, ctypes.byref(n)),
+           "isoloco_schedule_phases")
     return [buf[i] for i in range(min(n.value, max_phases))]
 
 
@@ -262,14 +266,14 @@ class IsoLoCoPlan:
     def timing(self):
         return isoloco_get_timing(self.handle)
 
-    def schedule(self):
-        return isoloco_schedule(self.handle)
+    def schedule(self, tall=0):
+        return isoloco_schedule(self.handle, tall=tall)
 
-    def schedule_split(self):
-        return isoloco_schedule(self.handle, with_split=True)
+    def schedule_split(self, tall=0):
+        return isoloco_schedule(self.handle, with_split=True, tall=tall)
 
-    def schedule_phases(self):
-        return isoloco_schedule_phases(self.handle)
+    def schedule_phases(self, tall=0):
+        return isoloco_schedule_phases(self.handle, tall=tall)
 
     def close(self):
         if self.handle is not None:

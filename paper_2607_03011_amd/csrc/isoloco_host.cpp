@@ -315,14 +315,18 @@ struct isoloco_plan_s {
   TaskListHost gram_list, poly_list, update_list;
   int64_t n_norm = 0;  // Gram-norm partial slots (gram_tiles(n) per matrix)
   int64_t n_cnt = 0;   // split-K tile counters
-  std::vector<double> sched;  // short schedule followed by its continuation phases
-  int n_short = 0;            // steps of the short schedule
-  std::vector<int> phase_end; // steps at the end of each phase (the last is the length)
+  // Per schedule class (kSchedSquare, kSchedTall): the short schedule
+  // followed by its continuation phases, and the steps at the end of each
+  // phase (the last is the class's length).
+  std::vector<double> sched[kSchedClasses];
+  std::vector<int> phase_end[kSchedClasses];
+  int n_steps = 0;            // longest schedule: polar steps the launch sequence runs
+  std::vector<float> coef;    // device table: [class][n_steps][3], padded with each class's last step
   int64_t n2d = 0;   // elements of one Delta / X buffer
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
-  size_t off_pnorm = 0, off_cnt = 0;
+  size_t off_pnorm = 0, off_cnt = 0, off_coef = 0;
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
   size_t off_poly = 0, off_gpart = 0, total = 0;
@@ -339,6 +343,47 @@ struct isoloco_plan_s {
 };
 
 namespace {
+
+// Phases of one schedule class: a short schedule that assumes sigma_min >=
+// ell_fast, then continuations for smaller bounds, the middle bounds that lie
+// strictly between the bounds before them and ell0, and ell0.  After every
+// phase but the last, each matrix whose Q^T Q is already the identity stops;
+// the others run the next phase, built for what the phases so far made of its
+// bound.
+void build_phases(const isoloco_options& o, const float (&mid)[2], std::vector<double>& sched,
+                  std::vector<int>& ends) {
+  sched.clear();
+  ends.clear();
+  if (o.orth == ISOLOCO_ORTH_NS5) {
+    // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
+    // quintic (Section 4.3; the paper's own coefficients are not printed)
+    for (int k = 0; k < kNs5Steps; ++k) sched.insert(sched.end(), kNs5Coeffs, kNs5Coeffs + 3);
+  } else if (o.ell_fast > o.ell0) {
+    sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
+    ends.push_back((int)sched.size() / 3);
+    std::vector<double> bounds;
+    double above = o.ell_fast;
+    for (float b : mid)
+      if (b > o.ell0 && b < above) {
+        bounds.push_back(b);
+        above = b;
+      }
+    bounds.push_back(o.ell0);
+    for (double b : bounds) {
+      const int done = (int)sched.size() / 3;
+      double lb = b;
+      for (int k = 0; k < done; ++k) lb = peval(&sched[3 * k], lb);
+      if (done >= o.max_steps || lb >= 1.0 - o.tol) continue;
+      const std::vector<double> rest = build_schedule(lb, o.tol, o.max_steps - done);
+      if (rest.empty()) continue;
+      sched.insert(sched.end(), rest.begin(), rest.end());
+      ends.push_back((int)sched.size() / 3);
+    }
+  } else {
+    sched = build_schedule(o.ell0, o.tol, o.max_steps);
+  }
+  if (ends.empty() || ends.back() != (int)sched.size() / 3) ends.push_back((int)sched.size() / 3);
+}
 
 void plan_matrices(isoloco_plan_s* p) {
   const int V = p->dtype == ISOLOCO_BF16 ? 8 : 4;
@@ -367,6 +412,7 @@ void plan_matrices(isoloco_plan_s* p) {
     mi.sq_off = sq;
     mi.vec = (mi.m % 4 == 0 && mi.n % 4 == 0) ? 1 : 0;
     mi.tensor = (int32_t)t;
+    mi.sched = mi.m >= 2 * (int64_t)mi.n ? kSchedTall : kSchedSquare;
     // Split the Gram's K dimension of a tall matrix (few output tiles, long
     // K) so that no single tile dominates the launch.  Every slice writes an
     // n x n partial that is read back once, so the count stays small: six
@@ -547,6 +593,7 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_ptr = take(p->chunks.size() * sizeof(double));
   p->off_pnorm = take((size_t)p->n_norm * sizeof(double));
   p->off_cnt = take((size_t)p->n_cnt * sizeof(int));
+  p->off_coef = take(p->coef.size() * sizeof(float));
   p->off_delta = take((size_t)p->n2d * sizeof(float));
   p->off_x0 = take((size_t)p->n2d * sizeof(float));
   p->off_x1 = take((size_t)p->n2d * sizeof(float));
@@ -587,6 +634,8 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
   t.part_norm = reinterpret_cast<double*>(w + p->off_pnorm);
   t.split_cnt = reinterpret_cast<int*>(w + p->off_cnt);
+  t.coef = reinterpret_cast<const float*>(w + p->off_coef);
+  t.n_steps = p->n_steps;
   t.delta = reinterpret_cast<float*>(w + p->off_delta);
   t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
   t.x[1] = reinterpret_cast<float*>(w + p->off_x1);
@@ -629,13 +678,20 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.ell0 == 0.f) o.ell0 = 1e-10f;
   if (o.tol == 0.f) o.tol = 1e-6f;
   if (o.check == 0) o.check = 1;
-  if (o.ell_fast == 0.f) o.ell_fast = 1e-4f;
+  if (o.ell_fast == 0.f) o.ell_fast = 1e-3f;
+  if (o.ell_mid[0] == 0.f) o.ell_mid[0] = 2e-8f;
+  if (o.ell_mid[1] == 0.f) o.ell_mid[1] = -1.f;
+  if (o.ell_mid_tall[0] == 0.f) o.ell_mid_tall[0] = 1e-4f;
+  if (o.ell_mid_tall[1] == 0.f) o.ell_mid_tall[1] = 2e-8f;
   if (o.max_steps < 1 || o.max_steps > 200)
     return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
   if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
   if (!(o.tol > 0.f && o.tol < 0.5f)) return fail(ISOLOCO_ERR_INVALID_ARG, "tol must be in (0, 0.5)");
   if (!(o.ell_fast < 1.f) || std::isnan(o.ell_fast))
     return fail(ISOLOCO_ERR_INVALID_ARG, "ell_fast must be < 1 (negative: one phase)");
+  for (float b : {o.ell_mid[0], o.ell_mid[1], o.ell_mid_tall[0], o.ell_mid_tall[1]})
+    if (!(b < 1.f) || std::isnan(b))
+      return fail(ISOLOCO_ERR_INVALID_ARG, "ell_mid bounds must be < 1 (negative: none)");
   if (o.check != 1 && o.check != -1) return fail(ISOLOCO_ERR_INVALID_ARG, "check must be 1 or -1");
   if (o.precision < ISOLOCO_PREC_MIXED || o.precision > ISOLOCO_PREC_BF16X6)
     return fail(ISOLOCO_ERR_INVALID_ARG, "unknown precision %d", o.precision);
@@ -684,36 +740,16 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     p->dtype = worker_dtype;
     p->opts = o;
     plan_matrices(p);
-    // Phases: a short schedule that assumes sigma_min >= ell_fast, then
-    // continuations for ever smaller bounds, first the geometric mean of
-    // ell_fast and ell0, then ell0 itself.  After every phase but the last,
-    // each matrix whose Q^T Q is already the identity stops; the others run
-    // the next phase, built for what the phases so far made of its bound.
-    if (o.orth == ISOLOCO_ORTH_NS5) {
-      // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
-      // quintic (Section 4.3; the paper's own coefficients are not printed)
-      p->sched.clear();
-      for (int k = 0; k < kNs5Steps; ++k) p->sched.insert(p->sched.end(), kNs5Coeffs, kNs5Coeffs + 3);
-    } else if (o.ell_fast > o.ell0) {
-      p->sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
-      p->phase_end.push_back((int)p->sched.size() / 3);
-      const double bounds[2] = {std::sqrt((double)o.ell_fast * o.ell0), o.ell0};
-      for (double b : bounds) {
-        const int done = (int)p->sched.size() / 3;
-        double lb = b;
-        for (int k = 0; k < done; ++k) lb = peval(&p->sched[3 * k], lb);
-        if (done >= o.max_steps || lb >= 1.0 - o.tol) continue;
-        const std::vector<double> rest = build_schedule(lb, o.tol, o.max_steps - done);
-        if (rest.empty()) continue;
-        p->sched.insert(p->sched.end(), rest.begin(), rest.end());
-        p->phase_end.push_back((int)p->sched.size() / 3);
+    for (int c = 0; c < kSchedClasses; ++c)
+      build_phases(o, c == kSchedTall ? o.ell_mid_tall : o.ell_mid, p->sched[c], p->phase_end[c]);
+    p->n_steps = 0;
+    for (int c = 0; c < kSchedClasses; ++c) p->n_steps = std::max(p->n_steps, p->phase_end[c].back());
+    p->coef.assign((size_t)kSchedClasses * p->n_steps * 3, 0.f);
+    for (int c = 0; c < kSchedClasses; ++c)
+      for (int k = 0; k < p->n_steps; ++k) {
+        const int kk = std::min(k, (int)p->sched[c].size() / 3 - 1);
+        for (int q = 0; q < 3; ++q) p->coef[((size_t)c * p->n_steps + k) * 3 + q] = (float)p->sched[c][3 * kk + q];
       }
-    } else {
-      p->sched = build_schedule(o.ell0, o.tol, o.max_steps);
-    }
-    if (p->phase_end.empty() || p->phase_end.back() != (int)p->sched.size() / 3)
-      p->phase_end.push_back((int)p->sched.size() / 3);
-    p->n_short = p->phase_end.front();
     plan_workspace(p);
   } catch (...) {
     delete p;
@@ -748,7 +784,8 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
       (e = up(plan->off_chunks, plan->chunks.data(), plan->chunks.size() * sizeof(Chunk))) != hipSuccess ||
       (e = up(plan->off_gt, plan->gram_list.tasks.data(), plan->gram_list.tasks.size() * sizeof(Task))) != hipSuccess ||
       (e = up(plan->off_pt, plan->poly_list.tasks.data(), plan->poly_list.tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess)
+      (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_coef, plan->coef.data(), plan->coef.size() * sizeof(float))) != hipSuccess)
     return hip_fail(e, "copying plan tables to the workspace");
   if (!plan->mats.empty()) {
     e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
@@ -835,16 +872,22 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   e = timed(kPhReduce, [&] { return launch_reduce(t, a, st); });
   if (e != hipSuccess) return hip_fail(e, "reduce launch");
   if (t.n_mat > 0) {
-    const int S = (int)plan->sched.size() / 3;
-    const std::vector<int>& ends = plan->phase_end;
-    const int n_ph = (int)ends.size();
-    const bool phased = n_ph > 1;
-    const int buf_total = (S - 1) & 1;
-    // index of the phase that ends after step k, -1 if none but the last does
-    auto ends_phase = [&](int k) {
-      for (int i = 0; i + 1 < n_ph; ++i)
-        if (ends[i] == k + 1) return i;
-      return -1;
+    const int S = plan->n_steps;
+    FroArgs fa{};
+    fa.fixed_g = ns5 ? 1 : 0;
+    for (int c = 0; c < kSchedClasses; ++c) {
+      fa.steps_total[c] = plan->phase_end[c].back();
+      fa.buf_total[c] = (fa.steps_total[c] - 1) & 1;
+    }
+    // what the end of step k (k + 1 steps done) means for class c: a switch
+    // (a phase but the last ends), the end of the class's schedule before the
+    // launch sequence's end, or nothing
+    auto action_after = [&](int c, int k, bool check) {
+      const std::vector<int>& ends = plan->phase_end[c];
+      if (k + 1 == ends.back()) return k + 1 < S ? (check ? kActFinal : kActStop) : kActNone;
+      for (size_t i = 0; i + 1 < ends.size(); ++i)
+        if (ends[i] == k + 1) return kActSwitch;
+      return kActNone;
     };
     const char* what = "";
     // The polar iteration on the matrices in tt.delta (state in tt.scalars;
@@ -853,38 +896,37 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     auto polar = [&](const DevTables& tt, bool check) -> hipError_t {
       hipError_t r;
       what = "fro launch";
-      if ((r = timed(kPhOther, [&] { return launch_fro(tt, S, buf_total, ns5 ? 1 : 0, st); })) != hipSuccess)
-        return r;
+      if ((r = timed(kPhOther, [&] { return launch_fro(tt, fa, st); })) != hipSuccess) return r;
       NormArgs na{};
       na.flag_unconverged = ns5 ? 0 : 1;
-      na.steps_total = S;
-      na.buf_total = buf_total;
       na.tol_switch = kSwitchTol;
+      for (int c = 0; c < kSchedClasses; ++c) {
+        na.steps_total[c] = fa.steps_total[c];
+        na.buf_total[c] = fa.buf_total[c];
+      }
       auto gram = [&](const PolarStep& ps) -> hipError_t {
         return timed(kPhGram, [&] { return launch_gemm(tt, 0, ps, st); });
       };
-      auto norm = [&](int mode, int only_active) -> hipError_t {
+      auto norm = [&](int mode) -> hipError_t {
         na.mode = mode;
-        na.only_active = only_active;
+        na.only_active = 1;
         return timed(kPhOther, [&] { return launch_gram_norm(tt, na, st); });
       };
       const float* xin = tt.delta;
+      bool have_gram = false;  // the Gram of xin was formed by the last phase end's check
       for (int k = 0; k < S; ++k) {
         PolarStep ps{};
         ps.xin = xin;
         ps.xout = tt.x[k & 1];
-        ps.ca = (float)plan->sched[3 * k];
-        ps.cb = (float)plan->sched[3 * k + 1];
-        ps.cc = (float)plan->sched[3 * k + 2];
+        ps.step = k;
         ps.first = (k == 0);
-        ps.only_active = (k >= ends[0]);
+        ps.only_active = 1;
         ps.arith = step_arith(plan->opts.precision, k, kProdGram);
         // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
         ps.norm_mode = (k == 0 && !ns5) ? kNormFirst : -1;
         what = "polar step launch";
-        // the first Gram of a later phase was formed by the switch check
-        if (!(k > 0 && ends_phase(k - 1) >= 0) && (r = gram(ps)) != hipSuccess) return r;
-        if (ps.norm_mode == kNormFirst && (r = norm(kNormFirst, 0)) != hipSuccess) return r;
+        if (!have_gram && (r = gram(ps)) != hipSuccess) return r;
+        if (ps.norm_mode == kNormFirst && (r = norm(kNormFirst)) != hipSuccess) return r;
         PolarStep pp = ps, pu = ps;
         pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
         pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
@@ -892,29 +934,44 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
             (r = timed(kPhUpdate, [&] { return launch_gemm(tt, 2, pu, st); })) != hipSuccess)
           return r;
         xin = ps.xout;
-        const int ph = ends_phase(k);
-        if (ph >= 0) {
-          // the matrices still running check Q^T Q = I; those that pass stop
-          // here with the factor in x[k & 1]
+        have_gram = false;
+        bool any = false, residual = false;
+        for (int c = 0; c < kSchedClasses; ++c) {
+          na.action[c] = action_after(c, k, check);
+          any = any || na.action[c] != kActNone;
+          residual = residual || na.action[c] == kActSwitch || na.action[c] == kActFinal;
+        }
+        if (!any) continue;
+        // a phase end: the matrices still running check Q^T Q = I; those
+        // that pass (or whose schedule is done) stop here with the factor in
+        // x[k & 1].  The check's Gram is the next step's.
+        na.steps_here = k + 1;
+        na.buf_here = k & 1;
+        what = "switch check launch";
+        if (residual) {
           PolarStep pc{};
           pc.xin = xin;
-          pc.only_active = ph > 0;
+          pc.only_active = 1;
           pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
-          pc.norm_mode = kNormSwitch;
-          na.steps_short = k + 1;
-          na.buf_short = k & 1;
-          what = "switch check launch";
-          if ((r = gram(pc)) != hipSuccess || (r = norm(kNormSwitch, pc.only_active)) != hipSuccess) return r;
+          pc.norm_mode = kNormPhase;
+          if ((r = gram(pc)) != hipSuccess) return r;
+          have_gram = true;
         }
+        if ((r = norm(kNormPhase)) != hipSuccess) return r;
       }
       if (check) {
+        // the classes whose schedules run to the end of the sequence
+        for (int c = 0; c < kSchedClasses; ++c)
+          na.action[c] = plan->phase_end[c].back() == S ? kActFinal : kActNone;
+        na.steps_here = S;
+        na.buf_here = (S - 1) & 1;
         PolarStep pc{};
         pc.xin = xin;
-        pc.only_active = phased ? 1 : 0;
+        pc.only_active = 1;
         pc.arith = step_arith(plan->opts.precision, S, kProdGram);
-        pc.norm_mode = kNormFinal;
+        pc.norm_mode = kNormPhase;
         what = "check launch";
-        if ((r = gram(pc)) != hipSuccess || (r = norm(kNormFinal, pc.only_active)) != hipSuccess) return r;
+        if ((r = gram(pc)) != hipSuccess || (r = norm(kNormPhase)) != hipSuccess) return r;
       }
       return hipSuccess;
     };
@@ -988,24 +1045,28 @@ isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out,
   return ISOLOCO_OK;
 }
 
-isoloco_status isoloco_schedule(isoloco_plan_t plan, double* coeffs, int32_t max_steps, int32_t* n_steps,
-                                int32_t* n_short) {
+isoloco_status isoloco_schedule(isoloco_plan_t plan, int32_t tall, double* coeffs, int32_t max_steps,
+                                int32_t* n_steps, int32_t* n_short) {
   if (!plan || !n_steps) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
-  const int S = (int)plan->sched.size() / 3;
+  if (tall != 0 && tall != 1) return fail(ISOLOCO_ERR_INVALID_ARG, "tall must be 0 or 1");
+  const std::vector<double>& sched = plan->sched[tall ? kSchedTall : kSchedSquare];
+  const int S = (int)sched.size() / 3;
   *n_steps = S;
-  if (n_short) *n_short = plan->n_short;
+  if (n_short) *n_short = plan->phase_end[tall ? kSchedTall : kSchedSquare].front();
   if (coeffs)
-    for (int i = 0; i < 3 * std::min<int>(S, std::max(max_steps, 0)); ++i) coeffs[i] = plan->sched[i];
+    for (int i = 0; i < 3 * std::min<int>(S, std::max(max_steps, 0)); ++i) coeffs[i] = sched[i];
   return ISOLOCO_OK;
 }
 
-isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t* ends, int32_t max_phases,
+isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t tall, int32_t* ends, int32_t max_phases,
                                        int32_t* n_phases) {
   if (!plan || !n_phases) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
-  const int n = (int)plan->phase_end.size();
+  if (tall != 0 && tall != 1) return fail(ISOLOCO_ERR_INVALID_ARG, "tall must be 0 or 1");
+  const std::vector<int>& pe = plan->phase_end[tall ? kSchedTall : kSchedSquare];
+  const int n = (int)pe.size();
   *n_phases = n;
   if (ends)
-    for (int i = 0; i < std::min<int>(n, std::max(max_phases, 0)); ++i) ends[i] = plan->phase_end[i];
+    for (int i = 0; i < std::min<int>(n, std::max(max_phases, 0)); ++i) ends[i] = pe[i];
   return ISOLOCO_OK;
 }
 

@@ -40,6 +40,8 @@ struct DevTables {
   float* gram;
   float* poly;
   float* gpart;
+  const float* coef;  // polynomial coefficients [class][n_steps][3] (schedule classes of MatInfo::sched)
+  int n_steps;
   int n_mat, n_chunks, n_iso_chunks;
 };
 
@@ -64,7 +66,7 @@ struct PolarStep {
   const float* xin_alt;  // if set, matrix m reads X from xin_alt when its qbuf is 1 (Gram mode)
   const float* bin;      // if set, the Gram's second operand (same layout as X): X^T B
   float* xout;
-  float ca, cb, cc;
+  int step;         // polar step: the polynomial product takes each matrix's coefficients of this step
   int first;
   int only_active;  // 1: skip matrices whose scalars say active == 0
   int arith;        // Arith
@@ -72,26 +74,40 @@ struct PolarStep {
                     // leaves in DevTables::part_norm (kNormFirst: sum A^2, others sum (A - I)^2)
 };
 
-// Gram-norm modes
+// Gram-norm modes (a Gram launch with norm_mode >= 0 leaves the per-tile
+// partials that gram_norm_final_kernel reads)
 enum NormMode {
-  kNormFirst = 0,   // gscale = ||A||_F^(-1/2) of the first step
-  kNormFinal = 1,   // final check: resid and the not-converged flag
-  kNormSwitch = 2,  // end of a phase but the last: resid; converged matrices stop
+  kNormFirst = 0,  // gscale = ||A||_F^(-1/2) of the first step (partials of sum A^2)
+  kNormPhase = 1,  // a phase end: resid from sum (A - I)^2, then each class's action
+};
+
+// What a phase end does to the matrices of one schedule class
+enum NormAction {
+  kActNone = 0,    // not this class's phase end: nothing
+  kActSwitch = 1,  // resid; matrices within tol_switch stop here, the others go on
+  kActFinal = 2,   // the class's schedule is done: resid, the not-converged flag, stop
+  kActStop = 3,    // the class's schedule is done, no residual wanted: stop
 };
 
 struct NormArgs {
   int mode;
   int only_active;
-  int steps_short, steps_total;  // steps done at this phase's end, schedule length
-  int buf_short, buf_total;      // X buffer holding the result after this phase, after all
-  float tol_switch;              // residual below which a matrix stops at the phase's end
-  int flag_unconverged;          // final check: flag residuals above 1e-3 (not for a fixed-length variant)
+  int action[kSchedClasses];
+  int steps_here, buf_here;  // steps done at this phase end, X buffer holding their result
+  int steps_total[kSchedClasses], buf_total[kSchedClasses];  // per class: schedule length, its buffer
+  float tol_switch;          // residual below which a matrix stops at a switch
+  int flag_unconverged;      // kActFinal: flag residuals above 1e-3 (not for a fixed-length variant)
+};
+
+// Initial per-matrix iteration state: steps and result buffer of each class's full schedule
+struct FroArgs {
+  int steps_total[kSchedClasses], buf_total[kSchedClasses];
+  int fixed_g;  // the first step uses g = 1 (no Gram-norm scaling)
 };
 
 hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
 // also initialises the per-matrix iteration state (active, qbuf, steps)
-// fixed_g: the first step uses g = 1 (no Gram-norm scaling)
-hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fixed_g, hipStream_t st);
+hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st);
 // mode: 0 Gram, 1 polynomial, 2 update
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st);
 // per-matrix decisions from the norm partials of the Gram launched before with

@@ -308,7 +308,7 @@ __device__ __forceinline__ double wave_sum_range(const double* part, int begin, 
 // ||Delta||_F per matrix (one wavefront per matrix).
 __global__ void __launch_bounds__(64)
 fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
-           MatScalars* __restrict__ sc, int n_mat, int steps_total, int buf_total, int fixed_g) {
+           MatScalars* __restrict__ sc, int n_mat, FroArgs a) {
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
   const double s = wave_sum_range(part_sq, mi.chunk_begin, mi.chunk_end);
@@ -319,12 +319,12 @@ fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
   if (!isfinite(s)) o.flags |= 1;
   else if (s == 0.0) o.flags |= 2;
   o.inv_fro = (o.flags == 0) ? (float)(1.0 / sqrt(s)) : 0.f;
-  o.gscale = (fixed_g && o.flags == 0) ? 1.f : 0.f;  // else set from the first Gram
+  o.gscale = (a.fixed_g && o.flags == 0) ? 1.f : 0.f;  // else set from the first Gram
   o.sigma_bar = 0.f;
   o.resid = -1.f;
-  o.steps = steps_total;
+  o.steps = a.steps_total[mi.sched];
   o.active = 1;
-  o.qbuf = buf_total;
+  o.qbuf = a.buf_total[mi.sched];
   sc[m] = o;
 }
 
@@ -424,7 +424,8 @@ struct GemmArgs {
   float* gpart;       // split-K Gram partials
   int* split_cnt;     // split-K Gram: arrival counter per output tile
   double* part_norm;  // Gram: per-tile partial sums of squares (norm_mode >= 0)
-  float ca, cb, cc;   // step coefficients p(x) = ca x + cb x^3 + cc x^5
+  const float* coef;  // Poly: coefficients [class][n_steps][3] of p(x) = ca x + cb x^3 + cc x^5
+  int step, n_steps;  // Poly: this step, and the table's steps per class
   int first;          // 1 on the first step (inputs pre-scaled by 1/||Delta||_F, g applied)
   int only_active;    // 1: tasks of matrices that stopped iterating return at once
   int norm_mode;      // Gram: -1, or kNormFirst (sum A^2) / other (sum (A - I)^2) per tile
@@ -441,6 +442,7 @@ struct GemmSetup {
   int64_t sr, sc;
   float xscale;  // applied to X operands as they are loaded (1/||Delta||_F on the first step)
   float gs;      // normalisation g of the first step (1 afterwards)
+  float ca, cb, cc;  // Poly: this matrix's step coefficients (its schedule class)
 };
 
 template <int MODE, int TILE = kBM>
@@ -469,6 +471,10 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     s.M = n;
     s.N = n;
   } else if (MODE == kPoly) {
+    const float* c = g.coef + ((int64_t)mi.sched * g.n_steps + g.step) * 3;
+    s.ca = c[0];
+    s.cb = c[1];
+    s.cc = c[2];
     const float* a = g.gram + mi.sq_off;
     // A is symmetric (its diagonal tiles to rounding), so the operand A[k][i]
     // is read as A[i][k]: k-contiguous rows, the faster loads
@@ -513,7 +519,7 @@ __device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup
   }
   const int n = s.mi.n;
   // (g = 0 marks a zero or non-finite Delta: P' = 0 then, and rho is kept finite)
-  const float rho = s.gs != 0.f ? g.cb / (g.cc * s.gs * s.gs) : 0.f;
+  const float rho = s.gs != 0.f ? s.cb / (s.cc * s.gs * s.gs) : 0.f;
   const float* A = g.gram + s.mi.sq_off;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WNC, wn = wave % WNC;
@@ -749,7 +755,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup
           // so that the update is the plain product X' = X P; the accumulators
           // hold rho A + A A (see gemm_acc_init)
           const float g2 = s.gs * s.gs;
-          const float gamma = g.cc * g2 * g2 * s.gs, diag = g.ca * s.gs;
+          const float gamma = s.cc * g2 * g2 * s.gs, diag = s.ca * s.gs;
           float* out = g.poly + mi.sq_off;
           floatx4 v;
 #pragma unroll
@@ -1353,29 +1359,37 @@ __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs 
   }
 }
 
-// Per-matrix decisions from the norm partials (see NormMode).
+// Per-matrix decisions from the norm partials (see NormMode, NormAction).
 __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part,
                                        MatScalars* __restrict__ sc, int n_mat, NormArgs a) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
   if (m >= n_mat) return;
   MatScalars& o = sc[m];
   if (a.only_active && !o.active) return;
+  const MatInfo mi = mats[m];
+  const int act = a.mode == kNormFirst ? kActNone : a.action[mi.sched];
+  if (a.mode != kNormFirst && act == kActNone) return;
+  if (act == kActStop) {
+    o.active = 0;
+    return;
+  }
   double s = 0.0;
-  const int nt = gram_tiles(mats[m].n);
-  for (int x = 0; x < nt; ++x) s += part[mats[m].norm_off + x];
+  const int nt = gram_tiles(mi.n);
+  for (int x = 0; x < nt; ++x) s += part[mi.norm_off + x];
   if (a.mode == kNormFirst) {
     o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
     return;
   }
-  o.resid = (float)sqrt(s / mats[m].n);
-  if (a.mode == kNormSwitch) {
+  o.resid = (float)sqrt(s / mi.n);
+  if (act == kActSwitch) {
     // stop at the end of this phase when every singular value is already at 1
     const bool go_on = o.flags == 0 && !(o.resid <= a.tol_switch);
     o.active = go_on ? 1 : 0;
-    o.steps = go_on ? a.steps_total : a.steps_short;
-    o.qbuf = go_on ? a.buf_total : a.buf_short;
-  } else if (a.flag_unconverged && !(o.resid <= 1e-3f) && o.flags == 0) {
-    o.flags |= 4;
+    o.steps = go_on ? a.steps_total[mi.sched] : a.steps_here;
+    o.qbuf = go_on ? a.buf_total[mi.sched] : a.buf_here;
+  } else {
+    if (a.flag_unconverged && !(o.resid <= 1e-3f) && o.flags == 0) o.flags |= 4;
+    o.active = 0;
   }
 }
 
@@ -1575,10 +1589,9 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st) 
   return hipGetLastError();
 }
 
-hipError_t launch_fro(const DevTables& t, int steps_total, int buf_total, int fixed_g, hipStream_t st) {
+hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
-  hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat,
-                     steps_total, buf_total, fixed_g);
+  hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat, a);
   return hipGetLastError();
 }
 
@@ -1667,9 +1680,9 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.split_cnt = t.split_cnt;
   g.part_norm = t.part_norm;
   g.norm_mode = mode == kGram ? p.norm_mode : -1;
-  g.ca = p.ca;
-  g.cb = p.cb;
-  g.cc = p.cc;
+  g.coef = t.coef;
+  g.step = p.step;
+  g.n_steps = t.n_steps;
   g.first = p.first;
   g.only_active = p.only_active;
   g.tasks = nullptr;

@@ -20,6 +20,13 @@ constexpr int kMaxWorkers = 128;
 // Most K slices of a split Gram product.
 constexpr int kMaxKSplit = 6;
 
+// Schedule classes of the polar iteration: tall matrices (m >= 2n), whose
+// smallest singular value stays well away from zero for noise-like spectra,
+// and the others (square-ish, where it does not).
+constexpr int kSchedClasses = 2;
+constexpr int kSchedSquare = 0;
+constexpr int kSchedTall = 1;
+
 // One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
 // element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
 // with (sr, sc) = (n, 1) if trans == 0 and (1, m) (column-major) if trans ==
@@ -41,6 +48,7 @@ struct MatInfo {
   int32_t tensor;    // index in the caller's layout
   int32_t chunk_begin, chunk_end;  // range of this matrix in the chunk table
   int32_t wide;      // 1 if the tensor is stored wide (rows < cols)
+  int32_t sched;     // schedule class (kSchedSquare or kSchedTall)
   int32_t norm_off;  // first of this matrix's gram_tiles(n) Gram-norm partials
   int32_t cnt_off;   // split-K Gram: first of its gram_tiles(n) arrival counters (-1 if not split)
 };

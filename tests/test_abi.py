@@ -58,7 +58,7 @@ def test_plan_rejects(layout, n, K, dtype, err):
 
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
                                   dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
-                                  dict(ell_fast=float("nan")), dict(orth=2), dict(scale=3), dict(momentum=-1),
+                                  dict(ell_fast=float("nan")), dict(ell_mid=(1.0, 0.0)), dict(ell_mid=(1e-4, float("nan"))), dict(ell_mid_tall=(1.0, 0.0)), dict(orth=2), dict(scale=3), dict(momentum=-1),
                                   dict(target=2), dict(orth=1), dict(orth=1, scale=0), dict(clip=3),
                                   dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1)])
 def test_plan_rejects_options(opts):
@@ -145,29 +145,44 @@ def test_two_phase_schedule(ell_fast):
     assert np.abs(_compose(sched[ns:], y) - 1).max() <= 1e-6
 
 
-def test_phases_converge_on_their_bounds():
-    """Default phases: [ell_fast, 1], then [sqrt(ell_fast ell0), 1], then
-    [ell0, 1]; a value that one phase converged stays converged through the
-    phases after it."""
+@pytest.mark.parametrize("tall,bounds", [(0, (1e-3, 2e-8, 1e-10)), (1, (1e-3, 1e-4, 2e-8, 1e-10))],
+                         ids=["square", "tall"])
+def test_phases_converge_on_their_bounds(tall, bounds):
+    """Default phases of each class: [ell_fast, 1], then its middle bounds,
+    then [ell0, 1]; a value that one phase converged stays converged through
+    the phases after it."""
     h = iso.isoloco_plan(LAY, 8256, 4)
-    sched = iso.isoloco_schedule(h)
-    ends = iso.isoloco_schedule_phases(h)
-    _, ns = iso.isoloco_schedule(h, with_split=True)
+    sched = iso.isoloco_schedule(h, tall=tall)
+    ends = iso.isoloco_schedule_phases(h, tall=tall)
+    _, ns = iso.isoloco_schedule(h, with_split=True, tall=tall)
     iso.isoloco_plan_destroy(h)
-    assert len(ends) == 3 and ends[0] == ns and ends[-1] == len(sched)
-    assert ends[0] < ends[1] < ends[2]
-    for e, bound in zip(ends, (1e-4, 1e-7, 1e-10)):
+    assert len(ends) == len(bounds) and ends[0] == ns and ends[-1] == len(sched)
+    assert all(a < b for a, b in zip(ends, ends[1:]))
+    for e, bound in zip(ends, bounds):
         x = np.geomspace(bound, 1.0, 100001)
         assert np.abs(_compose(sched[:e], x) - 1).max() <= 1e-6, (e, bound)
         y = _compose(sched[:e], np.linspace(0.5, 1.0, 1001))
         assert np.abs(_compose(sched[e:], y) - 1).max() <= 1e-6, e
 
 
-def test_phases_of_single_and_fixed_schedules():
-    for opts, n in ((dict(ell_fast=-1.0), 1), (dict(orth=1, scale=1), 1), (dict(max_steps=12), 2)):
+def test_class_schedule_argument_checked():
+    h = iso.isoloco_plan(LAY, 8256, 4)
+    with pytest.raises(iso.IsoLoCoError):
+        iso.isoloco_schedule(h, tall=2)
+    with pytest.raises(iso.IsoLoCoError):
+        iso.isoloco_schedule_phases(h, tall=-1)
+    iso.isoloco_plan_destroy(h)
+
+
+@pytest.mark.parametrize("tall", [0, 1], ids=["square", "tall"])
+def test_phases_of_single_and_fixed_schedules(tall):
+    key = "ell_mid_tall" if tall else "ell_mid"
+    for opts, n in ((dict(ell_fast=-1.0), 1), (dict(orth=1, scale=1), 1), (dict(max_steps=12), 2 + tall),
+                    ({key: (-1.0, -1.0)}, 2), ({key: (0.5, -1.0)}, 2), ({key: (1e-7, -1.0)}, 3),
+                    ({key: (1e-4, 1e-7)}, 4), ({key: (1e-7, 1e-4)}, 3)):
         h = iso.isoloco_plan(LAY, 8256, 4, 0, opts)
-        ends = iso.isoloco_schedule_phases(h)
-        S = len(iso.isoloco_schedule(h))
+        ends = iso.isoloco_schedule_phases(h, tall=tall)
+        S = len(iso.isoloco_schedule(h, tall=tall))
         iso.isoloco_plan_destroy(h)
         assert len(ends) == n and ends[-1] == S and ends == sorted(set(ends)), (opts, ends)
 

@@ -420,11 +420,11 @@ def test_two_phase_stops_well_conditioned_matrices_early(iso):
     cfg = _cfg(lay, n, K=4)
     dev = torch.device("cuda", 0)
     plan = iso.IsoLoCoPlan(lay, n, 4, iso.ISOLOCO_F32, device=dev)
-    ends = plan.schedule_phases()
+    ends, ends_tall = plan.schedule_phases(tall=0), plan.schedule_phases(tall=1)
     _, _, st = _run_and_compare(iso, cfg, seed=4, plan=plan)
-    print("steps", [s.steps for s in st[:2]], "phase ends", ends, flush=True)
+    print("steps", [s.steps for s in st[:2]], "phase ends", ends, ends_tall, flush=True)
     assert st[0].steps in ends[1:]
-    assert st[1].steps == ends[0]
+    assert st[1].steps == ends_tall[0]
     plan.close()
 
 
@@ -438,17 +438,21 @@ def _planted_tail(rows, cols, tiny, rng):
 
 
 def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
-    """Three phases (short schedule for [1e-4, 1], continuations for
-    [1e-7, 1] and [1e-10, 1], bounds on sigma / ||Delta^T Delta||_F^(1/2)):
-    a tall matrix with singular values in [1e-2, 1] stops after the first, a
-    square one in [1e-5, 1] after the second, and a square one whose smallest
-    singular value sits alone near 1.5e-8 (relative) runs all three; each
-    matches the oracle."""
+    """Per class (bounds on sigma / ||Delta^T Delta||_F^(1/2)): tall matrices
+    (m >= 2n) run phases for [1e-3, 1], [1e-4, 1], [2e-8, 1] and [1e-10, 1],
+    the others for [1e-3, 1], [2e-8, 1] and [1e-10, 1], all in the same
+    launches.  Tall matrices with singular values in [1e-2, 1], [3e-4, 1] and
+    [1e-5, 1] stop after the first, second and third of theirs; a square one
+    in [1e-5, 1] after its second, and a square one whose smallest singular
+    value sits alone near 5e-9 (relative) runs all three.  Each matches the
+    oracle."""
     from workload import custom_layout
-    lay, n = custom_layout([(192, 64, KIND_ISO), (256, 256, KIND_ISO), (256, 256, KIND_ISO)], align=4)
+    lay, n = custom_layout([(192, 64, KIND_ISO), (64, 192, KIND_ISO), (288, 96, KIND_ISO),
+                            (256, 256, KIND_ISO), (256, 256, KIND_ISO)], align=4)
     rng = np.random.default_rng(5)
     delta = np.zeros(n)
-    mats = (_planted(192, 64, 1e-2, rng), _planted(256, 256, 1e-5, rng), _planted_tail(256, 256, 3e-8, rng))
+    mats = (_planted(192, 64, 1e-2, rng), _planted(64, 192, 3e-4, rng), _planted(288, 96, 1e-5, rng),
+            _planted(256, 256, 1e-5, rng), _planted_tail(256, 256, 1e-8, rng))
     for (off, rows, cols, kind), m in zip(lay, mats):
         delta[off:off + rows * cols] = (m * 1e-3).reshape(-1)
     dev = torch.device("cuda", 0)
@@ -456,9 +460,9 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
     mom = torch.zeros_like(theta)
     w = torch.tensor(-delta, dtype=torch.float32, device=dev).reshape(1, n).contiguous()
     plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, device=dev)
-    ends = plan.schedule_phases()
-    assert len(ends) == 3
-    print("case: planted tails, phase ends", ends, flush=True)
+    ends, ends_tall = plan.schedule_phases(tall=0), plan.schedule_phases(tall=1)
+    assert len(ends) == 3 and len(ends_tall) == 4
+    print("case: planted spectra, phase ends", ends, ends_tall, flush=True)
     plan.aggregate(theta, w, mom, 1.0, 0.7, 0.9)
     torch.cuda.synchronize()
     st = plan.stats()
@@ -470,8 +474,9 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
         e = relF(th[off:off + rows * cols], th_r)
         print("tensor %d steps %d resid %.2e: theta %.2e" % (i, st[i].steps, st[i].orth_resid, e), flush=True)
         assert e <= TOL and st[i].flags == 0
+        assert 0 <= st[i].orth_resid <= TOL
         assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
-    assert [s.steps for s in st] == ends
+    assert [s.steps for s in st] == [ends_tall[0], ends_tall[1], ends_tall[2], ends[1], ends[2]]
     plan.close()
 
 
