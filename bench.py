@@ -175,6 +175,8 @@ def main():
     ap.add_argument("--ell-mid", type=float, nargs=2, default=[0.0, 0.0],
                     help="bounds of the middle phases of the polar schedule of matrices with m < 2n "
                          "(0: the library's default, negative: none)")
+    ap.add_argument("--streams", type=int, default=0, choices=[0, 1, 2],
+                    help="streams of the polar iteration (0: the library's default)")
     ap.add_argument("--ell-mid-tall", type=float, nargs=2, default=[0.0, 0.0],
                     help="the same for tall matrices (m >= 2n)")
     ap.add_argument("--ell-fast", type=float, default=0.0,
@@ -204,7 +206,8 @@ def main():
     vopts = {"exact": {}, "fast": dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS),
              "clip_high": dict(clip=iso.ISOLOCO_CLIP_HIGH), "clip_low": dict(clip=iso.ISOLOCO_CLIP_LOW)}[args.variant]
     plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, ell_mid=tuple(args.ell_mid),
-                                                                       ell_mid_tall=tuple(args.ell_mid_tall), **vopts),
+                                                                       ell_mid_tall=tuple(args.ell_mid_tall), streams=args.streams,
+                                                                       **vopts),
                            device=dev)
     phase_ends = {"square": plan.schedule_phases(tall=0), "tall": plan.schedule_phases(tall=1)}
     stream = torch.cuda.current_stream(dev)

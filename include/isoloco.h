@@ -31,8 +31,10 @@
  * stream and returns; buffers must stay valid until the stream passes that
  * point.  One plan must not be used by two streams at once; distinct plans
  * are independent.  The call issues kernel launches only (no host
- * synchronisation, memset or allocation), so it may be captured in a HIP
- * graph; every replay then repeats the step on the same buffers.
+ * synchronisation, memset or allocation; with two streams also an event
+ * record and wait to fork the plan's second stream off the caller's and
+ * one to join it back), so it may be captured in a HIP graph; every replay
+ * then repeats the step on the same buffers.
  *
  * Errors.  Every function returns an isoloco_status; no C++ exception crosses
  * this boundary.  A call that fails validation enqueues nothing.  The last
@@ -133,6 +135,12 @@ typedef struct {
                         value stays away from zero for noise-like spectra: defaults 1e-4
                         and 2e-8.  The two classes iterate in the same launches, each with
                         its own coefficients                                               */
+  int32_t streams;   /* 1: the polar iteration of every matrix on the caller's stream; 2: the
+                        tall matrices on the caller's stream and the others on a second
+                        stream of the plan's (forked after the reduction, joined before the
+                        scale), so that each fills the other's launch gaps and last waves;
+                        0 (default): 2 when the corrected matrices hold at most 2^28
+                        elements, else 1 (large products compete for the caches instead)  */
 } isoloco_options;
 
 #define ISOLOCO_PREC_MIXED 0

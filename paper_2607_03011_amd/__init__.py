@@ -62,7 +62,7 @@ class isoloco_options(ctypes.Structure):
                 ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float),
                 ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
                 ("target", ctypes.c_int32), ("clip", ctypes.c_int32), ("ell_mid", ctypes.c_float * 2),
-                ("ell_mid_tall", ctypes.c_float * 2)]
+                ("ell_mid_tall", ctypes.c_float * 2), ("streams", ctypes.c_int32)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):

@@ -64,6 +64,8 @@ constexpr double kCushion = 0.1;
 // (about 5x the rounding floor of the split-bf16 Gram; the polar factor is then
 // within about half this value of the exact one)
 constexpr float kSwitchTol = 5e-5f;
+// Default streams = 2 for plans whose corrected matrices hold at most this many elements.
+constexpr int64_t kTwoStreamMaxElems = (int64_t)1 << 28;
 // In the mixed precision mode the update products of the first kX6Steps steps
 // use bf16x5 (X in 3 bf16 parts, P' in 2), everything else bf16x3.  Those
 // early updates X' = X P' carry the large coefficients of the steps that
@@ -313,6 +315,7 @@ struct isoloco_plan_s {
   std::vector<Chunk> chunks;
   int n_iso_chunks = 0;
   TaskListHost gram_list, poly_list, update_list;
+  TaskListHost gram_cls[kSchedClasses], poly_cls[kSchedClasses], update_cls[kSchedClasses];
   int64_t n_norm = 0;  // Gram-norm partial slots (gram_tiles(n) per matrix)
   int64_t n_cnt = 0;   // split-K tile counters
   // Per schedule class (kSchedSquare, kSchedTall): the short schedule
@@ -327,6 +330,10 @@ struct isoloco_plan_s {
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
   size_t off_pnorm = 0, off_cnt = 0, off_coef = 0;
+  size_t off_gtc[kSchedClasses] = {}, off_ptc[kSchedClasses] = {}, off_utc[kSchedClasses] = {};
+  // the second stream of the per-class mode, with its fork and join events
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
   size_t off_poly = 0, off_gpart = 0, total = 0;
@@ -534,46 +541,54 @@ void plan_matrices(isoloco_plan_s* p) {
     else if (tk.tm % 2 == 0 && tk.tn % 2 == 0)
       big[split_layouts && M.trans ? 1 : 0].push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
   };
-  std::vector<int> order(p->mats.size());
-  for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
-    return (int64_t)p->mats[a].kchunk > (int64_t)p->mats[b].kchunk;
-  });
-  for (int mi : order) {
-    const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM;
-    // the Gram matrix is symmetric: tiles on and above the diagonal only
-    for (int ks = 0; ks < M.ksplit; ++ks) {
-      const int64_t kb = (int64_t)ks * M.kchunk, ke = std::min<int64_t>(M.m, kb + M.kchunk);
-      const bool kin = (ke - kb) % 32 == 0;
+  // The lists of every matrix (one stream), and of each schedule class alone
+  // (a stream per class).
+  auto build_lists = [&](int cls, TaskListHost& G, TaskListHost& P, TaskListHost& U) {
+    split_layouts = false;
+    std::vector<int> order;
+    for (size_t i = 0; i < p->mats.size(); ++i)
+      if (cls < 0 || p->mats[i].sched == cls) order.push_back((int)i);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+      return (int64_t)p->mats[a].kchunk > (int64_t)p->mats[b].kchunk;
+    });
+    for (int mi : order) {
+      const MatInfo& M = p->mats[mi];
+      const int T = (M.n + kBM - 1) / kBM;
+      // the Gram matrix is symmetric: tiles on and above the diagonal only
+      for (int ks = 0; ks < M.ksplit; ++ks) {
+        const int64_t kb = (int64_t)ks * M.kchunk, ke = std::min<int64_t>(M.m, kb + M.kchunk);
+        const bool kin = (ke - kb) % 32 == 0;
+        for (int a = 0; a < T; ++a)
+          for (int b = a; b < T; ++b)
+            put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, ks});
+      }
+    }
+    flush(G, true);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
+    for (int mi : order) {
+      const MatInfo& M = p->mats[mi];
+      const int T = (M.n + kBM - 1) / kBM;
+      const bool kin = M.n % 32 == 0;
       for (int a = 0; a < T; ++a)
         for (int b = a; b < T; ++b)
-          put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, ks});
+          put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, 0});
     }
-  }
-  flush(p->gram_list, true);
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
-  for (int mi : order) {
-    const MatInfo& M = p->mats[mi];
-    const int T = (M.n + kBM - 1) / kBM;
-    const bool kin = M.n % 32 == 0;
-    for (int a = 0; a < T; ++a)
-      for (int b = a; b < T; ++b)
-        put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, 0});
-  }
-  flush(p->poly_list, false);
-  split_layouts = true;
-  for (int mi : order) {
-    const MatInfo& M = p->mats[mi];
-    const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
-    const int TM2 = M.m / 256, TN2 = M.n / 256;
-    const bool kin = M.n % 32 == 0;
-    for (int a = 0; a < TM; ++a)
-      for (int b = 0; b < TN; ++b)
-        put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && kin,
-            fast_ok(M) && kin && a < 2 * TM2 && b < 2 * TN2, Task{mi, a, b, 0});
-  }
-  flush(p->update_list, false);
+    flush(P, false);
+    split_layouts = true;
+    for (int mi : order) {
+      const MatInfo& M = p->mats[mi];
+      const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
+      const int TM2 = M.m / 256, TN2 = M.n / 256;
+      const bool kin = M.n % 32 == 0;
+      for (int a = 0; a < TM; ++a)
+        for (int b = 0; b < TN; ++b)
+          put(M, (a + 1) * kBM <= M.m && (b + 1) * kBN <= M.n && kin,
+              fast_ok(M) && kin && a < 2 * TM2 && b < 2 * TN2, Task{mi, a, b, 0});
+    }
+    flush(U, false);
+  };
+  build_lists(-1, p->gram_list, p->poly_list, p->update_list);
+  for (int c = 0; c < kSchedClasses; ++c) build_lists(c, p->gram_cls[c], p->poly_cls[c], p->update_cls[c]);
 }
 
 void plan_workspace(isoloco_plan_s* p) {
@@ -588,6 +603,11 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_gt = take(p->gram_list.tasks.size() * sizeof(Task));
   p->off_pt = take(p->poly_list.tasks.size() * sizeof(Task));
   p->off_ut = take(p->update_list.tasks.size() * sizeof(Task));
+  for (int c = 0; c < kSchedClasses; ++c) {
+    p->off_gtc[c] = take(p->gram_cls[c].tasks.size() * sizeof(Task));
+    p->off_ptc[c] = take(p->poly_cls[c].tasks.size() * sizeof(Task));
+    p->off_utc[c] = take(p->update_cls[c].tasks.size() * sizeof(Task));
+  }
   p->off_sc = take(p->mats.size() * sizeof(MatScalars));
   p->off_psq = take(p->chunks.size() * sizeof(double));
   p->off_ptr = take(p->chunks.size() * sizeof(double));
@@ -606,29 +626,39 @@ void plan_workspace(isoloco_plan_s* p) {
   p->total = o;
 }
 
+TaskList dev_list(const isoloco_plan_s* p, const TaskListHost& L, size_t off) {
+  TaskList d{};
+  d.tasks = reinterpret_cast<const Task*>(p->ws + off);
+  for (int q = 0; q < 3; ++q) {
+    d.seg_off[q] = L.seg_off[q];
+    d.seg_cnt[q] = L.seg_cnt[q];
+    d.rem_off[q] = L.rem_off[q];
+    d.rem_cnt[q] = L.rem_cnt[q];
+  }
+  for (int q = 0; q < 2; ++q) {
+    d.big_off[q] = L.big_off[q];
+    d.big_cnt[q] = L.big_cnt[q];
+  }
+  return d;
+}
+
+// The tables with the task lists of one schedule class only.
+DevTables class_tables(const isoloco_plan_s* p, const DevTables& t, int c) {
+  DevTables d = t;
+  d.gram_list = dev_list(p, p->gram_cls[c], p->off_gtc[c]);
+  d.poly_list = dev_list(p, p->poly_cls[c], p->off_ptc[c]);
+  d.update_list = dev_list(p, p->update_cls[c], p->off_utc[c]);
+  return d;
+}
+
 DevTables dev_tables(const isoloco_plan_s* p) {
   DevTables t{};
   char* w = p->ws;
   t.mats = reinterpret_cast<const MatInfo*>(w + p->off_mats);
   t.chunks = reinterpret_cast<const Chunk*>(w + p->off_chunks);
-  auto list = [&](const TaskListHost& L, size_t off) {
-    TaskList d{};
-    d.tasks = reinterpret_cast<const Task*>(w + off);
-    for (int q = 0; q < 3; ++q) {
-      d.seg_off[q] = L.seg_off[q];
-      d.seg_cnt[q] = L.seg_cnt[q];
-      d.rem_off[q] = L.rem_off[q];
-      d.rem_cnt[q] = L.rem_cnt[q];
-    }
-    for (int q = 0; q < 2; ++q) {
-      d.big_off[q] = L.big_off[q];
-      d.big_cnt[q] = L.big_cnt[q];
-    }
-    return d;
-  };
-  t.gram_list = list(p->gram_list, p->off_gt);
-  t.poly_list = list(p->poly_list, p->off_pt);
-  t.update_list = list(p->update_list, p->off_ut);
+  t.gram_list = dev_list(p, p->gram_list, p->off_gt);
+  t.poly_list = dev_list(p, p->poly_list, p->off_pt);
+  t.update_list = dev_list(p, p->update_list, p->off_ut);
   t.scalars = reinterpret_cast<MatScalars*>(w + p->off_sc);
   t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
@@ -683,6 +713,8 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.ell_mid[1] == 0.f) o.ell_mid[1] = -1.f;
   if (o.ell_mid_tall[0] == 0.f) o.ell_mid_tall[0] = 1e-4f;
   if (o.ell_mid_tall[1] == 0.f) o.ell_mid_tall[1] = 2e-8f;
+  if (o.streams != 0 && o.streams != 1 && o.streams != 2)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "streams must be 0, 1 or 2");
   if (o.max_steps < 1 || o.max_steps > 200)
     return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
   if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
@@ -738,8 +770,17 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     p->n_elems = n_elems;
     p->K = K;
     p->dtype = worker_dtype;
-    p->opts = o;
     plan_matrices(p);
+    if (o.streams == 0) {
+      // Two streams fill each other's launch gaps and partial last waves,
+      // which matter while launches are short; for large matrices the
+      // concurrent products rather compete for the caches (same-box
+      // measurements: 109.5M parameters 2% faster, 341M 1%, 888M 4% slower).
+      int64_t n2d = 0;
+      for (const MatInfo& mi : p->mats) n2d += (int64_t)mi.m * mi.n;
+      o.streams = n2d <= kTwoStreamMaxElems ? 2 : 1;
+    }
+    p->opts = o;
     for (int c = 0; c < kSchedClasses; ++c)
       build_phases(o, c == kSchedTall ? o.ell_mid_tall : o.ell_mid, p->sched[c], p->phase_end[c]);
     p->n_steps = 0;
@@ -787,6 +828,14 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
       (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess ||
       (e = up(plan->off_coef, plan->coef.data(), plan->coef.size() * sizeof(float))) != hipSuccess)
     return hip_fail(e, "copying plan tables to the workspace");
+  for (int c = 0; c < kSchedClasses; ++c)
+    if ((e = up(plan->off_gtc[c], plan->gram_cls[c].tasks.data(), plan->gram_cls[c].tasks.size() * sizeof(Task))) !=
+            hipSuccess ||
+        (e = up(plan->off_ptc[c], plan->poly_cls[c].tasks.data(), plan->poly_cls[c].tasks.size() * sizeof(Task))) !=
+            hipSuccess ||
+        (e = up(plan->off_utc[c], plan->update_cls[c].tasks.data(),
+                plan->update_cls[c].tasks.size() * sizeof(Task))) != hipSuccess)
+    return hip_fail(e, "copying plan tables to the workspace");
   if (!plan->mats.empty()) {
     e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
     if (e != hipSuccess) return hip_fail(e, "clearing per-matrix scalars");
@@ -799,6 +848,13 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
   // done before any stream of the caller's (some may not wait for the null stream)
   e = hipStreamSynchronize(nullptr);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if (plan->opts.streams == 2 && !plan->side) {
+    // the second stream of the per-class mode (default priority)
+    if ((e = hipStreamCreateWithFlags(&plan->side, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&plan->ev_fork, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&plan->ev_join, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "creating the second stream");
+  }
   plan->ws = w;
   plan->ws_bytes = bytes;
   plan->device = dev;
@@ -857,47 +913,54 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   const bool ns5 = plan->opts.orth == ISOLOCO_ORTH_NS5;
 
   plan->ev_used = 0;
-  auto timed = [&](int phase, auto&& launch) -> hipError_t {
+  // (events on stream s around the launch when timing is on)
+  auto timed_on = [&](hipStream_t s, int phase, auto&& launch) -> hipError_t {
     if (!plan->timing) return launch();
     const size_t i = (size_t)plan->ev_used;
     if (2 * i + 1 >= plan->events.size()) return launch();
-    hipError_t r = hipEventRecord(plan->events[2 * i], st);
+    hipError_t r = hipEventRecord(plan->events[2 * i], s);
     if (r != hipSuccess) return r;
     if ((r = launch()) != hipSuccess) return r;
-    r = hipEventRecord(plan->events[2 * i + 1], st);
+    r = hipEventRecord(plan->events[2 * i + 1], s);
     plan->ev_phase[i] = phase;
     plan->ev_used++;
     return r;
   };
+  auto timed = [&](int phase, auto&& launch) -> hipError_t { return timed_on(st, phase, launch); };
   e = timed(kPhReduce, [&] { return launch_reduce(t, a, st); });
   if (e != hipSuccess) return hip_fail(e, "reduce launch");
   if (t.n_mat > 0) {
     const int S = plan->n_steps;
     FroArgs fa{};
     fa.fixed_g = ns5 ? 1 : 0;
+    int n_cls[kSchedClasses] = {};
+    for (const MatInfo& mi : plan->mats) n_cls[mi.sched]++;
     for (int c = 0; c < kSchedClasses; ++c) {
       fa.steps_total[c] = plan->phase_end[c].back();
       fa.buf_total[c] = (fa.steps_total[c] - 1) & 1;
     }
-    // what the end of step k (k + 1 steps done) means for class c: a switch
-    // (a phase but the last ends), the end of the class's schedule before the
-    // launch sequence's end, or nothing
-    auto action_after = [&](int c, int k, bool check) {
-      const std::vector<int>& ends = plan->phase_end[c];
-      if (k + 1 == ends.back()) return k + 1 < S ? (check ? kActFinal : kActStop) : kActNone;
-      for (size_t i = 0; i + 1 < ends.size(); ++i)
-        if (ends[i] == k + 1) return kActSwitch;
-      return kActNone;
-    };
+    // a stream per schedule class when asked for and both have matrices
+    const bool two = plan->opts.streams == 2 && plan->side && n_cls[0] > 0 && n_cls[1] > 0;
     const char* what = "";
-    // The polar iteration on the matrices in tt.delta (state in tt.scalars;
-    // the chunk partials of their squared norms in tt.part_sq); the factor of
-    // matrix m ends in tt.x[scalars[m].qbuf].
-    auto polar = [&](const DevTables& tt, bool check) -> hipError_t {
+    // The polar iteration of the matrices of class cls (-1: every matrix) on
+    // stream s, from the scalars fro_kernel set (tt.scalars; the matrices are
+    // in tt.delta); the factor of matrix m ends in tt.x[scalars[m].qbuf].
+    auto iterate = [&](const DevTables& tt, bool check, int cls, hipStream_t s) -> hipError_t {
       hipError_t r;
-      what = "fro launch";
-      if ((r = timed(kPhOther, [&] { return launch_fro(tt, fa, st); })) != hipSuccess) return r;
+      const int Sx = cls < 0 ? S : plan->phase_end[cls].back();
+      // what the end of step k (k + 1 steps done) means for class c: a switch
+      // (a phase but the last ends), the end of the class's schedule before
+      // the launch sequence's end, or nothing
+      auto action_after = [&](int c, int k) {
+        if (cls >= 0 && c != cls) return kActNone;
+        const std::vector<int>& ends = plan->phase_end[c];
+        if (k + 1 == ends.back()) return k + 1 < Sx ? (check ? kActFinal : kActStop) : kActNone;
+        for (size_t i = 0; i + 1 < ends.size(); ++i)
+          if (ends[i] == k + 1) return kActSwitch;
+        return kActNone;
+      };
       NormArgs na{};
+      na.cls = cls;
       na.flag_unconverged = ns5 ? 0 : 1;
       na.tol_switch = kSwitchTol;
       for (int c = 0; c < kSchedClasses; ++c) {
@@ -905,16 +968,16 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         na.buf_total[c] = fa.buf_total[c];
       }
       auto gram = [&](const PolarStep& ps) -> hipError_t {
-        return timed(kPhGram, [&] { return launch_gemm(tt, 0, ps, st); });
+        return timed_on(s, kPhGram, [&] { return launch_gemm(tt, 0, ps, s); });
       };
       auto norm = [&](int mode) -> hipError_t {
         na.mode = mode;
         na.only_active = 1;
-        return timed(kPhOther, [&] { return launch_gram_norm(tt, na, st); });
+        return timed_on(s, kPhOther, [&] { return launch_gram_norm(tt, na, s); });
       };
       const float* xin = tt.delta;
       bool have_gram = false;  // the Gram of xin was formed by the last phase end's check
-      for (int k = 0; k < S; ++k) {
+      for (int k = 0; k < Sx; ++k) {
         PolarStep ps{};
         ps.xin = xin;
         ps.xout = tt.x[k & 1];
@@ -930,14 +993,14 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         PolarStep pp = ps, pu = ps;
         pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
         pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
-        if ((r = timed(kPhPoly, [&] { return launch_gemm(tt, 1, pp, st); })) != hipSuccess ||
-            (r = timed(kPhUpdate, [&] { return launch_gemm(tt, 2, pu, st); })) != hipSuccess)
+        if ((r = timed_on(s, kPhPoly, [&] { return launch_gemm(tt, 1, pp, s); })) != hipSuccess ||
+            (r = timed_on(s, kPhUpdate, [&] { return launch_gemm(tt, 2, pu, s); })) != hipSuccess)
           return r;
         xin = ps.xout;
         have_gram = false;
         bool any = false, residual = false;
         for (int c = 0; c < kSchedClasses; ++c) {
-          na.action[c] = action_after(c, k, check);
+          na.action[c] = action_after(c, k);
           any = any || na.action[c] != kActNone;
           residual = residual || na.action[c] == kActSwitch || na.action[c] == kActFinal;
         }
@@ -962,17 +1025,36 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       if (check) {
         // the classes whose schedules run to the end of the sequence
         for (int c = 0; c < kSchedClasses; ++c)
-          na.action[c] = plan->phase_end[c].back() == S ? kActFinal : kActNone;
-        na.steps_here = S;
-        na.buf_here = (S - 1) & 1;
+          na.action[c] = (cls < 0 || c == cls) && plan->phase_end[c].back() == Sx ? kActFinal : kActNone;
+        na.steps_here = Sx;
+        na.buf_here = (Sx - 1) & 1;
         PolarStep pc{};
         pc.xin = xin;
         pc.only_active = 1;
-        pc.arith = step_arith(plan->opts.precision, S, kProdGram);
+        pc.arith = step_arith(plan->opts.precision, Sx, kProdGram);
         pc.norm_mode = kNormPhase;
         what = "check launch";
         if ((r = gram(pc)) != hipSuccess || (r = norm(kNormPhase)) != hipSuccess) return r;
       }
+      return hipSuccess;
+    };
+    auto polar = [&](const DevTables& tt, bool check) -> hipError_t {
+      hipError_t r;
+      what = "fro launch";
+      if ((r = timed(kPhOther, [&] { return launch_fro(tt, fa, st); })) != hipSuccess) return r;
+      if (!two) return iterate(tt, check, -1, st);
+      // fork: the second stream waits for the scalars; join before the scale
+      what = "stream fork";
+      if ((r = hipEventRecord(plan->ev_fork, st)) != hipSuccess ||
+          (r = hipStreamWaitEvent(plan->side, plan->ev_fork, 0)) != hipSuccess)
+        return r;
+      if ((r = iterate(class_tables(plan, tt, kSchedTall), check, kSchedTall, st)) != hipSuccess ||
+          (r = iterate(class_tables(plan, tt, kSchedSquare), check, kSchedSquare, plan->side)) != hipSuccess)
+        return r;
+      what = "stream join";
+      if ((r = hipEventRecord(plan->ev_join, plan->side)) != hipSuccess ||
+          (r = hipStreamWaitEvent(st, plan->ev_join, 0)) != hipSuccess)
+        return r;
       return hipSuccess;
     };
     if ((e = polar(t, plan->opts.check == 1)) != hipSuccess) return hip_fail(e, what);
@@ -1118,8 +1200,12 @@ isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out) {
 }
 
 isoloco_status isoloco_plan_destroy(isoloco_plan_t plan) {
-  if (plan)
+  if (plan) {
     for (hipEvent_t ev : plan->events) (void)hipEventDestroy(ev);
+    if (plan->ev_fork) (void)hipEventDestroy(plan->ev_fork);
+    if (plan->ev_join) (void)hipEventDestroy(plan->ev_join);
+    if (plan->side) (void)hipStreamDestroy(plan->side);
+  }
   delete plan;
   return ISOLOCO_OK;
 }

@@ -92,6 +92,7 @@ enum NormAction {
 struct NormArgs {
   int mode;
   int only_active;
+  int cls;  // -1: every matrix; else only the matrices of this schedule class
   int action[kSchedClasses];
   int steps_here, buf_here;  // steps done at this phase end, X buffer holding their result
   int steps_total[kSchedClasses], buf_total[kSchedClasses];  // per class: schedule length, its buffer

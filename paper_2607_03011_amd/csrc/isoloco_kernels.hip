@@ -1367,6 +1367,7 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
   MatScalars& o = sc[m];
   if (a.only_active && !o.active) return;
   const MatInfo mi = mats[m];
+  if (a.cls >= 0 && mi.sched != a.cls) return;
   const int act = a.mode == kNormFirst ? kActNone : a.action[mi.sched];
   if (a.mode != kNormFirst && act == kActNone) return;
   if (act == kActStop) {

@@ -58,7 +58,7 @@ def test_plan_rejects(layout, n, K, dtype, err):
 
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
                                   dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
-                                  dict(ell_fast=float("nan")), dict(ell_mid=(1.0, 0.0)), dict(ell_mid=(1e-4, float("nan"))), dict(ell_mid_tall=(1.0, 0.0)), dict(orth=2), dict(scale=3), dict(momentum=-1),
+                                  dict(ell_fast=float("nan")), dict(ell_mid=(1.0, 0.0)), dict(ell_mid=(1e-4, float("nan"))), dict(ell_mid_tall=(1.0, 0.0)), dict(streams=3), dict(orth=2), dict(scale=3), dict(momentum=-1),
                                   dict(target=2), dict(orth=1), dict(orth=1, scale=0), dict(clip=3),
                                   dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1)])
 def test_plan_rejects_options(opts):

@@ -519,20 +519,51 @@ def test_single_phase_schedule(iso, precision):
     _run_and_compare(iso, _cfg(lay, n, K=3), seed=9, opts=dict(ell_fast=-1.0, precision=precision))
 
 
+# Both schedule classes, tall ones with split K
+TWO_CLASSES = [(300, 200, KIND_ISO), (5000, 160, KIND_ISO), (192, 800, KIND_ISO), (256, 256, KIND_ISO),
+               (129, 1, KIND_AVG), (640, 96, KIND_ISO)]
+
+
 @pytest.mark.parametrize("variant", [None, {"clip": "high"}], ids=["exact", "clip_high"])
-def test_graph_capture_replays(iso, variant):
-    """The step only enqueues kernels on the caller's stream (no host sync, no
-    memset, no allocation), so it can be captured in a HIP graph: every replay,
-    with eager steps and synchronisations in between, must equal the eager
-    result bit for bit."""
+def test_two_streams(iso, variant):
+    """streams = 2 runs the tall matrices and the others on two streams: the
+    same results as one stream, bit for bit, and the oracle's."""
     from workload import ReplicaGenerator, custom_layout
-    lay, n = custom_layout(RAGGED + [(520, 130, KIND_ISO)], align=4)
+    lay, n = custom_layout(TWO_CLASSES, align=4)
+    cfg = _cfg(lay, n, K=3)
+    dev = torch.device("cuda", 0)
+    opts = variant_opts(variant) if variant else {}
+    _run_and_compare(iso, cfg, seed=14, opts=dict(opts, streams=2), variant=variant)
+    gen = ReplicaGenerator(cfg, seed=15, device=dev)
+    theta0, _ = gen.init_state()
+    workers = gen.workers(theta0, 1)
+    out = []
+    for streams in (1, 2):
+        plan = iso.IsoLoCoPlan(lay, n, 3, iso.ISOLOCO_F32, opts=dict(opts, streams=streams), device=dev)
+        t, m = theta0.clone(), torch.zeros_like(theta0)
+        plan.aggregate(t, workers, m, 1.0, 0.7, 0.9)
+        torch.cuda.synchronize()
+        out.append((t, m, [(s.steps, s.flags) for s in plan.stats()]))
+        plan.close()
+    assert torch.equal(out[0][0], out[1][0]) and torch.equal(out[0][1], out[1][1])
+    assert out[0][2] == out[1][2]
+
+
+@pytest.mark.parametrize("streams", [1, 2])
+@pytest.mark.parametrize("variant", [None, {"clip": "high"}], ids=["exact", "clip_high"])
+def test_graph_capture_replays(iso, variant, streams):
+    """The step only enqueues kernels (no host sync, no memset, no allocation;
+    with streams = 2 also a fork to the plan's second stream and a join), so
+    it can be captured in a HIP graph: every replay, with eager steps and
+    synchronisations in between, must equal the eager result bit for bit."""
+    from workload import ReplicaGenerator, custom_layout
+    lay, n = custom_layout(RAGGED + [(520, 130, KIND_ISO), (5000, 160, KIND_ISO)], align=4)
     cfg = _cfg(lay, n, K=3)
     dev = torch.device("cuda", 0)
     gen = ReplicaGenerator(cfg, seed=12, device=dev)
     theta0, _ = gen.init_state()
     workers = gen.workers(theta0, 1)
-    opts = variant_opts(variant) if variant else None
+    opts = dict(variant_opts(variant) if variant else {}, streams=streams)
     plan = iso.IsoLoCoPlan(lay, n, 3, iso.ISOLOCO_F32, opts=opts, device=dev)
 
     def eager():
