@@ -243,8 +243,12 @@ typedef struct {
   float poly_ms;    /* batched polynomial products b A + c A^2, all steps          */
   float update_ms;  /* batched updates X <- a X + X P, all steps                   */
   float finish_ms;  /* fused Nesterov write-back of the corrected tensors          */
-  float other_ms;   /* norms, split-K sums, trace and sigma_bar                    */
+  float other_ms;   /* norms, trace and sigma_bar                                  */
   int32_t gram_launches, poly_launches, update_launches, launches;
+  float products_busy_ms; /* union of the Gram, polynomial and update launches' intervals:
+                        the time some product runs (with two streams the launches overlap,
+                        and each per-phase sum above counts every launch's own duration) */
+  int32_t streams;  /* streams the polar iteration used (1 or 2)                      */
 } isoloco_timing;
 
 /* enable = 1 turns per-launch event timing on for later aggregates, 0 off. */

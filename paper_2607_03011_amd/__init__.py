@@ -76,7 +76,8 @@ class isoloco_timing(ctypes.Structure):
                 ("poly_ms", ctypes.c_float), ("update_ms", ctypes.c_float), ("finish_ms", ctypes.c_float),
                 ("other_ms", ctypes.c_float), ("gram_launches", ctypes.c_int32),
                 ("poly_launches", ctypes.c_int32), ("update_launches", ctypes.c_int32),
-                ("launches", ctypes.c_int32)]
+                ("launches", ctypes.c_int32), ("products_busy_ms", ctypes.c_float),
+                ("streams", ctypes.c_int32)]
 
 
 # torch brings its own copy of the HIP runtime (same SONAME as ROCm's).  Load it

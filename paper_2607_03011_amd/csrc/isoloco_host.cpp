@@ -334,6 +334,7 @@ struct isoloco_plan_s {
   // the second stream of the per-class mode, with its fork and join events
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  int last_streams = 1;  // streams the last aggregate's polar iteration used
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
   size_t off_poly = 0, off_gpart = 0, total = 0;
@@ -941,6 +942,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     }
     // a stream per schedule class when asked for and both have matrices
     const bool two = plan->opts.streams == 2 && plan->side && n_cls[0] > 0 && n_cls[1] > 0;
+    plan->last_streams = two ? 2 : 1;
     const char* what = "";
     // The polar iteration of the matrices of class cls (-1: every matrix) on
     // stream s, from the scalars fro_kernel set (tt.scalars; the matrices are
@@ -1183,9 +1185,17 @@ isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out) {
   if ((e = hipEventElapsedTime(&ms, plan->events[0], plan->events[2 * n - 1])) != hipSuccess)
     return hip_fail(e, "hipEventElapsedTime");
   out->total_ms = ms;
+  std::vector<std::pair<float, float>> prod;  // product launch intervals from the first event
   for (int i = 0; i < n; ++i) {
     if ((e = hipEventElapsedTime(&ms, plan->events[2 * i], plan->events[2 * i + 1])) != hipSuccess)
       return hip_fail(e, "hipEventElapsedTime");
+    const int ph = plan->ev_phase[i];
+    if (ph == kPhGram || ph == kPhPoly || ph == kPhUpdate) {
+      float t0 = 0.f;
+      if ((e = hipEventElapsedTime(&t0, plan->events[0], plan->events[2 * i])) != hipSuccess)
+        return hip_fail(e, "hipEventElapsedTime");
+      prod.emplace_back(t0, t0 + ms);
+    }
     out->launches++;
     switch (plan->ev_phase[i]) {
       case kPhReduce: out->reduce_ms += ms; break;
@@ -1196,6 +1206,20 @@ isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out) {
       default: out->other_ms += ms; break;
     }
   }
+  std::sort(prod.begin(), prod.end());
+  float busy = 0.f, lo = 0.f, hi = -1.f;
+  for (const auto& iv : prod) {
+    if (iv.first > hi) {
+      if (hi > lo) busy += hi - lo;
+      lo = iv.first;
+      hi = iv.second;
+    } else {
+      hi = std::max(hi, iv.second);
+    }
+  }
+  if (hi > lo) busy += hi - lo;
+  out->products_busy_ms = busy;
+  out->streams = plan->last_streams;
   return ISOLOCO_OK;
 }
 

@@ -550,6 +550,33 @@ def test_two_streams(iso, variant):
 
 
 @pytest.mark.parametrize("streams", [1, 2])
+def test_timing_products_busy(iso, streams):
+    """Per-launch timing: the products' busy time (the union of their launch
+    intervals) equals the sum of their durations on one stream and is at most
+    that sum on two, where launches overlap."""
+    from workload import ReplicaGenerator, custom_layout
+    lay, n = custom_layout(TWO_CLASSES, align=4)
+    cfg = _cfg(lay, n, K=3)
+    dev = torch.device("cuda", 0)
+    gen = ReplicaGenerator(cfg, seed=16, device=dev)
+    theta, mom = gen.init_state()
+    workers = gen.workers(theta, 1)
+    plan = iso.IsoLoCoPlan(lay, n, 3, iso.ISOLOCO_F32, opts=dict(streams=streams), device=dev)
+    plan.enable_timing(True)
+    plan.aggregate(theta, workers, mom, 1.0, 0.7, 0.9)
+    tm = plan.timing()
+    plan.close()
+    total = tm.gram_ms + tm.poly_ms + tm.update_ms
+    print("streams %d: busy %.3f ms, launch sum %.3f ms, total %.3f ms" %
+          (tm.streams, tm.products_busy_ms, total, tm.total_ms), flush=True)
+    assert tm.streams == streams
+    assert 0 < tm.products_busy_ms <= total * (1 + 1e-5) + 1e-3
+    assert tm.products_busy_ms <= tm.total_ms
+    if streams == 1:
+        assert tm.products_busy_ms >= total * (1 - 1e-5) - 1e-3
+
+
+@pytest.mark.parametrize("streams", [1, 2])
 @pytest.mark.parametrize("variant", [None, {"clip": "high"}], ids=["exact", "clip_high"])
 def test_graph_capture_replays(iso, variant, streams):
     """The step only enqueues kernels (no host sync, no memset, no allocation;
