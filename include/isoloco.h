@@ -127,7 +127,7 @@ typedef struct {
                         second polar iteration runs on Delta - sigma_bar Q                 */
   float ell_mid[2];  /* bounds of the middle phases (see ell_fast), each followed by the same
                         test, for matrices with m < 2n (m x n in tall coordinates, m >= n);
-                        ell_mid[0] defaults to 2e-8, ell_mid[1] to none.  A negative bound,
+                        defaults 3e-7 and 2e-8.  A negative bound,
                         or one not strictly between the bounds before and ell0, is left out
                         (with both left out, the continuation after the short schedule
                         reaches [ell0, 1])                                                 */

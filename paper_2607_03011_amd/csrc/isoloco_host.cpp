@@ -710,8 +710,8 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.tol == 0.f) o.tol = 1e-6f;
   if (o.check == 0) o.check = 1;
   if (o.ell_fast == 0.f) o.ell_fast = 1e-3f;
-  if (o.ell_mid[0] == 0.f) o.ell_mid[0] = 2e-8f;
-  if (o.ell_mid[1] == 0.f) o.ell_mid[1] = -1.f;
+  if (o.ell_mid[0] == 0.f) o.ell_mid[0] = 3e-7f;
+  if (o.ell_mid[1] == 0.f) o.ell_mid[1] = 2e-8f;
   if (o.ell_mid_tall[0] == 0.f) o.ell_mid_tall[0] = 1e-4f;
   if (o.ell_mid_tall[1] == 0.f) o.ell_mid_tall[1] = 2e-8f;
   if (o.streams != 0 && o.streams != 1 && o.streams != 2)

@@ -145,7 +145,7 @@ def test_two_phase_schedule(ell_fast):
     assert np.abs(_compose(sched[ns:], y) - 1).max() <= 1e-6
 
 
-@pytest.mark.parametrize("tall,bounds", [(0, (1e-3, 2e-8, 1e-10)), (1, (1e-3, 1e-4, 2e-8, 1e-10))],
+@pytest.mark.parametrize("tall,bounds", [(0, (1e-3, 3e-7, 2e-8, 1e-10)), (1, (1e-3, 1e-4, 2e-8, 1e-10))],
                          ids=["square", "tall"])
 def test_phases_converge_on_their_bounds(tall, bounds):
     """Default phases of each class: [ell_fast, 1], then its middle bounds,
