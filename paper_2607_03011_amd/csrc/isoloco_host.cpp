@@ -316,6 +316,7 @@ struct isoloco_plan_s {
   int n_iso_chunks = 0;
   TaskListHost gram_list, poly_list, update_list;
   TaskListHost gram_cls[kSchedClasses], poly_cls[kSchedClasses], update_cls[kSchedClasses];
+  std::vector<int> chunk_cls[kSchedClasses];  // the corrected chunks of each schedule class
   int64_t n_norm = 0;  // Gram-norm partial slots (gram_tiles(n) per matrix)
   int64_t n_cnt = 0;   // split-K tile counters
   // Per schedule class (kSchedSquare, kSchedTall): the short schedule
@@ -331,6 +332,7 @@ struct isoloco_plan_s {
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
   size_t off_pnorm = 0, off_cnt = 0, off_coef = 0;
   size_t off_gtc[kSchedClasses] = {}, off_ptc[kSchedClasses] = {}, off_utc[kSchedClasses] = {};
+  size_t off_cic[kSchedClasses] = {};
   // the second stream of the per-class mode, with its fork and join events
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
@@ -481,6 +483,7 @@ void plan_matrices(isoloco_plan_s* p) {
     sq += ((int64_t)mi.n * mi.n + 63) / 64 * 64;
   }
   p->n_iso_chunks = (int)p->chunks.size();
+  for (int i = 0; i < p->n_iso_chunks; ++i) p->chunk_cls[p->mats[p->chunks[i].mat].sched].push_back(i);
   for (size_t t = 0; t < p->layout.size(); ++t) {
     const isoloco_tensor& T = p->layout[t];
     if (T.kind == ISOLOCO_KIND_ISO) continue;
@@ -608,6 +611,7 @@ void plan_workspace(isoloco_plan_s* p) {
     p->off_gtc[c] = take(p->gram_cls[c].tasks.size() * sizeof(Task));
     p->off_ptc[c] = take(p->poly_cls[c].tasks.size() * sizeof(Task));
     p->off_utc[c] = take(p->update_cls[c].tasks.size() * sizeof(Task));
+    p->off_cic[c] = take(p->chunk_cls[c].size() * sizeof(int));
   }
   p->off_sc = take(p->mats.size() * sizeof(MatScalars));
   p->off_psq = take(p->chunks.size() * sizeof(double));
@@ -649,6 +653,9 @@ DevTables class_tables(const isoloco_plan_s* p, const DevTables& t, int c) {
   d.gram_list = dev_list(p, p->gram_cls[c], p->off_gtc[c]);
   d.poly_list = dev_list(p, p->poly_cls[c], p->off_ptc[c]);
   d.update_list = dev_list(p, p->update_cls[c], p->off_utc[c]);
+  d.chunk_idx = reinterpret_cast<const int*>(p->ws + p->off_cic[c]);
+  d.n_chunk_idx = (int)p->chunk_cls[c].size();
+  d.cls = c;
   return d;
 }
 
@@ -666,6 +673,9 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.part_norm = reinterpret_cast<double*>(w + p->off_pnorm);
   t.split_cnt = reinterpret_cast<int*>(w + p->off_cnt);
   t.coef = reinterpret_cast<const float*>(w + p->off_coef);
+  t.chunk_idx = nullptr;
+  t.n_chunk_idx = 0;
+  t.cls = -1;
   t.n_steps = p->n_steps;
   t.delta = reinterpret_cast<float*>(w + p->off_delta);
   t.x[0] = reinterpret_cast<float*>(w + p->off_x0);
@@ -835,7 +845,9 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
         (e = up(plan->off_ptc[c], plan->poly_cls[c].tasks.data(), plan->poly_cls[c].tasks.size() * sizeof(Task))) !=
             hipSuccess ||
         (e = up(plan->off_utc[c], plan->update_cls[c].tasks.data(),
-                plan->update_cls[c].tasks.size() * sizeof(Task))) != hipSuccess)
+                plan->update_cls[c].tasks.size() * sizeof(Task))) != hipSuccess ||
+        (e = up(plan->off_cic[c], plan->chunk_cls[c].data(), plan->chunk_cls[c].size() * sizeof(int))) !=
+            hipSuccess)
     return hip_fail(e, "copying plan tables to the workspace");
   if (!plan->mats.empty()) {
     e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
@@ -1040,18 +1052,36 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       }
       return hipSuccess;
     };
-    auto polar = [&](const DevTables& tt, bool check) -> hipError_t {
+    // the scale and the write-back of the matrices in tt (after their polar
+    // iteration) on stream s
+    auto tail = [&](const DevTables& tt, hipStream_t s) -> hipError_t {
+      hipError_t r;
+      what = "scale launch";
+      if ((r = timed_on(s, kPhOther, [&] { return launch_scale(tt, a, s); })) != hipSuccess) return r;
+      what = "finish launch";
+      return timed_on(s, kPhFinish, [&] { return launch_finish(tt, a, s); });
+    };
+    // The polar iteration of every matrix of tt; with two streams each class
+    // on its own, and then (with_tail) each class's scale and write-back on
+    // its stream before the join.
+    auto polar = [&](const DevTables& tt, bool check, bool with_tail) -> hipError_t {
       hipError_t r;
       what = "fro launch";
       if ((r = timed(kPhOther, [&] { return launch_fro(tt, fa, st); })) != hipSuccess) return r;
-      if (!two) return iterate(tt, check, -1, st);
-      // fork: the second stream waits for the scalars; join before the scale
+      if (!two) {
+        if ((r = iterate(tt, check, -1, st)) != hipSuccess) return r;
+        return with_tail ? tail(tt, st) : hipSuccess;
+      }
+      // fork: the second stream waits for the scalars; join at the end
       what = "stream fork";
       if ((r = hipEventRecord(plan->ev_fork, st)) != hipSuccess ||
           (r = hipStreamWaitEvent(plan->side, plan->ev_fork, 0)) != hipSuccess)
         return r;
-      if ((r = iterate(class_tables(plan, tt, kSchedTall), check, kSchedTall, st)) != hipSuccess ||
-          (r = iterate(class_tables(plan, tt, kSchedSquare), check, kSchedSquare, plan->side)) != hipSuccess)
+      const DevTables tt_tall = class_tables(plan, tt, kSchedTall), tt_sq = class_tables(plan, tt, kSchedSquare);
+      if ((r = iterate(tt_tall, check, kSchedTall, st)) != hipSuccess ||
+          (with_tail && (r = tail(tt_tall, st)) != hipSuccess) ||
+          (r = iterate(tt_sq, check, kSchedSquare, plan->side)) != hipSuccess ||
+          (with_tail && (r = tail(tt_sq, plan->side)) != hipSuccess))
         return r;
       what = "stream join";
       if ((r = hipEventRecord(plan->ev_join, plan->side)) != hipSuccess ||
@@ -1059,18 +1089,24 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         return r;
       return hipSuccess;
     };
-    if ((e = polar(t, plan->opts.check == 1)) != hipSuccess) return hip_fail(e, what);
+    if (!a.clip) {
+      if ((e = polar(t, plan->opts.check == 1, true)) != hipSuccess) return hip_fail(e, what);
+      plan->last_stream = st;
+      plan->has_run = true;
+      return ISOLOCO_OK;
+    }
+    if ((e = polar(t, plan->opts.check == 1, false)) != hipSuccess) return hip_fail(e, what);
     if ((e = timed(kPhOther, [&] { return launch_scale(t, a, st); })) != hipSuccess)
       return hip_fail(e, "scale launch");
-    if (a.clip) {
-      // E = Delta - sigma_bar Q, its polar factor Q2 (a second iteration), then
+    {
+      // clip variants: E = Delta - sigma_bar Q, its polar factor Q2 (a second iteration), then
       // |E| = Q (Q2^T E): the correction U diag(min or max(sigma, sigma_bar)) V^T
       // is (E -+ |E|) / 2 + sigma_bar Q
       DevTables t2 = t;
       t2.scalars = t.scalars2;
       if ((e = timed(kPhOther, [&] { return launch_clip_prep(t, st); })) != hipSuccess)
         return hip_fail(e, "clip launch");
-      if ((e = polar(t2, false)) != hipSuccess) return hip_fail(e, what);
+      if ((e = polar(t2, false, false)) != hipSuccess) return hip_fail(e, what);
       PolarStep pc{};
       pc.xin = t.x[0];
       pc.xin_alt = t.x[1];
@@ -1179,12 +1215,16 @@ isoloco_status isoloco_get_timing(isoloco_plan_t plan, isoloco_timing* out) {
   *out = isoloco_timing{};
   if (!plan->timing || plan->ev_used == 0) return ISOLOCO_OK;
   const int n = plan->ev_used;
-  hipError_t e = hipEventSynchronize(plan->events[2 * n - 1]);
-  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  hipError_t e;
   float ms = 0;
-  if ((e = hipEventElapsedTime(&ms, plan->events[0], plan->events[2 * n - 1])) != hipSuccess)
-    return hip_fail(e, "hipEventElapsedTime");
-  out->total_ms = ms;
+  // launches on two streams may end in either order: the total runs to the
+  // latest end
+  for (int i = 0; i < n; ++i) {
+    if ((e = hipEventSynchronize(plan->events[2 * i + 1])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    if ((e = hipEventElapsedTime(&ms, plan->events[0], plan->events[2 * i + 1])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    out->total_ms = std::max(out->total_ms, ms);
+  }
   std::vector<std::pair<float, float>> prod;  // product launch intervals from the first event
   for (int i = 0; i < n; ++i) {
     if ((e = hipEventElapsedTime(&ms, plan->events[2 * i], plan->events[2 * i + 1])) != hipSuccess)

@@ -42,6 +42,12 @@ struct DevTables {
   float* gpart;
   const float* coef;  // polynomial coefficients [class][n_steps][3] (schedule classes of MatInfo::sched)
   int n_steps;
+  // the scale and write-back launches cover the corrected chunks listed here
+  // (the chunks of one schedule class) and the matrices of class cls; every
+  // corrected chunk and matrix when chunk_idx is null and cls is -1
+  const int* chunk_idx;
+  int n_chunk_idx;
+  int cls;
   int n_mat, n_chunks, n_iso_chunks;
 };
 

@@ -297,21 +297,23 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
   }
 }
 
-// Sum of a matrix's chunk partials by one wavefront: lane l adds partials
-// l, l + 64, ... in order, then a fixed butterfly (deterministic).
-__device__ __forceinline__ double wave_sum_range(const double* part, int begin, int end) {
+// Sum of a matrix's chunk partials by a 256-thread block: thread t adds
+// partials t, t + 256, ... in order, then block_sum256 (deterministic).
+// Result valid in thread 0.
+__device__ __forceinline__ double block_sum_range(const double* part, int begin, int end, double* lds4) {
   double s = 0.0;
-  for (int c = begin + (int)(threadIdx.x & 63); c < end; c += 64) s += part[c];
-  return wave_sum(s);
+  for (int c = begin + (int)threadIdx.x; c < end; c += 256) s += part[c];
+  return block_sum256(s, lds4);
 }
 
-// ||Delta||_F per matrix (one wavefront per matrix).
-__global__ void __launch_bounds__(64)
+// ||Delta||_F per matrix (one block per matrix).
+__global__ void __launch_bounds__(256)
 fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
            MatScalars* __restrict__ sc, int n_mat, FroArgs a) {
+  __shared__ double red[4];
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
-  const double s = wave_sum_range(part_sq, mi.chunk_begin, mi.chunk_end);
+  const double s = block_sum_range(part_sq, mi.chunk_begin, mi.chunk_end, red);
   if (threadIdx.x != 0) return;
   MatScalars o;
   o.fro = (float)sqrt(s);
@@ -1398,10 +1400,12 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
 // workspace layout: chunk_ws maps the chunk's elements; groups of 4 are
 // contiguous when c.vec).
 __global__ void __launch_bounds__(kStreamThreads)
-trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc, const float* __restrict__ x0,
-             const float* __restrict__ x1, const float* __restrict__ delta, double* __restrict__ part_tr) {
+trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatScalars* __restrict__ sc,
+             const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ delta,
+             double* __restrict__ part_tr) {
   __shared__ double red[4];
-  const Chunk c = chunks[blockIdx.x];
+  const int ci = idx ? idx[blockIdx.x] : (int)blockIdx.x;
+  const Chunk c = chunks[ci];
   const float* q = sc[c.mat].qbuf ? x1 : x0;
   double s = 0.0;
   int done = 0;
@@ -1420,18 +1424,20 @@ trace_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc
     s += (double)q[o] * delta[o];
   }
   s = block_sum256(s, red);
-  if (threadIdx.x == 0) part_tr[blockIdx.x] = s;
+  if (threadIdx.x == 0) part_tr[ci] = s;
 }
 
 // The scale of each correction.  mode 0: <Q, Delta>_F / r, the mean singular
 // value (from the trace partials); 1: ||Delta||_F / sqrt(r), their RMS;
 // 2: sqrt(rows / cols) of the tensor as stored (Muon's sqrt(fan_out / fan_in)).
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(256)
 sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
-             MatScalars* __restrict__ sc, int n_mat, int mode) {
+             MatScalars* __restrict__ sc, int n_mat, int mode, int cls) {
+  __shared__ double red[4];
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
-  const double s = mode == 0 ? wave_sum_range(part_tr, mi.chunk_begin, mi.chunk_end) : 0.0;
+  if (cls >= 0 && mi.sched != cls) return;
+  const double s = mode == 0 ? block_sum_range(part_tr, mi.chunk_begin, mi.chunk_end, red) : 0.0;
   if (threadIdx.x != 0) return;
   MatScalars& o = sc[m];
   if (o.flags & 1) o.sigma_bar = __builtin_nanf("");
@@ -1478,12 +1484,12 @@ __device__ __forceinline__ void finish_quad(float* __restrict__ theta, float* __
 // and f = alpha sigma_bar (clip variants: P is their correction, already
 // scaled, and f = 1).  A tile chunk reads its column-major P through LDS.
 __global__ void __launch_bounds__(kStreamThreads)
-finish_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict__ sc,
+finish_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatScalars* __restrict__ sc,
               const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ dclip,
               float* __restrict__ theta, float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball,
               int target_update, int clip) {
   __shared__ TileLds tl;
-  const Chunk c = chunks[blockIdx.x];
+  const Chunk c = chunks[idx ? idx[blockIdx.x] : blockIdx.x];
   const MatScalars s = sc[c.mat];
   const float* q = clip ? dclip : (s.qbuf ? x1 : x0);
   float f = clip ? 1.f : alpha * s.sigma_bar;
@@ -1592,7 +1598,7 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st) 
 
 hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st) {
   if (t.n_mat == 0) return hipSuccess;
-  hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat, a);
+  hipLaunchKernelGGL(fro_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.part_sq, t.scalars, t.n_mat, a);
   return hipGetLastError();
 }
 
@@ -1701,18 +1707,20 @@ hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t s
 }
 
 hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
-  if (t.n_iso_chunks == 0) return hipSuccess;
+  const int n = t.chunk_idx ? t.n_chunk_idx : t.n_iso_chunks;
+  if (n == 0) return hipSuccess;
   if (a.scale == 0)
-    hipLaunchKernelGGL(trace_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+    hipLaunchKernelGGL(trace_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.scalars,
                        t.x[0], t.x[1], t.delta, t.part_tr);
-  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(64), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat,
-                     a.scale);
+  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat,
+                     a.scale, t.cls);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) {
-  if (t.n_iso_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(finish_kernel, dim3(t.n_iso_chunks), dim3(kStreamThreads), 0, st, t.chunks, t.scalars,
+  const int n = t.chunk_idx ? t.n_chunk_idx : t.n_iso_chunks;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(finish_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.scalars,
                      t.x[0], t.x[1], t.delta, a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update,
                      a.clip);
   return hipGetLastError();
