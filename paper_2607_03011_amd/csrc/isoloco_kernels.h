@@ -7,11 +7,14 @@
 namespace isoloco {
 
 // A task list of 128 x 128 tiles in segments: interior tiles (segment 0, both
-// storage orders; the kernel picks the loaders per task; segment 1 is empty)
-// and tiles that touch a ragged edge (segment 2, bounds-checked kernel).  The
-// same array also holds the cover used by the bf16x3 steps: interior
-// 256 x 256 tiles (big segment 0; 1 is empty) plus, in segments as above, the
-// 128 x 128 tiles they leave uncovered.
+// storage orders, the kernel picking the loaders per task; in the update
+// lists the column-major ones go to segment 1 instead) and tiles that touch a
+// ragged edge (segment 2, bounds-checked kernel).  In
+// the update lists the same array also holds the cover the split-bf16
+// kernels use: interior 256 x 256 tiles (big segments 0 and 1, split by
+// storage order like the 128 x 128 ones) plus, in segments as above, the
+// 128 x 128 tiles they leave uncovered; the Gram and polynomial lists have no
+// 256 x 256 tiles (rem = seg).
 struct TaskList {
   const Task* tasks;
   int seg_off[3];

@@ -94,7 +94,7 @@ struct MatScalars {
   float resid;      // ||Q^T Q - I||_F / sqrt(n), or -1 if not computed
   int32_t flags;    // ISOLOCO_FLAG_* bits
   int32_t steps;    // polar steps this matrix has taken
-  int32_t active;   // 1 while the matrix still iterates (second phase of the schedule)
+  int32_t active;   // 1 while the matrix still iterates (cleared when a phase end stops it)
   int32_t qbuf;     // which X buffer holds the final polar factor
 };
 
