@@ -861,8 +861,17 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
   // done before any stream of the caller's (some may not wait for the null stream)
   e = hipStreamSynchronize(nullptr);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if (plan->side && plan->device != dev) {
+    // the workspace moved to another device: the second stream goes with it
+    (void)hipEventDestroy(plan->ev_fork);
+    (void)hipEventDestroy(plan->ev_join);
+    (void)hipStreamDestroy(plan->side);
+    plan->side = nullptr;
+    plan->ev_fork = plan->ev_join = nullptr;
+  }
   if (plan->opts.streams == 2 && !plan->side) {
-    // the second stream of the per-class mode (default priority)
+    // the second stream of the per-class mode (default priority), on the
+    // workspace's device
     if ((e = hipStreamCreateWithFlags(&plan->side, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&plan->ev_fork, hipEventDisableTiming)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&plan->ev_join, hipEventDisableTiming)) != hipSuccess)
