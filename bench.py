@@ -79,9 +79,9 @@ def gemm_bytes_per_step(layout, stats):
 # device copy; summaries in profiles/) for the default workload and precision.  It is
 # reported only while the kernel and planner sources are the ones it was measured on.
 MEASURED_TRAFFIC = {
-    "sources_sha256": "e8c453601b1ebbab9c1af732101fe96145761549433654dd096a8e1ed6763efd",
+    "sources_sha256": "a258c1ef048c9b66a2be64789069d166922e94178c7038ec073a7d37d14b3d4c",
     "workload": 2, "precision": "mixed",
-    "gemm_bytes_per_step": 26.56e9, "reduce_bytes_per_launch": 7.892e9, "finish_bytes_per_launch": 2.195e9,
+    "gemm_bytes_per_step": 25.69e9, "reduce_bytes_per_launch": 7.892e9, "finish_bytes_per_launch": 2.195e9,
 }
 
 
@@ -172,15 +172,13 @@ def main():
                     help="exact: Algorithm 2 (converged polar factor, mean singular value); fast: "
                          "Section 4.3 (five Newton-Schulz steps, RMS of the singular values); clip_high / "
                          "clip_low: Section 4.5 (only the singular values above / below the mean set to it)")
-    ap.add_argument("--ell-mid", type=float, nargs=2, default=[0.0, 0.0],
-                    help="bounds of the middle phases of the polar schedule of matrices with m < 2n "
-                         "(0: the library's default, negative: none)")
     ap.add_argument("--streams", type=int, default=0, choices=[0, 1, 2],
                     help="streams of the polar iteration (0: the library's default)")
-    ap.add_argument("--ell-mid-tall", type=float, nargs=2, default=[0.0, 0.0],
-                    help="the same for tall matrices (m >= 2n)")
-    ap.add_argument("--ell-fast", type=float, default=0.0,
-                    help="short-schedule bound (0: library default; negative: one phase)")
+    ap.add_argument("--phase-tall", type=float, nargs=3, default=[0.0, 0.0, 0.0],
+                    help="phase bounds of the polar schedule of tall matrices, m >= 2n (0: the library's "
+                         "default, negative: end of the list; a negative first bound: one phase)")
+    ap.add_argument("--phase-square", type=float, nargs=3, default=[0.0, 0.0, 0.0],
+                    help="the same for the other matrices")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build measures one GPU; the IsoLoCo step here runs unsharded on a "
@@ -205,9 +203,9 @@ def main():
             "bf16x6": iso.ISOLOCO_PREC_BF16X6, "fp32": iso.ISOLOCO_PREC_FP32}[args.precision]
     vopts = {"exact": {}, "fast": dict(orth=iso.ISOLOCO_ORTH_NS5, scale=iso.ISOLOCO_SCALE_RMS),
              "clip_high": dict(clip=iso.ISOLOCO_CLIP_HIGH), "clip_low": dict(clip=iso.ISOLOCO_CLIP_LOW)}[args.variant]
-    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, ell_fast=args.ell_fast, ell_mid=tuple(args.ell_mid),
-                                                                       ell_mid_tall=tuple(args.ell_mid_tall), streams=args.streams,
-                                                                       **vopts),
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, phase_tall=tuple(args.phase_tall),
+                                                                       phase_square=tuple(args.phase_square),
+                                                                       streams=args.streams, **vopts),
                            device=dev)
     phase_ends = {"square": plan.schedule_phases(tall=0), "tall": plan.schedule_phases(tall=1)}
     stream = torch.cuda.current_stream(dev)

@@ -97,16 +97,11 @@ typedef struct {
                         MIXED (default): the update products X P of the first 3 steps
                         in bf16x5 (X in 3 parts, P in 2: 5 products, about the accuracy
                         of bf16x6 for this product), bf16x3 for every other product      */
-  float ell_fast;    /* the iteration first runs the short schedule for [ell_fast, 1]; a matrix
-                        whose Q^T Q is then the identity to 5e-5 stops there; the others run
-                        a continuation that reaches [ell_mid, 1], the same test, and a last
-                        one that reaches [ell0, 1] (default 1e-3; a negative value runs the
-                        single schedule for [ell0, 1])                                         */
   /* Variants of the step that the paper studies (all 0: Algorithm 2). */
   int32_t orth;      /* ISOLOCO_ORTH_POLAR: Q = U V^T, the converged polar factor (Algorithm 2);
                         ISOLOCO_ORTH_NS5: the fast variant's five Newton-Schulz steps of the
                         Muon quintic (3.4445, -4.7750, 2.0315) on Delta / ||Delta||_F
-                        (Section 4.3); ell0, tol, ell_fast do not apply, and the residual
+                        (Section 4.3); ell0, tol and the phases do not apply, and the residual
                         of check is reported without the not-converged flag                */
   int32_t scale;     /* ISOLOCO_SCALE_MEAN: sigma_bar = <Q, Delta>_F / r, the mean singular
                         value (Algorithm 2; needs ORTH_POLAR); ISOLOCO_SCALE_RMS:
@@ -125,16 +120,20 @@ typedef struct {
                         above / below the mean to the mean, keeping U, V and the other
                         singular values (Section 4.5).  Needs ORTH_POLAR and SCALE_MEAN; a
                         second polar iteration runs on Delta - sigma_bar Q                 */
-  float ell_mid[2];  /* bounds of the middle phases (see ell_fast), each followed by the same
-                        test, for matrices with m < 2n (m x n in tall coordinates, m >= n);
-                        defaults 3e-7 and 2e-8.  A negative bound,
-                        or one not strictly between the bounds before and ell0, is left out
-                        (with both left out, the continuation after the short schedule
-                        reaches [ell0, 1])                                                 */
-  float ell_mid_tall[2]; /* the same for tall matrices (m >= 2n), whose smallest singular
-                        value stays away from zero for noise-like spectra: defaults 1e-4
-                        and 2e-8.  The two classes iterate in the same launches, each with
-                        its own coefficients                                               */
+  float phase_tall[3];   /* Phases of the polar iteration of tall matrices (m >= 2n in tall
+                        coordinates, m x n with m >= n): bounds b0 > b1 > b2 on
+                        sigma_min / ||Delta^T Delta||_F^(1/2).  The iteration first runs the
+                        schedule for [b0, 1]; a matrix whose Q^T Q is then the identity to
+                        5e-5 stops there, the others continue with the schedule that takes
+                        what the steps so far made of b1 to 1, the same test, and so on,
+                        until a last phase reaches [ell0, 1].  0 selects the default of a
+                        slot (1e-3, 1e-4, 2e-8); a negative entry ends the list; an entry
+                        not strictly between the one before and ell0 is left out.  A
+                        negative b0 runs the single schedule for [ell0, 1].  The smallest
+                        singular value of a tall noise-like matrix stays away from zero   */
+  float phase_square[3]; /* the same for the other matrices (square-ish, m < 2n), whose
+                        smallest singular value does not: defaults 3e-7, 2e-8, none.  Both
+                        classes iterate in the same launches, each with its coefficients */
   int32_t streams;   /* 1: the polar iteration of every matrix on the caller's stream; 2: the
                         tall matrices on the caller's stream and the others on a second
                         stream of the plan's (forked after the reduction, joined before the
@@ -224,8 +223,8 @@ isoloco_status isoloco_schedule(isoloco_plan_t plan, int32_t tall, double* coeff
 
 /* The phases of one class's schedule (tall as above): ends[i] is the number of
  * steps done when phase i ends (increasing; the last equals the schedule
- * length).  Phase 0 is the short schedule for [ell_fast, 1]; each later phase
- * continues it for a smaller bound (the class's middle bounds, then ell0).
+ * length).  Phase 0 is the schedule for the class's first bound; each later
+ * phase continues it for a smaller bound (the class's next bounds, then ell0).
  * After every phase but the last, the matrices whose Q^T Q is the identity to
  * the switch tolerance stop.  Both classes iterate in the same launches; a
  * class whose schedule is shorter stops at its end.  Writes at most max_phases

@@ -59,10 +59,10 @@ class isoloco_tensor(ctypes.Structure):
 
 class isoloco_options(ctypes.Structure):
     _fields_ = [("max_steps", ctypes.c_int32), ("ell0", ctypes.c_float), ("tol", ctypes.c_float),
-                ("check", ctypes.c_int32), ("precision", ctypes.c_int32), ("ell_fast", ctypes.c_float),
+                ("check", ctypes.c_int32), ("precision", ctypes.c_int32),
                 ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
-                ("target", ctypes.c_int32), ("clip", ctypes.c_int32), ("ell_mid", ctypes.c_float * 2),
-                ("ell_mid_tall", ctypes.c_float * 2), ("streams", ctypes.c_int32)]
+                ("target", ctypes.c_int32), ("clip", ctypes.c_int32), ("phase_tall", ctypes.c_float * 3),
+                ("phase_square", ctypes.c_float * 3), ("streams", ctypes.c_int32)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):

@@ -354,13 +354,13 @@ struct isoloco_plan_s {
 
 namespace {
 
-// Phases of one schedule class: a short schedule that assumes sigma_min >=
-// ell_fast, then continuations for smaller bounds, the middle bounds that lie
-// strictly between the bounds before them and ell0, and ell0.  After every
+// Phases of one schedule class: a schedule that assumes sigma_min >= the
+// class's first bound, then continuations for its smaller bounds (those that
+// lie strictly between the bound before and ell0) and ell0.  After every
 // phase but the last, each matrix whose Q^T Q is already the identity stops;
 // the others run the next phase, built for what the phases so far made of its
-// bound.
-void build_phases(const isoloco_options& o, const float (&mid)[2], std::vector<double>& sched,
+// bound.  A negative first bound: the single schedule for [ell0, 1].
+void build_phases(const isoloco_options& o, const float (&bound)[3], std::vector<double>& sched,
                   std::vector<int>& ends) {
   sched.clear();
   ends.clear();
@@ -368,15 +368,15 @@ void build_phases(const isoloco_options& o, const float (&mid)[2], std::vector<d
     // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
     // quintic (Section 4.3; the paper's own coefficients are not printed)
     for (int k = 0; k < kNs5Steps; ++k) sched.insert(sched.end(), kNs5Coeffs, kNs5Coeffs + 3);
-  } else if (o.ell_fast > o.ell0) {
-    sched = build_schedule(o.ell_fast, o.tol, o.max_steps);
+  } else if (bound[0] > o.ell0) {
+    sched = build_schedule(bound[0], o.tol, o.max_steps);
     ends.push_back((int)sched.size() / 3);
     std::vector<double> bounds;
-    double above = o.ell_fast;
-    for (float b : mid)
-      if (b > o.ell0 && b < above) {
-        bounds.push_back(b);
-        above = b;
+    double above = bound[0];
+    for (int i = 1; i < 3 && bound[i] >= 0.f; ++i)
+      if (bound[i] > o.ell0 && bound[i] < above) {
+        bounds.push_back(bound[i]);
+        above = bound[i];
       }
     bounds.push_back(o.ell0);
     for (double b : bounds) {
@@ -719,22 +719,21 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   if (o.ell0 == 0.f) o.ell0 = 1e-10f;
   if (o.tol == 0.f) o.tol = 1e-6f;
   if (o.check == 0) o.check = 1;
-  if (o.ell_fast == 0.f) o.ell_fast = 1e-3f;
-  if (o.ell_mid[0] == 0.f) o.ell_mid[0] = 3e-7f;
-  if (o.ell_mid[1] == 0.f) o.ell_mid[1] = 2e-8f;
-  if (o.ell_mid_tall[0] == 0.f) o.ell_mid_tall[0] = 1e-4f;
-  if (o.ell_mid_tall[1] == 0.f) o.ell_mid_tall[1] = 2e-8f;
+  const float def_tall[3] = {1e-3f, 1e-4f, 2e-8f}, def_square[3] = {3e-7f, 2e-8f, -1.f};
+  for (int i = 0; i < 3; ++i) {
+    if (o.phase_tall[i] == 0.f) o.phase_tall[i] = def_tall[i];
+    if (o.phase_square[i] == 0.f) o.phase_square[i] = def_square[i];
+  }
   if (o.streams != 0 && o.streams != 1 && o.streams != 2)
     return fail(ISOLOCO_ERR_INVALID_ARG, "streams must be 0, 1 or 2");
   if (o.max_steps < 1 || o.max_steps > 200)
     return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
   if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
   if (!(o.tol > 0.f && o.tol < 0.5f)) return fail(ISOLOCO_ERR_INVALID_ARG, "tol must be in (0, 0.5)");
-  if (!(o.ell_fast < 1.f) || std::isnan(o.ell_fast))
-    return fail(ISOLOCO_ERR_INVALID_ARG, "ell_fast must be < 1 (negative: one phase)");
-  for (float b : {o.ell_mid[0], o.ell_mid[1], o.ell_mid_tall[0], o.ell_mid_tall[1]})
-    if (!(b < 1.f) || std::isnan(b))
-      return fail(ISOLOCO_ERR_INVALID_ARG, "ell_mid bounds must be < 1 (negative: none)");
+  for (int i = 0; i < 3; ++i)
+    for (float b : {o.phase_tall[i], o.phase_square[i]})
+      if (!(b < 1.f) || std::isnan(b))
+        return fail(ISOLOCO_ERR_INVALID_ARG, "phase bounds must be < 1 (negative: end of the list)");
   if (o.check != 1 && o.check != -1) return fail(ISOLOCO_ERR_INVALID_ARG, "check must be 1 or -1");
   if (o.precision < ISOLOCO_PREC_MIXED || o.precision > ISOLOCO_PREC_BF16X6)
     return fail(ISOLOCO_ERR_INVALID_ARG, "unknown precision %d", o.precision);
@@ -793,7 +792,7 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     }
     p->opts = o;
     for (int c = 0; c < kSchedClasses; ++c)
-      build_phases(o, c == kSchedTall ? o.ell_mid_tall : o.ell_mid, p->sched[c], p->phase_end[c]);
+      build_phases(o, c == kSchedTall ? o.phase_tall : o.phase_square, p->sched[c], p->phase_end[c]);
     p->n_steps = 0;
     for (int c = 0; c < kSchedClasses; ++c) p->n_steps = std::max(p->n_steps, p->phase_end[c].back());
     p->coef.assign((size_t)kSchedClasses * p->n_steps * 3, 0.f);

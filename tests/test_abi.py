@@ -57,8 +57,10 @@ def test_plan_rejects(layout, n, K, dtype, err):
 
 
 @pytest.mark.parametrize("opts", [dict(max_steps=-1), dict(max_steps=500), dict(ell0=1.5), dict(ell0=-1e-3),
-                                  dict(tol=0.7), dict(check=3), dict(precision=5), dict(ell_fast=1.0),
-                                  dict(ell_fast=float("nan")), dict(ell_mid=(1.0, 0.0)), dict(ell_mid=(1e-4, float("nan"))), dict(ell_mid_tall=(1.0, 0.0)), dict(streams=3), dict(orth=2), dict(scale=3), dict(momentum=-1),
+                                  dict(tol=0.7), dict(check=3), dict(precision=5), dict(phase_tall=(1.0, 0, 0)),
+                                  dict(phase_tall=(float("nan"), 0, 0)), dict(phase_square=(1e-4, 1.0, 0)),
+                                  dict(phase_square=(1e-4, 1e-5, float("nan"))), dict(streams=3), dict(orth=2),
+                                  dict(scale=3), dict(momentum=-1),
                                   dict(target=2), dict(orth=1), dict(orth=1, scale=0), dict(clip=3),
                                   dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1)])
 def test_plan_rejects_options(opts):
@@ -128,14 +130,14 @@ def test_schedule_converges_on_interval(ell0, tol):
         assert abs(c) > 1e-6 * (abs(a) + abs(b))
 
 
-@pytest.mark.parametrize("ell_fast", [1e-4, 1e-2])
-def test_two_phase_schedule(ell_fast):
-    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell_fast=ell_fast))
+@pytest.mark.parametrize("first", [1e-4, 1e-2])
+def test_two_phase_schedule(first):
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(phase_square=(first, -1.0, 0.0)))
     sched, ns = iso.isoloco_schedule(h, with_split=True)
     iso.isoloco_plan_destroy(h)
     assert 0 < ns < len(sched)
-    # the short phase alone converges on [ell_fast, 1] ...
-    x = np.geomspace(ell_fast, 1.0, 100001)
+    # the short phase alone converges on [first, 1] ...
+    x = np.geomspace(first, 1.0, 100001)
     assert np.abs(_compose(sched[:ns], x) - 1).max() <= 1e-6
     # ... and the whole schedule on [ell0, 1]
     x = np.geomspace(1e-10, 1.0, 100001)
@@ -145,12 +147,12 @@ def test_two_phase_schedule(ell_fast):
     assert np.abs(_compose(sched[ns:], y) - 1).max() <= 1e-6
 
 
-@pytest.mark.parametrize("tall,bounds", [(0, (1e-3, 3e-7, 2e-8, 1e-10)), (1, (1e-3, 1e-4, 2e-8, 1e-10))],
+@pytest.mark.parametrize("tall,bounds", [(0, (3e-7, 2e-8, 1e-10)), (1, (1e-3, 1e-4, 2e-8, 1e-10))],
                          ids=["square", "tall"])
 def test_phases_converge_on_their_bounds(tall, bounds):
-    """Default phases of each class: [ell_fast, 1], then its middle bounds,
-    then [ell0, 1]; a value that one phase converged stays converged through
-    the phases after it."""
+    """Default phases of each class: [b0, 1], then its next bounds, then
+    [ell0, 1]; a value that one phase converged stays converged through the
+    phases after it."""
     h = iso.isoloco_plan(LAY, 8256, 4)
     sched = iso.isoloco_schedule(h, tall=tall)
     ends = iso.isoloco_schedule_phases(h, tall=tall)
@@ -176,10 +178,11 @@ def test_class_schedule_argument_checked():
 
 @pytest.mark.parametrize("tall", [0, 1], ids=["square", "tall"])
 def test_phases_of_single_and_fixed_schedules(tall):
-    key = "ell_mid_tall" if tall else "ell_mid"
-    for opts, n in ((dict(ell_fast=-1.0), 1), (dict(orth=1, scale=1), 1), (dict(max_steps=12), 2 + tall),
-                    ({key: (-1.0, -1.0)}, 2), ({key: (0.5, -1.0)}, 2), ({key: (1e-7, -1.0)}, 3),
-                    ({key: (1e-4, 1e-7)}, 4), ({key: (1e-7, 1e-4)}, 3)):
+    key = "phase_tall" if tall else "phase_square"
+    n_default = 4 if tall else 3
+    for opts, n in (({key: (-1.0, 0, 0)}, 1), (dict(orth=1, scale=1), 1), (dict(max_steps=12), 3 if tall else 1),
+                    ({key: (1e-3, -1.0, 0)}, 2), ({key: (1e-3, 0.5, -1.0)}, 2), ({key: (1e-3, 1e-7, -1.0)}, 3),
+                    ({key: (1e-3, 1e-4, 1e-7)}, 4), ({key: (1e-3, 1e-7, 1e-4)}, 3), ({}, n_default)):
         h = iso.isoloco_plan(LAY, 8256, 4, 0, opts)
         ends = iso.isoloco_schedule_phases(h, tall=tall)
         S = len(iso.isoloco_schedule(h, tall=tall))
@@ -187,11 +190,12 @@ def test_phases_of_single_and_fixed_schedules(tall):
         assert len(ends) == n and ends[-1] == S and ends == sorted(set(ends)), (opts, ends)
 
 
-def test_one_phase_when_ell_fast_negative():
-    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(ell_fast=-1.0))
-    sched, ns = iso.isoloco_schedule(h, with_split=True)
+def test_one_phase_when_first_bound_negative():
+    h = iso.isoloco_plan(LAY, 8256, 4, 0, dict(phase_tall=(-1.0, 0, 0), phase_square=(-1.0, 0, 0)))
+    for tall in (0, 1):
+        sched, ns = iso.isoloco_schedule(h, with_split=True, tall=tall)
+        assert ns == len(sched)
     iso.isoloco_plan_destroy(h)
-    assert ns == len(sched)
 
 
 def test_schedule_tolerates_overshoot_and_shrinks_small_values_never():

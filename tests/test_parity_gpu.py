@@ -423,7 +423,7 @@ def test_two_phase_stops_well_conditioned_matrices_early(iso):
     ends, ends_tall = plan.schedule_phases(tall=0), plan.schedule_phases(tall=1)
     _, _, st = _run_and_compare(iso, cfg, seed=4, plan=plan)
     print("steps", [s.steps for s in st[:2]], "phase ends", ends, ends_tall, flush=True)
-    assert st[0].steps in ends[1:]
+    assert st[0].steps in ends
     assert st[1].steps == ends_tall[0]
     plan.close()
 
@@ -440,11 +440,11 @@ def _planted_tail(rows, cols, tiny, rng):
 def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
     """Per class (bounds on sigma / ||Delta^T Delta||_F^(1/2)): tall matrices
     (m >= 2n) run phases for [1e-3, 1], [1e-4, 1], [2e-8, 1] and [1e-10, 1],
-    the others for [1e-3, 1], [3e-7, 1], [2e-8, 1] and [1e-10, 1], all in the
-    same launches.  Tall matrices with singular values in [1e-2, 1], [3e-4, 1]
+    the others for [3e-7, 1], [2e-8, 1] and [1e-10, 1], all in the same
+    launches.  Tall matrices with singular values in [1e-2, 1], [3e-4, 1]
     and [1e-5, 1] stop after the first, second and third of theirs; a square
-    one in [1e-5, 1] after its second, and a square one whose smallest
-    singular value sits alone near 5e-9 (relative) runs all four.  Each
+    one in [1e-5, 1] after its first, and a square one whose smallest
+    singular value sits alone near 5e-9 (relative) runs all three.  Each
     matches the oracle."""
     from workload import custom_layout
     lay, n = custom_layout([(192, 64, KIND_ISO), (64, 192, KIND_ISO), (288, 96, KIND_ISO),
@@ -461,7 +461,7 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
     w = torch.tensor(-delta, dtype=torch.float32, device=dev).reshape(1, n).contiguous()
     plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, device=dev)
     ends, ends_tall = plan.schedule_phases(tall=0), plan.schedule_phases(tall=1)
-    assert len(ends) == 4 and len(ends_tall) == 4
+    assert len(ends) == 3 and len(ends_tall) == 4
     print("case: planted spectra, phase ends", ends, ends_tall, flush=True)
     plan.aggregate(theta, w, mom, 1.0, 0.7, 0.9)
     torch.cuda.synchronize()
@@ -476,7 +476,7 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
         assert e <= TOL and st[i].flags == 0
         assert 0 <= st[i].orth_resid <= TOL
         assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
-    assert [s.steps for s in st] == [ends_tall[0], ends_tall[1], ends_tall[2], ends[1], ends[3]]
+    assert [s.steps for s in st] == [ends_tall[0], ends_tall[1], ends_tall[2], ends[0], ends[2]]
     plan.close()
 
 
@@ -516,7 +516,8 @@ def test_wide_geometric_spectrum(iso, precision):
 def test_single_phase_schedule(iso, precision):
     from workload import custom_layout
     lay, n = custom_layout(RAGGED, align=4)
-    _run_and_compare(iso, _cfg(lay, n, K=3), seed=9, opts=dict(ell_fast=-1.0, precision=precision))
+    _run_and_compare(iso, _cfg(lay, n, K=3), seed=9,
+                     opts=dict(phase_tall=(-1.0, 0, 0), phase_square=(-1.0, 0, 0), precision=precision))
 
 
 # Both schedule classes, tall ones with split K
