@@ -6,7 +6,7 @@ the C ABI, on the 109.5M-parameter LLaMA-style workload (12 blocks d = 768,
 FFN 2048, tied 32000 x 768 embedding) with K = 16 float32 replicas resident in
 HBM.  Prints one JSON line.
 
-    python bench.py [--steps 20] [--warmup 3] [--workload 2] [--no-cpu-baseline]
+    python bench.py [--steps 20] [--warmup 3] [--workload NAME] [--no-cpu-baseline]
 """
 import argparse
 import glob
@@ -80,8 +80,8 @@ def gemm_bytes_per_step(layout, stats):
 # reported only while the kernel and planner sources are the ones it was measured on.
 MEASURED_TRAFFIC = {
     "sources_sha256": "a258c1ef048c9b66a2be64789069d166922e94178c7038ec073a7d37d14b3d4c",
-    "workload": 2, "precision": "mixed",
-    "gemm_bytes_per_step": 25.69e9, "reduce_bytes_per_launch": 7.892e9, "finish_bytes_per_launch": 2.195e9,
+    "workload": "llama-12L-d768-V32000-K16", "precision": "mixed",
+    "gemm_bytes_per_step": 25.69e9, "reduce_bytes_per_launch": 7.892e9, "finish_bytes_per_step": 2.195e9,
 }
 
 
@@ -160,7 +160,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--workload", default="llama-12L-d768-V32000-K16",
+                    help="a workload name from workload.WORKLOADS")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
@@ -188,11 +189,13 @@ def main():
     import torch
 
     import paper_2607_03011_amd as iso
-    from workload import CONFIGS, ReplicaGenerator
+    from workload import WORKLOADS, ReplicaGenerator
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    cfg = CONFIGS[args.workload]
+    if args.workload not in WORKLOADS:
+        sys.exit("bench.py: unknown workload %r; known: %s" % (args.workload, ", ".join(WORKLOADS)))
+    cfg = WORKLOADS[args.workload]
     gen = ReplicaGenerator(cfg, seed=args.seed, device=dev)
     theta, mom = gen.init_state()
     workers = gen.workers(theta, step=1)
@@ -326,8 +329,10 @@ def main():
                             "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4)},
         "roofline_finish": {"bound": "hbm", "kernel": "finish_kernel", "achieved": round(fin_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(fin_gbs / PEAK_HBM_GBS, 4),
-                            "traffic": mt["finish_bytes_per_launch"] if measured else None,
-                            "bytes_per_launch": fbytes, "ms": round(per["finish_ms"], 4)},
+                            "traffic": mt["finish_bytes_per_step"] if measured else None,
+                            "bytes_per_step": fbytes, "ms": round(per["finish_ms"], 4),
+                            "note": "one launch per matrix class (two with both classes present); "
+                                    "bytes and ms are summed over a step's launches"},
         "phases_ms": {k: round(v, 4) for k, v in per.items()},
         "library_ms_p10_p50_p90": [round(float(x), 4) for x in np.percentile(step_ms, [10, 50, 90])],
         "input_restore_ms": round(restore_ms, 4),

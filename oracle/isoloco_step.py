@@ -10,7 +10,7 @@ Follows Algorithm 2 (IsoLoCo) of the paper in its own order:
 3. Nesterov momentum: B <- mu B + D;  P <- D + mu B;  theta <- theta - eta P,
    with B = 0 before the first step.
 
-Readings where the paper is ambiguous (each one is listed in the design doc):
+Readings where the paper is ambiguous:
 
 * sign of the pseudo-gradient: Algorithm 1 defines the averaged
   pseudo-gradient as the mean of (theta_global - theta_k), and Algorithm 2

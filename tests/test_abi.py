@@ -218,9 +218,9 @@ def test_schedule_length_default():
 
 
 def test_big_layout_plans_quickly():
-    from workload import CONFIGS
-    for k in (2, 3, 4):
-        c = CONFIGS[k]
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    for name in (LLAMA_110M, LLAMA_341M, LLAMA_888M):
+        c = WORKLOADS[name]
         h = iso.isoloco_plan(c.layout, c.n_elems, c.K, 0 if c.worker_dtype == "f32" else 1)
         ws = iso.isoloco_workspace_size(h)
         n2d = sum(r * cc for (_, r, cc, kind) in c.layout if kind == 0)

@@ -212,14 +212,14 @@ def test_variants_two_steps(iso, name, variant):
 
 @pytest.mark.parametrize("clip", ["high", "low"])
 def test_clip_full_block(iso, clip):
-    from workload import CONFIGS
-    _run_and_compare(iso, CONFIGS[1], variant={"clip": clip})
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    _run_and_compare(iso, WORKLOADS[BLOCK], variant={"clip": clip})
 
 
 @pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
 def test_fast_variant_full_block(iso, precision):
-    from workload import CONFIGS
-    _run_and_compare(iso, CONFIGS[1], opts=dict(precision=precision), variant={"orth": "ns5", "scale": "rms"})
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    _run_and_compare(iso, WORKLOADS[BLOCK], opts=dict(precision=precision), variant={"orth": "ns5", "scale": "rms"})
 
 
 def test_ragged_multi_tile_bf16(iso):
@@ -344,14 +344,14 @@ def test_alpha_zero_and_linearity(iso):
 
 @pytest.mark.parametrize("precision", [0, 1], ids=["mixed", "fp32"])
 def test_config0_full(iso, precision):
-    from workload import CONFIGS
-    _run_and_compare(iso, CONFIGS[0], opts=dict(precision=precision))
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    _run_and_compare(iso, WORKLOADS[SMALL], opts=dict(precision=precision))
 
 
 def test_config1_full_block(iso):
     """One d = 768 decoder block, K = 8, every tensor against the oracle."""
-    from workload import CONFIGS
-    _run_and_compare(iso, CONFIGS[1], select=None)
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    _run_and_compare(iso, WORKLOADS[BLOCK], select=None)
 
 
 def _one_of_each_shape(lay):
@@ -369,8 +369,8 @@ def test_config2_full_size_sampled(iso):
     the benchmark's launch configuration: every 1-D tensor and one tensor of
     each 2-D shape against the oracle; the polar-factor properties for all 85
     matrices."""
-    from workload import CONFIGS
-    cfg = CONFIGS[2]
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    cfg = WORKLOADS[LLAMA_110M]
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
                                                       return_inputs=True)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
@@ -382,8 +382,8 @@ def test_config3_full_size_sampled(iso):
     bf16 replicas with per-tensor scales from LogUniform(1e-4, 1e-2): 1-D
     tensors and one tensor of each shape against the oracle, properties for
     all 169 matrices."""
-    from workload import CONFIGS
-    cfg = CONFIGS[3]
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    cfg = WORKLOADS[LLAMA_341M]
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
                                                       return_inputs=True)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
@@ -394,8 +394,8 @@ def test_config4_full_size_sampled(iso):
     """16 blocks d = 2048 / FFN 5632 + 32000 x 2048 (888M parameters), K = 64
     bf16 replicas (114 GB in HBM): 1-D tensors and one square matrix against
     the oracle, properties for all 113 matrices."""
-    from workload import CONFIGS
-    cfg = CONFIGS[4]
+    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    cfg = WORKLOADS[LLAMA_888M]
     sample = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_AVG]
     sample.append(next(i for i, t in enumerate(cfg.layout) if (t[1], t[2]) == (2048, 2048)))
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True)

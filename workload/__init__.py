@@ -6,5 +6,5 @@ plus per-worker Gaussian noise).  It holds none of the method's arithmetic.
 It is used by the tests, the benchmark and the smoke check, for both the HIP
 path and the float64 oracle, which then see the same bytes.
 """
-from .shapes import CONFIGS, WorkloadConfig, llama_layout, custom_layout  # noqa: F401
+from .shapes import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M, WorkloadConfig, llama_layout, custom_layout  # noqa: F401
 from .generate import ReplicaGenerator, tensor_seed  # noqa: F401

@@ -65,16 +65,23 @@ def _cfg(name, K, dtype, rank, lay, steps, **kw):
                           steps=steps, **kw)
 
 
-CONFIGS = {
+WORKLOADS = {w.name: w for w in (
     # one 128 x 64 matrix and one 64-vector, K = 4
-    0: _cfg("single-128x64-K4", 4, "f32", 32, custom_layout([(128, 64, KIND_ISO), (64, 1, KIND_AVG)]), 1),
+    _cfg("single-128x64-K4", 4, "f32", 32, custom_layout([(128, 64, KIND_ISO), (64, 1, KIND_AVG)]), 1),
     # one decoder block, d = 768, FFN 2048, K = 8
-    1: _cfg("llama-block-d768-K8", 8, "f32", 64, llama_layout(1, 768, 2048), 10),
+    _cfg("llama-block-d768-K8", 8, "f32", 64, llama_layout(1, 768, 2048), 10),
     # 12 blocks d = 768 + tied 32000 x 768 embedding (109.5M parameters), K = 16
-    2: _cfg("llama-12L-d768-V32000-K16", 16, "f32", 64, llama_layout(12, 768, 2048, 32000), 20),
+    _cfg("llama-12L-d768-V32000-K16", 16, "f32", 64, llama_layout(12, 768, 2048, 32000), 20),
     # 24 blocks d = 1024, FFN 2816 + 32000 x 1024 embedding, K = 32, bf16 replicas
-    3: _cfg("llama-24L-d1024-V32000-K32-bf16", 32, "bf16", 64, llama_layout(24, 1024, 2816, 32000), 10,
-            log_uniform_scale=(1e-4, 1e-2)),
+    _cfg("llama-24L-d1024-V32000-K32-bf16", 32, "bf16", 64, llama_layout(24, 1024, 2816, 32000), 10,
+         log_uniform_scale=(1e-4, 1e-2)),
     # 16 blocks d = 2048, FFN 5632 + 32000 x 2048 embedding, K = 64, bf16 replicas
-    4: _cfg("llama-16L-d2048-V32000-K64-bf16", 64, "bf16", 128, llama_layout(16, 2048, 5632, 32000), 5),
-}
+    _cfg("llama-16L-d2048-V32000-K64-bf16", 64, "bf16", 128, llama_layout(16, 2048, 5632, 32000), 5),
+)}
+
+# short names used by tests and the bench
+SMALL = "single-128x64-K4"
+BLOCK = "llama-block-d768-K8"
+LLAMA_110M = "llama-12L-d768-V32000-K16"
+LLAMA_341M = "llama-24L-d1024-V32000-K32-bf16"
+LLAMA_888M = "llama-16L-d2048-V32000-K64-bf16"
