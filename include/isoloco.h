@@ -12,7 +12,7 @@
  *             with Delta_l = U_l S_l V_l^T and sigma_bar_l = trace(S_l) / min(rows, cols)
  *             (Iso-C spectrum flattening, Section 2.2; the SVD branch of Algorithm 2)
  *   D_l     = Delta_l                                   every tensor of kind AVG
- *             (1-D tensors: "left unchanged", Section 4)
+ *             (1-D tensors take no correction, Section 4)
  *   B      <- mu * B + D;   P = D + mu * B;   theta <- theta - outer_lr * P
  *                                                       (Nesterov, Algorithm 2)
  *
