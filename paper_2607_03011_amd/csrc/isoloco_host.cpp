@@ -335,7 +335,7 @@ struct isoloco_plan_s {
   size_t off_cic[kSchedClasses] = {};
   // the second stream of the per-class mode, with its fork and join events
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_switch = nullptr;
   int last_streams = 1;  // streams the last aggregate's polar iteration used
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
@@ -864,16 +864,18 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
     // the workspace moved to another device: the second stream goes with it
     (void)hipEventDestroy(plan->ev_fork);
     (void)hipEventDestroy(plan->ev_join);
+    (void)hipEventDestroy(plan->ev_switch);
     (void)hipStreamDestroy(plan->side);
     plan->side = nullptr;
-    plan->ev_fork = plan->ev_join = nullptr;
+    plan->ev_fork = plan->ev_join = plan->ev_switch = nullptr;
   }
   if (plan->opts.streams == 2 && !plan->side) {
     // the second stream of the per-class mode (default priority), on the
     // workspace's device
     if ((e = hipStreamCreateWithFlags(&plan->side, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&plan->ev_fork, hipEventDisableTiming)) != hipSuccess ||
-        (e = hipEventCreateWithFlags(&plan->ev_join, hipEventDisableTiming)) != hipSuccess)
+        (e = hipEventCreateWithFlags(&plan->ev_join, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&plan->ev_switch, hipEventDisableTiming)) != hipSuccess)
       return hip_fail(e, "creating the second stream");
   }
   plan->ws = w;
@@ -919,6 +921,8 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   const DevTables t = dev_tables(plan);
   StepArgs a{};
+  a.steps_lo = 0;
+  a.steps_hi = INT32_MAX;
   a.theta = global;
   a.mom = momentum;
   for (int k = 0; k < plan->K; ++k) a.workers.p[k] = workers[k];
@@ -967,7 +971,10 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     // The polar iteration of the matrices of class cls (-1: every matrix) on
     // stream s, from the scalars fro_kernel set (tt.scalars; the matrices are
     // in tt.delta); the factor of matrix m ends in tt.x[scalars[m].qbuf].
-    auto iterate = [&](const DevTables& tt, bool check, int cls, hipStream_t s) -> hipError_t {
+    // ev_switch (if set): recorded on s after the class's first switch check,
+    // whose step count goes to *switch_steps (left alone if there is none)
+    auto iterate = [&](const DevTables& tt, bool check, int cls, hipStream_t s, hipEvent_t ev_switch = nullptr,
+                       int* switch_steps = nullptr) -> hipError_t {
       hipError_t r;
       const int Sx = cls < 0 ? S : plan->phase_end[cls].back();
       // what the end of step k (k + 1 steps done) means for class c: a switch
@@ -1043,6 +1050,10 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
           have_gram = true;
         }
         if ((r = norm(kNormPhase)) != hipSuccess) return r;
+        if (ev_switch && *switch_steps == 0 && cls >= 0 && na.action[cls] == kActSwitch) {
+          if ((r = hipEventRecord(ev_switch, s)) != hipSuccess) return r;
+          *switch_steps = k + 1;
+        }
       }
       if (check) {
         // the classes whose schedules run to the end of the sequence
@@ -1062,12 +1073,16 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     };
     // the scale and the write-back of the matrices in tt (after their polar
     // iteration) on stream s
-    auto tail = [&](const DevTables& tt, hipStream_t s) -> hipError_t {
+    // (only the matrices whose step count lies in [lo, hi])
+    auto tail = [&](const DevTables& tt, hipStream_t s, int lo = 0, int hi = INT32_MAX) -> hipError_t {
       hipError_t r;
+      StepArgs ar = a;
+      ar.steps_lo = lo;
+      ar.steps_hi = hi;
       what = "scale launch";
-      if ((r = timed_on(s, kPhOther, [&] { return launch_scale(tt, a, s); })) != hipSuccess) return r;
+      if ((r = timed_on(s, kPhOther, [&] { return launch_scale(tt, ar, s); })) != hipSuccess) return r;
       what = "finish launch";
-      return timed_on(s, kPhFinish, [&] { return launch_finish(tt, a, s); });
+      return timed_on(s, kPhFinish, [&] { return launch_finish(tt, ar, s); });
     };
     // The polar iteration of every matrix of tt; with two streams each class
     // on its own, and then (with_tail) each class's scale and write-back on
@@ -1086,11 +1101,28 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
           (r = hipStreamWaitEvent(plan->side, plan->ev_fork, 0)) != hipSuccess)
         return r;
       const DevTables tt_tall = class_tables(plan, tt, kSchedTall), tt_sq = class_tables(plan, tt, kSchedSquare);
+      // The square-ish matrices that stop at their class's first switch take
+      // their scale and write-back on the caller's stream (after the tall
+      // class's) while the others still iterate on the second stream.  A
+      // matrix's step count is final once it stops, and a matrix that goes on
+      // past that check only ever gets larger counts, so the two halves
+      // select disjoint matrices.
+      int sw = 0;
       if ((r = iterate(tt_tall, check, kSchedTall, st)) != hipSuccess ||
           (with_tail && (r = tail(tt_tall, st)) != hipSuccess) ||
-          (r = iterate(tt_sq, check, kSchedSquare, plan->side)) != hipSuccess ||
-          (with_tail && (r = tail(tt_sq, plan->side)) != hipSuccess))
+          (r = iterate(tt_sq, check, kSchedSquare, plan->side, with_tail ? plan->ev_switch : nullptr, &sw)) !=
+              hipSuccess)
         return r;
+      if (with_tail) {
+        if (sw > 0) {
+          what = "stream fork";
+          if ((r = hipStreamWaitEvent(st, plan->ev_switch, 0)) != hipSuccess ||
+              (r = tail(tt_sq, st, 0, sw)) != hipSuccess || (r = tail(tt_sq, plan->side, sw + 1)) != hipSuccess)
+            return r;
+        } else if ((r = tail(tt_sq, plan->side)) != hipSuccess) {
+          return r;
+        }
+      }
       what = "stream join";
       if ((r = hipEventRecord(plan->ev_join, plan->side)) != hipSuccess ||
           (r = hipStreamWaitEvent(st, plan->ev_join, 0)) != hipSuccess)
@@ -1276,6 +1308,7 @@ isoloco_status isoloco_plan_destroy(isoloco_plan_t plan) {
     for (hipEvent_t ev : plan->events) (void)hipEventDestroy(ev);
     if (plan->ev_fork) (void)hipEventDestroy(plan->ev_fork);
     if (plan->ev_join) (void)hipEventDestroy(plan->ev_join);
+    if (plan->ev_switch) (void)hipEventDestroy(plan->ev_switch);
     if (plan->side) (void)hipStreamDestroy(plan->side);
   }
   delete plan;

@@ -65,6 +65,9 @@ struct StepArgs {
   int heavy_ball;     // 1: theta <- theta - lr B (standard momentum); 0: Nesterov
   int target_update;  // 1: B <- mu B + Delta first and the update is corrected
   int scale;          // 0: mean singular value, 1: RMS, 2: sqrt(rows / cols)
+  // scale and write-back touch only the matrices whose polar step count lies
+  // in [steps_lo, steps_hi] (0 and INT32_MAX: every matrix)
+  int steps_lo, steps_hi;
 };
 
 // Arithmetic of one batched-product launch.

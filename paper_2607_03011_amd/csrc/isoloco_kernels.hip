@@ -1402,10 +1402,12 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
 __global__ void __launch_bounds__(kStreamThreads)
 trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatScalars* __restrict__ sc,
              const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ delta,
-             double* __restrict__ part_tr) {
+             double* __restrict__ part_tr, int steps_lo, int steps_hi) {
   __shared__ double red[4];
   const int ci = idx ? idx[blockIdx.x] : (int)blockIdx.x;
   const Chunk c = chunks[ci];
+  const int st = sc[c.mat].steps;
+  if (st < steps_lo || st > steps_hi) return;
   const float* q = sc[c.mat].qbuf ? x1 : x0;
   double s = 0.0;
   int done = 0;
@@ -1432,11 +1434,12 @@ trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, cons
 // 2: sqrt(rows / cols) of the tensor as stored (Muon's sqrt(fan_out / fan_in)).
 __global__ void __launch_bounds__(256)
 sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
-             MatScalars* __restrict__ sc, int n_mat, int mode, int cls) {
+             MatScalars* __restrict__ sc, int n_mat, int mode, int cls, int steps_lo, int steps_hi) {
   __shared__ double red[4];
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
   if (cls >= 0 && mi.sched != cls) return;
+  if (sc[m].steps < steps_lo || sc[m].steps > steps_hi) return;
   const double s = mode == 0 ? block_sum_range(part_tr, mi.chunk_begin, mi.chunk_end, red) : 0.0;
   if (threadIdx.x != 0) return;
   MatScalars& o = sc[m];
@@ -1487,10 +1490,11 @@ __global__ void __launch_bounds__(kStreamThreads)
 finish_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatScalars* __restrict__ sc,
               const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ dclip,
               float* __restrict__ theta, float* __restrict__ mom, float alpha, float lr, float mu, int heavy_ball,
-              int target_update, int clip) {
+              int target_update, int clip, int steps_lo, int steps_hi) {
   __shared__ TileLds tl;
   const Chunk c = chunks[idx ? idx[blockIdx.x] : blockIdx.x];
   const MatScalars s = sc[c.mat];
+  if (s.steps < steps_lo || s.steps > steps_hi) return;
   const float* q = clip ? dclip : (s.qbuf ? x1 : x0);
   float f = clip ? 1.f : alpha * s.sigma_bar;
   if (s.flags & 2) f = 0.f;
@@ -1711,9 +1715,9 @@ hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
   if (n == 0) return hipSuccess;
   if (a.scale == 0)
     hipLaunchKernelGGL(trace_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.scalars,
-                       t.x[0], t.x[1], t.delta, t.part_tr);
+                       t.x[0], t.x[1], t.delta, t.part_tr, a.steps_lo, a.steps_hi);
   hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat,
-                     a.scale, t.cls);
+                     a.scale, t.cls, a.steps_lo, a.steps_hi);
   return hipGetLastError();
 }
 
@@ -1722,7 +1726,7 @@ hipError_t launch_finish(const DevTables& t, const StepArgs& a, hipStream_t st) 
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(finish_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.scalars,
                      t.x[0], t.x[1], t.delta, a.theta, a.mom, a.alpha, a.lr, a.mu, a.heavy_ball, a.target_update,
-                     a.clip);
+                     a.clip, a.steps_lo, a.steps_hi);
   return hipGetLastError();
 }
 

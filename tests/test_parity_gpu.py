@@ -480,6 +480,57 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
     plan.close()
 
 
+def test_early_write_back_of_stopped_square_matrices(iso):
+    """With two streams, the square-ish matrices that stop at their class's
+    first phase end are scaled and written back on the caller's stream while
+    the others still iterate.  Every matrix must be written exactly once:
+    same theta, momentum and statistics as one stream, bit for bit, from a
+    non-zero momentum, on square matrices that stop at the first and at a
+    later phase end, and the oracle's result."""
+    from workload import custom_layout
+    lay, n = custom_layout([(192, 64, KIND_ISO), (256, 256, KIND_ISO), (256, 256, KIND_ISO),
+                            (128, 128, KIND_ISO), (96, 1, KIND_AVG)], align=4)
+    rng = np.random.default_rng(8)
+    delta = np.zeros(n)
+    mats = (_planted(192, 64, 1e-2, rng), _planted(256, 256, 1e-5, rng), _planted_tail(256, 256, 1e-8, rng),
+            _planted(128, 128, 1e-4, rng), 1e-3 * rng.standard_normal((96, 1)))
+    for (off, rows, cols, kind), m in zip(lay, mats):
+        delta[off:off + rows * cols] = (m * 1e-3).reshape(-1)
+    dev = torch.device("cuda", 0)
+    # theta = 0 so that the workers hold the planted spectra exactly (on top of
+    # theta ~ 0.02 the float32 rounding of theta - Delta would bury the 1e-8
+    # tail); a non-zero momentum shows a matrix written twice
+    theta0 = torch.zeros(n, dtype=torch.float32, device=dev)
+    mom0 = torch.tensor(1e-5 * rng.standard_normal(n), dtype=torch.float32, device=dev)
+    w = (theta0 - torch.tensor(delta, dtype=torch.float32, device=dev)).reshape(1, n).contiguous()
+    print("case: early write-back, planted square spectra, seed 8", flush=True)
+    out = []
+    for streams in (1, 2):
+        plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, opts=dict(streams=streams), device=dev)
+        ends = plan.schedule_phases(tall=0)
+        t, m = theta0.clone(), mom0.clone()
+        for _ in range(2):  # a second call reuses the plan's events and stream
+            t, m = theta0.clone(), mom0.clone()
+            plan.aggregate(t, w, m, 1.0, 0.7, 0.9)
+        torch.cuda.synchronize()
+        out.append((t, m, [(s.steps, s.flags, s.sigma_bar) for s in plan.stats()], ends))
+        plan.close()
+    steps = [s[0] for s in out[1][2]]
+    ends = out[1][3]
+    assert steps[1] == ends[0] and steps[2] > ends[0], (steps, ends)
+    assert torch.equal(out[0][0], out[1][0]) and torch.equal(out[0][1], out[1][1])
+    assert out[0][2] == out[1][2]
+    ref = oracle_per_tensor(lay, theta0.cpu().numpy(), [w.cpu().numpy()[0]], mom0.cpu().numpy(), 1.0, 0.7, 0.9)
+    th, mo = out[1][0].cpu().numpy(), out[1][1].cpu().numpy()
+    for i, (th_r, b_r, sb_r) in ref.items():
+        off, rows, cols, kind = lay[i]
+        e_t = relF(th[off:off + rows * cols] - theta0.cpu().numpy()[off:off + rows * cols],
+                   th_r - theta0.cpu().numpy()[off:off + rows * cols].astype(np.float64))
+        e_b = relF(mo[off:off + rows * cols], b_r)
+        print("tensor %d steps %d: theta step %.2e momentum %.2e" % (i, steps[i], e_t, e_b), flush=True)
+        assert e_t <= TOL and e_b <= TOL
+
+
 @pytest.mark.parametrize("precision", [0, 1, 3], ids=["mixed", "fp32", "bf16x6"])
 def test_wide_geometric_spectrum(iso, precision):
     """Spectra with many singular values far below the largest one need the
