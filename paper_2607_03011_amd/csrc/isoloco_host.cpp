@@ -336,6 +336,8 @@ struct isoloco_plan_s {
   // the second stream of the per-class mode, with its fork and join events
   hipStream_t side = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_switch = nullptr;
+  int n_cu = 0;          // compute units of the workspace's device
+  int64_t sq_tiles = 0;  // 256 x 256 output tiles of one update of every square-ish matrix
   int last_streams = 1;  // streams the last aggregate's polar iteration used
   size_t off_psq = 0, off_ptr = 0, off_delta = 0, off_x0 = 0, off_x1 = 0, off_gram = 0;
   size_t off_x2 = 0, off_sc2 = 0;  // clip variants only
@@ -423,6 +425,7 @@ void plan_matrices(isoloco_plan_s* p) {
     mi.vec = (mi.m % 4 == 0 && mi.n % 4 == 0) ? 1 : 0;
     mi.tensor = (int32_t)t;
     mi.sched = mi.m >= 2 * (int64_t)mi.n ? kSchedTall : kSchedSquare;
+    if (mi.sched == kSchedSquare) p->sq_tiles += (int64_t)((mi.m + 255) / 256) * ((mi.n + 255) / 256);
     // Split the Gram's K dimension of a tall matrix (few output tiles, long
     // K) so that no single tile dominates the launch.  Every slice writes an
     // n x n partial that is read back once, so the count stays small: six
@@ -875,7 +878,8 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
     if ((e = hipStreamCreateWithFlags(&plan->side, hipStreamNonBlocking)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&plan->ev_fork, hipEventDisableTiming)) != hipSuccess ||
         (e = hipEventCreateWithFlags(&plan->ev_join, hipEventDisableTiming)) != hipSuccess ||
-        (e = hipEventCreateWithFlags(&plan->ev_switch, hipEventDisableTiming)) != hipSuccess)
+        (e = hipEventCreateWithFlags(&plan->ev_switch, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipDeviceGetAttribute(&plan->n_cu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
       return hip_fail(e, "creating the second stream");
   }
   plan->ws = w;
@@ -1107,10 +1111,15 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       // matrix's step count is final once it stops, and a matrix that goes on
       // past that check only ever gets larger counts, so the two halves
       // select disjoint matrices.
+      // This pays only where the iterations after that check leave CUs idle:
+      // with more than 8 update tiles per CU in the class (888M workload:
+      // 4096 tiles of 2048 x 2048 matrices, half of which go on) the early
+      // pass competes with them and is left out.
+      const bool early = with_tail && plan->sq_tiles <= 8 * (int64_t)plan->n_cu;
       int sw = 0;
       if ((r = iterate(tt_tall, check, kSchedTall, st)) != hipSuccess ||
           (with_tail && (r = tail(tt_tall, st)) != hipSuccess) ||
-          (r = iterate(tt_sq, check, kSchedSquare, plan->side, with_tail ? plan->ev_switch : nullptr, &sw)) !=
+          (r = iterate(tt_sq, check, kSchedSquare, plan->side, early ? plan->ev_switch : nullptr, &sw)) !=
               hipSuccess)
         return r;
       if (with_tail) {
