@@ -112,6 +112,26 @@ def finish_bytes(layout):
     return sum(20 * r * c for (_, r, c, kind) in layout if kind == 0)
 
 
+def copy_ceiling_gbs(torch, dev, nbytes, reps=5):
+    """Bandwidth of a plain device-to-device copy that moves nbytes (nbytes / 2
+    read and nbytes / 2 written), timed with events on the current stream:
+    the best of `reps` copies, in GB/s."""
+    n = max(1, int(nbytes // 8))
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del src, dst
+    return 8.0 * n / (best * 1e-3) / 1e9
+
+
 def cpu_baseline(cfg, theta, workers, mom, budget_s, variant=None):
     """The float64 oracle timed on the host on a bounded sample of the step:
     all 1-D tensors plus one tensor of each 2-D shape, extrapolated to the whole
@@ -272,6 +292,8 @@ def main():
     per = {k: v / args.steps for k, v in acc.items()}
     st = plan.stats()
     resid = max(s.orth_resid for s, t in zip(st, cfg.layout) if t[3] == 0)
+    n_below = sum(1 for s, t in zip(st, cfg.layout) if t[3] == 0 and s.flags & iso.ISOLOCO_FLAG_BELOW_RESOLUTION)
+    n_unconv = sum(1 for s, t in zip(st, cfg.layout) if t[3] == 0 and s.flags & iso.ISOLOCO_FLAG_NOT_CONVERGED)
 
     flops, mfma_flops = gemm_flops_per_step(cfg.layout, st, True, args.precision)
     steps_hist = {}
@@ -282,10 +304,16 @@ def main():
     # (with two streams launches overlap, and their durations add up to more)
     gemm_ms = per["products_busy_ms"]
     launch_sum_ms = per["gram_ms"] + per["poly_ms"] + per["update_ms"]
+    # The method's work is counted as fp32 products (each split-bf16 product
+    # stands for one fp32 product) against the peak of the MFMA type that runs
+    # them: bf16 for the split modes, fp32 for the fp32 mode.  The bf16 part
+    # products actually issued (3, 5 or 6 per fp32 product) are reported beside.
     peak = PEAK_FP32_MFMA_TFS if args.precision == "fp32" else PEAK_BF16_MFMA_TFS
-    gemm_tfs = mfma_flops / (gemm_ms * 1e-3) / 1e12
+    gemm_tfs = flops / (gemm_ms * 1e-3) / 1e12
+    issued_tfs = mfma_flops / (gemm_ms * 1e-3) / 1e12
     rbytes = reduce_bytes(cfg.layout, cfg.n_elems, cfg.K, wbytes)
     red_gbs = rbytes / (per["reduce_ms"] * 1e-3) / 1e9
+    copy_gbs = copy_ceiling_gbs(torch, dev, rbytes)
     fbytes = finish_bytes(cfg.layout)
     fin_gbs = fbytes / (per["finish_ms"] * 1e-3) / 1e9
     gbytes = gemm_bytes_per_step(cfg.layout, st)
@@ -304,21 +332,28 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 (polar products: %s)" % args.precision,
+        "dtype": ("f32 (storage and accumulation; polar products in fp32 MFMA)" if args.precision == "fp32" else
+                  "f32 (storage and accumulation; polar products as split-bf16 MFMA, %s)" % args.precision),
         "data": "synthetic: seeded low-rank + Gaussian-noise pseudo-gradients, replicas resident in HBM; "
                 "every step restores theta and B = 0 so that it sees fresh pseudo-gradients",
         "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
                    "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
                    "variant": args.variant,
                    "polar_phase_ends": phase_ends, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
-        "roofline": {"bound": "mfma", "kernel": "gemm_%s_kernel (Gram, polynomial and update products)" %
-                     ("f32" if args.precision == "fp32" else "bf16"), "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
+        "roofline": {"bound": "mfma", "kernel": "batched polar products (gemm_%s: Gram, polynomial, update)" %
+                     ("f32_kernel" if args.precision == "fp32" else "bf16_kernel, gemm_bf16_big_kernel"),
+                     "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(gemm_tfs / peak, 4),
+                     "work": "the method's products as fp32 flops (symmetric Gram n(n+1)m, polynomial "
+                             "n(n+1)n, update 2mn^2 per polar step) over the time some product runs",
                      "traffic": mt["gemm_bytes_per_step"] if measured else None,
                      "traffic_unit": "HBM bytes per step over all product launches",
+                     "traffic_source": ("stored: rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE on these sources "
+                                        "(profiles/hbm_traffic__llama12L_K16.md)") if measured else None,
                      "algorithmic_bytes_per_step": gbytes,
-                     "mfma_flops_per_step": mfma_flops, "fp32_equivalent_flops_per_step": flops,
-                     "fp32_equivalent_tflops": round(flops / (gemm_ms * 1e-3) / 1e12, 3),
+                     "fp32_equivalent_flops_per_step": flops,
+                     "issued_mfma_flops_per_step": mfma_flops,
+                     "issued_tflops": round(issued_tfs, 3), "issued_frac": round(issued_tfs / peak, 4),
                      "ms_per_step": round(gemm_ms, 4),
                      "launch_durations_ms_per_step": round(launch_sum_ms, 4),
                      "streams": plan_streams,
@@ -326,7 +361,11 @@ def main():
         "roofline_reduce": {"bound": "hbm", "kernel": "reduce_kernel", "achieved": round(red_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(red_gbs / PEAK_HBM_GBS, 4),
                             "traffic": mt["reduce_bytes_per_launch"] if measured else None,
-                            "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4)},
+                            "bytes_per_launch": rbytes, "ms": round(per["reduce_ms"], 4),
+                            "copy_ceiling_gbs": round(copy_gbs, 1),
+                            "frac_of_copy_ceiling": round(red_gbs / copy_gbs, 4),
+                            "copy_ceiling_note": "same run: a device-to-device copy moving the same bytes "
+                                                 "(half read, half written), best of 5"},
         "roofline_finish": {"bound": "hbm", "kernel": "finish_kernel", "achieved": round(fin_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(fin_gbs / PEAK_HBM_GBS, 4),
                             "traffic": mt["finish_bytes_per_step"] if measured else None,
@@ -338,6 +377,8 @@ def main():
         "library_ms_p10_p50_p90": [round(float(x), 4) for x in np.percentile(step_ms, [10, 50, 90])],
         "input_restore_ms": round(restore_ms, 4),
         "max_orth_resid": resid,
+        "matrices_below_resolution": n_below,
+        "matrices_not_converged": n_unconv,
         "matrices_by_steps": {str(k): v for k, v in sorted(steps_hist.items())},
     }
     if not args.no_cpu_baseline:

@@ -37,8 +37,13 @@
  * then repeats the step on the same buffers.
  *
  * Errors.  Every function returns an isoloco_status; no C++ exception crosses
- * this boundary.  A call that fails validation enqueues nothing.  The last
- * error message of the calling thread is available from isoloco_last_error().
+ * this boundary.  A call that fails validation enqueues nothing.  An
+ * aggregate that fails later (ISOLOCO_ERR_HIP, a launch or event call
+ * refused by the runtime) may have enqueued part of the step, so that theta,
+ * B and the workspace hold a partial result; the caller's stream is then
+ * still ordered after every kernel the call enqueued, on either stream, and
+ * the first error is returned.  The last error message of the calling thread
+ * is available from isoloco_last_error().
  */
 #ifndef ISOLOCO_H
 #define ISOLOCO_H
@@ -169,13 +174,21 @@ typedef struct {
   int32_t steps;    /* polar iteration steps taken (ISO tensors): the short schedule's length
                        if the matrix stopped there, else the full length                     */
   int32_t flags;    /* bit 0: Delta_l had a non-finite value; bit 1: Delta_l == 0;
-                       bit 2: residual above 1e-3 (not converged)                            */
+                       bit 2: residual above 1e-3 after the last step (not converged);
+                       bit 3: below resolution -- the matrix failed the check after the
+                       phase built for sigma_min / ||Delta^T Delta||_F^(1/2) >= 2e-8, so a
+                       singular value lies below about 2e-8 of the normalisation, where the
+                       float32 rounding of Delta itself moves singular values by their own
+                       size: the sign of that direction in Q is decided by rounding and can
+                       differ from the float64 SVD's (Q stays orthonormal; the bit needs a
+                       phase bound at or below 2e-8, which the default phases have)      */
   int32_t reserved;
 } isoloco_tensor_stats;
 
 #define ISOLOCO_FLAG_NONFINITE 1
 #define ISOLOCO_FLAG_ZERO 2
 #define ISOLOCO_FLAG_NOT_CONVERGED 4
+#define ISOLOCO_FLAG_BELOW_RESOLUTION 8
 
 typedef struct isoloco_plan_s* isoloco_plan_t;
 

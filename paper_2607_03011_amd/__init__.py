@@ -44,6 +44,7 @@ ISOLOCO_CLIP_LOW = 2
 ISOLOCO_FLAG_NONFINITE = 1
 ISOLOCO_FLAG_ZERO = 2
 ISOLOCO_FLAG_NOT_CONVERGED = 4
+ISOLOCO_FLAG_BELOW_RESOLUTION = 8
 
 EXPORTED_SYMBOLS = (
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",

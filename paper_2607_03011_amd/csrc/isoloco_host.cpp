@@ -18,6 +18,11 @@
 
 using namespace isoloco;
 
+static_assert(kFlagNonfinite == ISOLOCO_FLAG_NONFINITE && kFlagZero == ISOLOCO_FLAG_ZERO &&
+                  kFlagNotConverged == ISOLOCO_FLAG_NOT_CONVERGED &&
+                  kFlagBelowResolution == ISOLOCO_FLAG_BELOW_RESOLUTION,
+              "the kernels' flag bits are the ABI's");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -60,6 +65,12 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // directly for intervals narrower than 1e-3.
 
 constexpr double kCushion = 0.1;
+// A matrix that fails the check at the end of a phase built for a bound at or
+// below this (as a fraction of ||X^T X||_F^(1/2)) has a singular value there.
+// The float32 rounding of Delta itself moves singular values by about 1e-8
+// of the normalisation for n = 768, so such a direction's sign in Q is set by
+// rounding rather than by Delta: the matrix is flagged (not an error).
+constexpr float kResolutionBound = 2e-8f;
 // ||X^T X - I||_F / sqrt(n) below which a matrix stops after the short schedule
 // (about 5x the rounding floor of the split-bf16 Gram; the polar factor is then
 // within about half this value of the exact one)
@@ -324,6 +335,7 @@ struct isoloco_plan_s {
   // phase (the last is the class's length).
   std::vector<double> sched[kSchedClasses];
   std::vector<int> phase_end[kSchedClasses];
+  std::vector<float> phase_bound[kSchedClasses];  // the bound each phase was built for
   int n_steps = 0;            // longest schedule: polar steps the launch sequence runs
   std::vector<float> coef;    // device table: [class][n_steps][3], padded with each class's last step
   int64_t n2d = 0;   // elements of one Delta / X buffer
@@ -363,9 +375,10 @@ namespace {
 // the others run the next phase, built for what the phases so far made of its
 // bound.  A negative first bound: the single schedule for [ell0, 1].
 void build_phases(const isoloco_options& o, const float (&bound)[3], std::vector<double>& sched,
-                  std::vector<int>& ends) {
+                  std::vector<int>& ends, std::vector<float>& bounds_out) {
   sched.clear();
   ends.clear();
+  bounds_out.clear();
   if (o.orth == ISOLOCO_ORTH_NS5) {
     // the fast variant: a fixed five-step Newton-Schulz iteration of the Muon
     // quintic (Section 4.3; the paper's own coefficients are not printed)
@@ -373,6 +386,7 @@ void build_phases(const isoloco_options& o, const float (&bound)[3], std::vector
   } else if (bound[0] > o.ell0) {
     sched = build_schedule(bound[0], o.tol, o.max_steps);
     ends.push_back((int)sched.size() / 3);
+    bounds_out.push_back(bound[0]);
     std::vector<double> bounds;
     double above = bound[0];
     for (int i = 1; i < 3 && bound[i] >= 0.f; ++i)
@@ -390,11 +404,15 @@ void build_phases(const isoloco_options& o, const float (&bound)[3], std::vector
       if (rest.empty()) continue;
       sched.insert(sched.end(), rest.begin(), rest.end());
       ends.push_back((int)sched.size() / 3);
+      bounds_out.push_back((float)b);
     }
   } else {
     sched = build_schedule(o.ell0, o.tol, o.max_steps);
   }
-  if (ends.empty() || ends.back() != (int)sched.size() / 3) ends.push_back((int)sched.size() / 3);
+  if (ends.empty() || ends.back() != (int)sched.size() / 3) {
+    ends.push_back((int)sched.size() / 3);
+    bounds_out.push_back(o.orth == ISOLOCO_ORTH_NS5 ? 0.f : o.ell0);
+  }
 }
 
 void plan_matrices(isoloco_plan_s* p) {
@@ -795,7 +813,8 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     }
     p->opts = o;
     for (int c = 0; c < kSchedClasses; ++c)
-      build_phases(o, c == kSchedTall ? o.phase_tall : o.phase_square, p->sched[c], p->phase_end[c]);
+      build_phases(o, c == kSchedTall ? o.phase_tall : o.phase_square, p->sched[c], p->phase_end[c],
+                   p->phase_bound[c]);
     p->n_steps = 0;
     for (int c = 0; c < kSchedClasses; ++c) p->n_steps = std::max(p->n_steps, p->phase_end[c].back());
     p->coef.assign((size_t)kSchedClasses * p->n_steps * 3, 0.f);
@@ -992,6 +1011,14 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
           if (ends[i] == k + 1) return kActSwitch;
         return kActNone;
       };
+      // at a switch after step k: was the phase that ends there built for a
+      // bound at or below the float32 resolution of Delta?
+      auto below_after = [&](int c, int k) {
+        const std::vector<int>& ends = plan->phase_end[c];
+        for (size_t i = 0; i + 1 < ends.size(); ++i)
+          if (ends[i] == k + 1) return plan->phase_bound[c][i] <= kResolutionBound ? 1 : 0;
+        return 0;
+      };
       NormArgs na{};
       na.cls = cls;
       na.flag_unconverged = ns5 ? 0 : 1;
@@ -1034,6 +1061,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
         bool any = false, residual = false;
         for (int c = 0; c < kSchedClasses; ++c) {
           na.action[c] = action_after(c, k);
+          na.flag_below[c] = na.action[c] == kActSwitch ? below_after(c, k) : 0;
           any = any || na.action[c] != kActNone;
           residual = residual || na.action[c] == kActSwitch || na.action[c] == kActFinal;
         }
@@ -1061,8 +1089,10 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       }
       if (check) {
         // the classes whose schedules run to the end of the sequence
-        for (int c = 0; c < kSchedClasses; ++c)
+        for (int c = 0; c < kSchedClasses; ++c) {
           na.action[c] = (cls < 0 || c == cls) && plan->phase_end[c].back() == Sx ? kActFinal : kActNone;
+          na.flag_below[c] = 0;
+        }
         na.steps_here = Sx;
         na.buf_here = (Sx - 1) & 1;
         PolarStep pc{};
@@ -1116,27 +1146,38 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       // 4096 tiles of 2048 x 2048 matrices, half of which go on) the early
       // pass competes with them and is left out.
       const bool early = with_tail && plan->sq_tiles <= 8 * (int64_t)plan->n_cu;
-      int sw = 0;
-      if ((r = iterate(tt_tall, check, kSchedTall, st)) != hipSuccess ||
-          (with_tail && (r = tail(tt_tall, st)) != hipSuccess) ||
-          (r = iterate(tt_sq, check, kSchedSquare, plan->side, early ? plan->ev_switch : nullptr, &sw)) !=
-              hipSuccess)
-        return r;
-      if (with_tail) {
+      auto forked = [&]() -> hipError_t {
+        hipError_t q;
+        int sw = 0;
+        if ((q = iterate(tt_tall, check, kSchedTall, st)) != hipSuccess ||
+            (with_tail && (q = tail(tt_tall, st)) != hipSuccess) ||
+            (q = iterate(tt_sq, check, kSchedSquare, plan->side, early ? plan->ev_switch : nullptr, &sw)) !=
+                hipSuccess)
+          return q;
+        if (!with_tail) return hipSuccess;
         if (sw > 0) {
           what = "stream fork";
-          if ((r = hipStreamWaitEvent(st, plan->ev_switch, 0)) != hipSuccess ||
-              (r = tail(tt_sq, st, 0, sw)) != hipSuccess || (r = tail(tt_sq, plan->side, sw + 1)) != hipSuccess)
-            return r;
-        } else if ((r = tail(tt_sq, plan->side)) != hipSuccess) {
-          return r;
+          if ((q = hipStreamWaitEvent(st, plan->ev_switch, 0)) != hipSuccess ||
+              (q = tail(tt_sq, st, 0, sw)) != hipSuccess || (q = tail(tt_sq, plan->side, sw + 1)) != hipSuccess)
+            return q;
+          return hipSuccess;
         }
+        return tail(tt_sq, plan->side);
+      };
+      // Once the fork is recorded the join is made whatever happens after it,
+      // so that the caller's stream is ordered after every kernel already
+      // enqueued on the second stream, also when a later launch fails (the
+      // first error is returned).
+      r = forked();
+      const char* what_first = what;
+      hipError_t rj = hipEventRecord(plan->ev_join, plan->side);
+      if (rj == hipSuccess) rj = hipStreamWaitEvent(st, plan->ev_join, 0);
+      if (r != hipSuccess) {
+        what = what_first;
+        return r;
       }
       what = "stream join";
-      if ((r = hipEventRecord(plan->ev_join, plan->side)) != hipSuccess ||
-          (r = hipStreamWaitEvent(st, plan->ev_join, 0)) != hipSuccess)
-        return r;
-      return hipSuccess;
+      return rj;
     };
     if (!a.clip) {
       if ((e = polar(t, plan->opts.check == 1, true)) != hipSuccess) return hip_fail(e, what);

@@ -110,6 +110,10 @@ struct NormArgs {
   int steps_total[kSchedClasses], buf_total[kSchedClasses];  // per class: schedule length, its buffer
   float tol_switch;          // residual below which a matrix stops at a switch
   int flag_unconverged;      // kActFinal: flag residuals above 1e-3 (not for a fixed-length variant)
+  // kActSwitch, per class: the phase that ends here was built for a bound at or
+  // below the float32 resolution of Delta, so a matrix that fails its check has
+  // a singular value that float arithmetic cannot resolve (kFlagBelowResolution)
+  int flag_below[kSchedClasses];
 };
 
 // Initial per-matrix iteration state: steps and result buffer of each class's full schedule

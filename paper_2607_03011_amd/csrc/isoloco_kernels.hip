@@ -318,8 +318,8 @@ fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
   MatScalars o;
   o.fro = (float)sqrt(s);
   o.flags = 0;
-  if (!isfinite(s)) o.flags |= 1;
-  else if (s == 0.0) o.flags |= 2;
+  if (!isfinite(s)) o.flags |= kFlagNonfinite;
+  else if (s == 0.0) o.flags |= kFlagZero;
   o.inv_fro = (o.flags == 0) ? (float)(1.0 / sqrt(s)) : 0.f;
   o.gscale = (a.fixed_g && o.flags == 0) ? 1.f : 0.f;  // else set from the first Gram
   o.sigma_bar = 0.f;
@@ -1380,18 +1380,22 @@ __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const d
   const int nt = gram_tiles(mi.n);
   for (int x = 0; x < nt; ++x) s += part[mi.norm_off + x];
   if (a.mode == kNormFirst) {
-    o.gscale = (o.flags == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
+    o.gscale = ((o.flags & kFlagInput) == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
     return;
   }
   o.resid = (float)sqrt(s / mi.n);
   if (act == kActSwitch) {
     // stop at the end of this phase when every singular value is already at 1
-    const bool go_on = o.flags == 0 && !(o.resid <= a.tol_switch);
+    const bool go_on = (o.flags & kFlagInput) == 0 && !(o.resid <= a.tol_switch);
+    // a matrix that still has a singular value away from 1 after the schedule
+    // for a bound at the float32 resolution of Delta has one below it: its
+    // direction in Q is decided by rounding, not by Delta
+    if (go_on && a.flag_below[mi.sched]) o.flags |= kFlagBelowResolution;
     o.active = go_on ? 1 : 0;
     o.steps = go_on ? a.steps_total[mi.sched] : a.steps_here;
     o.qbuf = go_on ? a.buf_total[mi.sched] : a.buf_here;
   } else {
-    if (a.flag_unconverged && !(o.resid <= 1e-3f) && o.flags == 0) o.flags |= 4;
+    if (a.flag_unconverged && !(o.resid <= 1e-3f) && (o.flags & kFlagInput) == 0) o.flags |= kFlagNotConverged;
     o.active = 0;
   }
 }
@@ -1443,8 +1447,8 @@ sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_t
   const double s = mode == 0 ? block_sum_range(part_tr, mi.chunk_begin, mi.chunk_end, red) : 0.0;
   if (threadIdx.x != 0) return;
   MatScalars& o = sc[m];
-  if (o.flags & 1) o.sigma_bar = __builtin_nanf("");
-  else if (o.flags & 2) o.sigma_bar = 0.f;
+  if (o.flags & kFlagNonfinite) o.sigma_bar = __builtin_nanf("");
+  else if (o.flags & kFlagZero) o.sigma_bar = 0.f;
   else if (mode == 0) o.sigma_bar = (float)(s / mi.n);
   else if (mode == 1) o.sigma_bar = (float)((double)o.fro / sqrt((double)mi.n));
   else o.sigma_bar = (float)(mi.wide ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
@@ -1497,7 +1501,7 @@ finish_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, con
   if (s.steps < steps_lo || s.steps > steps_hi) return;
   const float* q = clip ? dclip : (s.qbuf ? x1 : x0);
   float f = clip ? 1.f : alpha * s.sigma_bar;
-  if (s.flags & 2) f = 0.f;
+  if (s.flags & kFlagZero) f = 0.f;
   if (c.rows) {
     const int TR = c.rows, TC = c.cols;
     for (int it = threadIdx.x; it < TC * (kTileRows / 4); it += kStreamThreads) {
@@ -1550,7 +1554,7 @@ clip_prep_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restrict_
   const Chunk c = chunks[blockIdx.x];
   const MatScalars s = sc[c.mat];
   const float* q = s.qbuf ? x1 : x0;
-  const float sb = s.flags ? 0.f : s.sigma_bar;
+  const float sb = (s.flags & kFlagInput) ? 0.f : s.sigma_bar;
   double sq = 0.0;
   for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
     const int64_t o = chunk_ws(c, i);
@@ -1575,7 +1579,7 @@ clip_compose_kernel(const Chunk* __restrict__ chunks, const MatScalars* __restri
   const MatScalars s = sc[c.mat];
   const float sg = clip == 1 ? -0.5f : 0.5f;
   const float sb = s.sigma_bar;
-  const float al = (s.flags & 2) ? 0.f : alpha;
+  const float al = (s.flags & kFlagZero) ? 0.f : alpha;
   for (int i = threadIdx.x; i < c.count; i += kStreamThreads) {
     const int64_t o = chunk_ws(c, i);
     delta[o] = al * (0.5f * delta[o] + sg * x0[o] + sb * qcopy[o]);

@@ -85,6 +85,13 @@ struct Chunk {
 constexpr int kTileRows = 32;
 constexpr int kTileCols = 128;
 
+// Bits of MatScalars::flags (the values of the ISOLOCO_FLAG_* constants).
+constexpr int kFlagNonfinite = 1;        // Delta had a non-finite value
+constexpr int kFlagZero = 2;             // Delta == 0
+constexpr int kFlagNotConverged = 4;     // Q^T Q - I above 1e-3 after the last step
+constexpr int kFlagBelowResolution = 8;  // smallest singular value below the float32 resolution
+constexpr int kFlagInput = kFlagNonfinite | kFlagZero;  // properties of the input itself
+
 // Per-matrix scalars kept in the workspace.
 struct MatScalars {
   float fro;        // ||Delta||_F

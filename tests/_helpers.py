@@ -54,6 +54,47 @@ def variant_opts(variant):
     return {k: VARIANT_OPTS[k][v] for k, v in (variant or {}).items()}
 
 
+def oracle_pool_size():
+    """Worker processes for the oracle: the host's cores, at most 16 (the CPU
+    share of a one-GPU machine)."""
+    import os
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def oracle_per_tensor_spawned(inputs, alpha, lr, mu, variant=None, processes=None):
+    """The oracle's outer step tensor by tensor in a pool of freshly started
+    processes (safe after the GPU has been used: nothing is forked, and the
+    children import only numpy and the oracle), one compiled-Jacobi thread
+    each, largest tensors first.  ``inputs``: one ((offset, rows, cols, kind),
+    theta, [worker_k], B) per tensor, each array holding that tensor's
+    elements only.  Returns [(theta_new, B_new, sigma_bar)] in input order."""
+    import os
+    order = sorted(range(len(inputs)), key=lambda j: -inputs[j][0][1] * inputs[j][0][2])
+    jobs = []
+    for j in order:
+        (off, rows, cols, kind), th, ws, B = inputs[j]
+        jobs.append(((0, rows, cols, kind), th, list(ws), B, alpha, lr, mu, variant))
+    procs = processes or oracle_pool_size()
+    saved = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS")}
+    # the children read these when their libraries load: one thread per process
+    os.environ["OMP_NUM_THREADS"] = "1"
+    os.environ["OPENBLAS_NUM_THREADS"] = "1"
+    try:
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(max(1, min(procs, len(jobs)))) as pool:
+            res = pool.map(_oracle_one, jobs, chunksize=1)
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    out = [None] * len(inputs)
+    for j, r in zip(order, res):
+        out[j] = r
+    return out
+
+
 def oracle_per_tensor(layout, theta, workers, B, alpha, lr, mu, select=None, processes=1, variant=None):
     """Oracle outer step evaluated tensor by tensor (the tensors of the step are
     independent), optionally on a subset.  Runs in this process by default (the

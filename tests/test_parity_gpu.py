@@ -10,7 +10,8 @@ recovered from the momentum (B_1 = alpha sigma_bar Q when B_0 = 0) and
 import numpy as np
 import pytest
 
-from _helpers import KIND_AVG, KIND_ISO, oracle_per_tensor, relF, variant_opts, workers_host
+from _helpers import (KIND_AVG, KIND_ISO, oracle_per_tensor, oracle_per_tensor_spawned, relF, variant_opts,
+                      workers_host)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -43,7 +44,15 @@ def _host_slices(theta, workers, mom, layout, select):
 
 
 def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select=None, check_q=True,
-                     theta=None, mom=None, plan=None, opts=None, return_inputs=False, variant=None):
+                     theta=None, mom=None, plan=None, opts=None, return_inputs=False, variant=None,
+                     spawned=False, max_flagged=0):
+    """One step through the C ABI against the oracle on the same bytes.  Every
+    selected tensor must match within TOL, except matrices that carry the
+    below-resolution flag (a singular value below what the float32 rounding
+    of Delta resolves, so the sign of its direction may differ from the
+    float64 SVD's): at most ``max_flagged`` of them, each still orthonormal
+    and finite, reported with their errors.  ``spawned``: evaluate the oracle
+    in a process pool (large layouts)."""
     if variant:
         opts = dict(opts or {}, **variant_opts(variant))
         # Q = B / (alpha * scale) is orthonormal only for the exact polar factor
@@ -68,12 +77,25 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
     plan.aggregate(theta, workers, mom, alpha, lr, mu)
     torch.cuda.synchronize()
     st = plan.stats()
+    if spawned:
+        import time
+        from _helpers import oracle_pool_size
+        t0 = time.time()
+        res = oracle_per_tensor_spawned([(cfg.layout[i],) + host[i] for i in sel], alpha, lr, mu, variant=variant)
+        ref_all = dict(zip(sel, res))
+        print("oracle: %d tensors in %.1f s on %d processes" % (len(sel), time.time() - t0, oracle_pool_size()),
+              flush=True)
+    flagged = []
+    worst_iso = worst_avg = 0.0
     for i in sel:
         off, rows, cols, kind = cfg.layout[i]
         sl = slice(off, off + rows * cols)
         th0, wh, b0 = host[i]
-        th_r, b_r, sb_r = oracle_per_tensor([(0, rows, cols, kind)], th0, wh, b0, alpha, lr, mu,
-                                            variant=variant)[0]
+        if spawned:
+            th_r, b_r, sb_r = ref_all[i]
+        else:
+            th_r, b_r, sb_r = oracle_per_tensor([(0, rows, cols, kind)], th0, wh, b0, alpha, lr, mu,
+                                                variant=variant)[0]
         th = theta[sl].double().cpu().numpy()
         b = mom[sl].double().cpu().numpy()
         e_th = relF(th, th_r)
@@ -83,8 +105,18 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
         if kind == KIND_ISO:
             msg += " sigma_bar gpu %.6e oracle %.6e steps %d resid %.2e flags %d" % (
                 st[i].sigma_bar, sb_r, st[i].steps, st[i].orth_resid, st[i].flags)
-        print(msg, flush=True)
-        assert e_th <= TOL and e_b <= TOL and e_upd <= TOL, msg
+        below = kind == KIND_ISO and bool(st[i].flags & iso.ISOLOCO_FLAG_BELOW_RESOLUTION)
+        if kind == KIND_ISO and not below:
+            worst_iso = max(worst_iso, e_th, e_b)
+        elif kind != KIND_ISO:
+            worst_avg = max(worst_avg, e_th, e_b)
+        print(msg + (" [below resolution]" if below else ""), flush=True)
+        if below:
+            flagged.append((i, e_th, e_b))
+            assert np.isfinite(th).all() and np.isfinite(b).all(), msg
+            assert 0 <= st[i].orth_resid <= TOL, msg
+        else:
+            assert e_th <= TOL and e_b <= TOL and e_upd <= TOL, msg
         if kind == KIND_ISO and check_q and not b0.any() and sb_r > 0 and alpha != 0:
             Q = b.reshape(rows, cols) / (alpha * st[i].sigma_bar)
             G = Q.T @ Q if rows >= cols else Q @ Q.T
@@ -92,6 +124,12 @@ def _run_and_compare(iso, cfg, seed=0, step=1, alpha=1.0, lr=0.7, mu=0.9, select
             orth = np.linalg.norm(G - np.eye(r)) / np.sqrt(r)
             assert orth <= TOL, (i, orth)
             assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
+    print("worst relative Frobenius error over %d tensors: matrices %.2e, other tensors %.2e (theta, B); "
+          "%d flagged below resolution" % (len(sel), worst_iso, worst_avg, len(flagged)), flush=True)
+    assert len(flagged) <= max_flagged, flagged
+    if flagged:
+        print("below resolution (outside the contract): %s" % ", ".join(
+            "tensor %d theta %.2e B %.2e" % f for f in flagged), flush=True)
     if own:
         plan.close()
     if return_inputs:
@@ -131,7 +169,7 @@ def _check_polar_properties(lay, st, mom, theta_in, workers, alpha=1.0):
         assert asym <= TOL, (i, asym)
         assert lmin >= -TOL, (i, lmin)
         assert abs(sb - st[i].sigma_bar) <= TOL * st[i].sigma_bar, (i, sb, st[i].sigma_bar)
-        assert st[i].flags == 0 and 0 <= st[i].orth_resid <= TOL
+        assert st[i].flags & ~8 == 0 and 0 <= st[i].orth_resid <= TOL
     print("all matrices: max orth %.2e, max asym(Q^T Delta) %.2e, min eig %.2e" % tuple(worst), flush=True)
 
 
@@ -364,16 +402,86 @@ def _one_of_each_shape(lay):
     return sample
 
 
-def test_config2_full_size_sampled(iso):
-    """The 109.5M-parameter workload (K = 16, fp32 replicas) at full size in
-    the benchmark's launch configuration: every 1-D tensor and one tensor of
-    each 2-D shape against the oracle; the polar-factor properties for all 85
-    matrices."""
-    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+@pytest.mark.timeout(900)
+def test_config2_full_gate_two_steps(iso):
+    """The 109.5M-parameter workload (K = 16 fp32 replicas: 85 matrices, 24
+    vectors) at full size in the benchmark's launch configuration, every
+    tensor against the oracle, over two chained steps: step 1 from B = 0,
+    step 2 from the GPU's theta and B after step 1 (B != 0) with fresh
+    replicas, the oracle getting the same inputs (shared-input parity).
+    Matrices flagged below resolution are reported, at most 2 of the 170
+    (about 5e-4 of the square ones have a singular value there)."""
+    from workload import WORKLOADS, LLAMA_110M
     cfg = WORKLOADS[LLAMA_110M]
-    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
-                                                      return_inputs=True)
-    _check_polar_properties(cfg.layout, st, mom, th_in, workers)
+    dev = torch.device("cuda", 0)
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, iso.ISOLOCO_F32, device=dev)
+    theta, mom, st1 = _run_and_compare(iso, cfg, seed=0, step=1, plan=plan, spawned=True, max_flagged=2)
+    assert mom.abs().max().item() > 0
+    _, _, st2 = _run_and_compare(iso, cfg, seed=0, step=2, theta=theta, mom=mom, plan=plan, spawned=True,
+                                 max_flagged=2, check_q=False)
+    plan.close()
+    for st in (st1, st2):
+        hist = {}
+        for s_, t in zip(st, cfg.layout):
+            if t[3] == KIND_ISO:
+                hist[s_.steps] = hist.get(s_.steps, 0) + 1
+        print("matrices by polar steps:", dict(sorted(hist.items())), flush=True)
+
+
+def test_config2_embedding_excluded(iso):
+    """Section 4.5's ablation that leaves the embedding out of the correction:
+    the 109.5M workload with its tied 32000 x 768 embedding marked AVG (a 2-D
+    tensor that takes the plain mean and the momentum step).  The embedding,
+    every vector and one matrix of each corrected shape against the oracle."""
+    from workload import WORKLOADS, LLAMA_110M
+    import dataclasses
+    base = WORKLOADS[LLAMA_110M]
+    lay = [list(t) for t in base.layout]
+    emb = max(range(len(lay)), key=lambda i: lay[i][1] * lay[i][2])
+    assert (lay[emb][1], lay[emb][2]) == (32000, 768)
+    lay[emb][3] = KIND_AVG
+    cfg = dataclasses.replace(base, layout=[tuple(t) for t in lay])
+    sel = _one_of_each_shape(cfg.layout)
+    assert emb in sel
+    _, _, st = _run_and_compare(iso, cfg, select=sel, spawned=True)
+    assert st[emb].steps == 0 and st[emb].fro_norm == -1.0
+
+
+def test_not_converged_flag(iso):
+    """A step cap too short for the spectrum (max_steps = 3 on a 256 x 256
+    matrix with singular values spread over [1e-5, 1]): the not-converged
+    flag is set, with the residual get_stats reports, and theta and B stay
+    finite; a vector of the same step still matches the oracle."""
+    from workload import custom_layout
+    lay, n = custom_layout([(256, 256, KIND_ISO), (96, 1, KIND_AVG)], align=4)
+    rng = np.random.default_rng(21)
+    delta = np.zeros(n)
+    delta[:256 * 256] = (_planted(256, 256, 1e-5, rng) * 1e-3).reshape(-1)
+    delta[256 * 256:] = 1e-3 * rng.standard_normal(96)
+    dev = torch.device("cuda", 0)
+    theta = torch.zeros(n, dtype=torch.float32, device=dev)
+    mom = torch.zeros_like(theta)
+    w = torch.tensor(-delta, dtype=torch.float32, device=dev).reshape(1, n).contiguous()
+    print("case: max_steps = 3, planted [1e-5, 1] spectrum", flush=True)
+    plan = iso.IsoLoCoPlan(lay, n, 1, iso.ISOLOCO_F32, opts=dict(max_steps=3), device=dev)
+    plan.aggregate(theta, w, mom, 1.0, 0.7, 0.9)
+    torch.cuda.synchronize()
+    st = plan.stats()
+    plan.close()
+    print("steps %d resid %.3e flags %d" % (st[0].steps, st[0].orth_resid, st[0].flags), flush=True)
+    assert st[0].steps == 3
+    assert st[0].flags & iso.ISOLOCO_FLAG_NOT_CONVERGED
+    assert st[0].orth_resid > 1e-3
+    assert bool(torch.isfinite(theta).all()) and bool(torch.isfinite(mom).all())
+    # the residual reported is that of the factor written: B = sigma_bar Q
+    Q = mom[:256 * 256].double().reshape(256, 256) / st[0].sigma_bar
+    orth = (torch.linalg.norm(Q.T @ Q - torch.eye(256, dtype=Q.dtype, device=dev)) / 16.0).item()
+    assert abs(orth - st[0].orth_resid) <= 0.05 * orth, (orth, st[0].orth_resid)
+    ref = oracle_per_tensor(lay, np.zeros(n, np.float32), [w.cpu().numpy()[0]], np.zeros(n, np.float32),
+                            1.0, 0.7, 0.9, select=[1])
+    th_r, b_r, _ = ref[1]
+    sl = slice(lay[1][0], lay[1][0] + 96)
+    assert relF(theta[sl].cpu().numpy(), th_r) <= 1e-6 and relF(mom[sl].cpu().numpy(), b_r) <= 1e-6
 
 
 @pytest.mark.timeout(900)
@@ -385,20 +493,22 @@ def test_config3_full_size_sampled(iso):
     from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
     cfg = WORKLOADS[LLAMA_341M]
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
-                                                      return_inputs=True)
+                                                      return_inputs=True, max_flagged=1)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
 
 
 @pytest.mark.timeout(900)
 def test_config4_full_size_sampled(iso):
     """16 blocks d = 2048 / FFN 5632 + 32000 x 2048 (888M parameters), K = 64
-    bf16 replicas (114 GB in HBM): 1-D tensors and one square matrix against
-    the oracle, properties for all 113 matrices."""
+    bf16 replicas (114 GB in HBM): 1-D tensors, one square and one tall
+    matrix against the oracle, properties for all 113 matrices."""
     from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
     cfg = WORKLOADS[LLAMA_888M]
     sample = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_AVG]
-    sample.append(next(i for i, t in enumerate(cfg.layout) if (t[1], t[2]) == (2048, 2048)))
-    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True)
+    for shape in ((2048, 2048), (5632, 2048)):
+        sample.append(next(i for i, t in enumerate(cfg.layout) if (t[1], t[2]) == shape))
+    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True,
+                                                      max_flagged=1)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
 
 
@@ -472,11 +582,17 @@ def test_each_matrix_stops_after_the_phase_that_covers_it(iso):
     for i, (th_r, b_r, sb_r) in ref.items():
         off, rows, cols, kind = lay[i]
         e = relF(th[off:off + rows * cols], th_r)
-        print("tensor %d steps %d resid %.2e: theta %.2e" % (i, st[i].steps, st[i].orth_resid, e), flush=True)
-        assert e <= TOL and st[i].flags == 0
+        print("tensor %d steps %d resid %.2e flags %d: theta %.2e" % (i, st[i].steps, st[i].orth_resid,
+                                                                     st[i].flags, e), flush=True)
+        assert e <= TOL
         assert 0 <= st[i].orth_resid <= TOL
         assert abs(st[i].sigma_bar - sb_r) <= TOL * sb_r
     assert [s.steps for s in st] == [ends_tall[0], ends_tall[1], ends_tall[2], ends[0], ends[2]]
+    # the square matrix with an isolated singular value near 5e-9 of the
+    # normalisation fails the check after the phase for 2e-8: it is flagged
+    # below resolution (its Delta is exact here, so it still matches), the
+    # others are not flagged
+    assert [s.flags for s in st] == [0, 0, 0, 0, iso.ISOLOCO_FLAG_BELOW_RESOLUTION]
     plan.close()
 
 
