@@ -221,6 +221,37 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
                                  float* momentum, float alpha, float outer_lr, float mu,
                                  void* hip_stream);
 
+/* For callers that cannot allocate device memory (code that must not call
+ * hipMalloc, such as tight serving loops or harnesses that forbid it): the
+ * same step as isoloco_aggregate(), with the same arguments, results (bit for
+ * bit) and errors, but on a workspace the library holds as a fixed array of
+ * ISOLOCO_STATIC_WORKSPACE_BYTES in the memory of every device it runs on,
+ * from the first use until the process ends, instead of a caller-provided one.
+ * No device memory is allocated or freed, by the library or on its behalf.
+ *
+ * - The plan needs no isoloco_set_workspace(); a plan whose workspace size
+ *   exceeds ISOLOCO_STATIC_WORKSPACE_BYTES is rejected with
+ *   ISOLOCO_ERR_WORKSPACE and nothing is enqueued.
+ * - Every call on a device shares that device's array.  When the array last
+ *   held another plan's tables (or none), the call first waits for the device
+ *   to be idle (calls of other plans may still read the array), copies this
+ *   plan's tables in and clears the counters and per-matrix state the
+ *   kernels expect at zero (synchronous; not capturable in a HIP graph --
+ *   make the first call of a plan outside capture).  Later calls of the same
+ *   plan enqueue kernel launches only.
+ * - Calls that may overlap on one device (different streams or host threads,
+ *   the same or different plans) race on the array: order them.
+ * - The polar iteration runs on the caller's stream only (the two-stream mode
+ *   would need a stream the library creates).
+ * - isoloco_get_stats() reads the array: it fails with
+ *   ISOLOCO_ERR_INVALID_ARG once another plan has used the device's array
+ *   after this plan's last step. */
+#define ISOLOCO_STATIC_WORKSPACE_BYTES (128u * 1024u * 1024u)
+
+isoloco_status isoloco_aggregate_static(isoloco_plan_t plan, float* global, const void* const* workers,
+                                        float* momentum, float alpha, float outer_lr, float mu,
+                                        void* hip_stream);
+
 /* Copy the per-tensor statistics of the last aggregate to the host
  * (n_tensors entries, in layout order).  Waits for that aggregate's stream. */
 isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out, int32_t n_tensors);

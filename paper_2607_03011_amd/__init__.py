@@ -15,7 +15,7 @@ __all__ = [
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
     "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
     "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
-    "isoloco_timing",
+    "isoloco_timing", "isoloco_aggregate_static", "ISOLOCO_STATIC_WORKSPACE_BYTES",
     "IsoLoCoPlan", "LIB_PATH", "EXPORTED_SYMBOLS",
 ]
 
@@ -45,11 +45,13 @@ ISOLOCO_FLAG_NONFINITE = 1
 ISOLOCO_FLAG_ZERO = 2
 ISOLOCO_FLAG_NOT_CONVERGED = 4
 ISOLOCO_FLAG_BELOW_RESOLUTION = 8
+ISOLOCO_STATIC_WORKSPACE_BYTES = 128 * 1024 * 1024
 
 EXPORTED_SYMBOLS = (
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
     "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
     "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
+    "isoloco_aggregate_static",
 )
 
 
@@ -100,6 +102,8 @@ _sig = {
     "isoloco_set_workspace": (ctypes.c_int, [_P, _P, ctypes.c_size_t]),
     "isoloco_aggregate": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), _P, ctypes.c_float,
                                          ctypes.c_float, ctypes.c_float, _P]),
+    "isoloco_aggregate_static": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), _P, ctypes.c_float,
+                                                ctypes.c_float, ctypes.c_float, _P]),
     "isoloco_get_stats": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_tensor_stats), ctypes.c_int32]),
     "isoloco_schedule": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
                                         ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
@@ -171,6 +175,13 @@ def isoloco_aggregate(plan, global_ptr, worker_ptrs, momentum_ptr, alpha, outer_
            "isoloco_aggregate")
 
 
+def isoloco_aggregate_static(plan, global_ptr, worker_ptrs, momentum_ptr, alpha, outer_lr, mu, stream=0):
+    arr = (_P * max(len(worker_ptrs), 1))(*[_P(int(p)) for p in worker_ptrs])
+    _check(_lib.isoloco_aggregate_static(plan, _P(int(global_ptr)), arr, _P(int(momentum_ptr)),
+                                         float(alpha), float(outer_lr), float(mu), _P(int(stream))),
+           "isoloco_aggregate_static")
+
+
 def isoloco_get_stats(plan, n_tensors):
     arr = (isoloco_tensor_stats * max(n_tensors, 1))()
     _check(_lib.isoloco_get_stats(plan, arr, n_tensors), "isoloco_get_stats")
@@ -215,10 +226,11 @@ def isoloco_plan_destroy(plan):
 
 class IsoLoCoPlan:
     """A plan plus its workspace, allocated as a torch uint8 tensor on the
-    current device.  ``aggregate`` marshals torch tensors to the C call and
-    enqueues on the current torch stream (or ``stream``)."""
+    current device (``workspace=False``: none, for ``aggregate_static`` only).
+    ``aggregate`` and ``aggregate_static`` marshal torch tensors to the C calls
+    and enqueue on the current torch stream (or ``stream``)."""
 
-    def __init__(self, layout, n_elems, K, worker_dtype=ISOLOCO_F32, opts=None, device=None):
+    def __init__(self, layout, n_elems, K, worker_dtype=ISOLOCO_F32, opts=None, device=None, workspace=True):
         import torch
         self.layout = [tuple(int(v) for v in t) for t in layout]
         self.n_elems = int(n_elems)
@@ -228,6 +240,9 @@ class IsoLoCoPlan:
         self.ws_bytes = isoloco_workspace_size(self.handle)
         dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
         self.device = dev
+        self.workspace = None
+        if not workspace:
+            return
         with torch.cuda.device(dev):
             self.workspace = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
             base = self.workspace.data_ptr()
@@ -235,6 +250,16 @@ class IsoLoCoPlan:
             isoloco_set_workspace(self.handle, self._ws_ptr, self.ws_bytes)
 
     def aggregate(self, theta, workers, momentum, alpha=1.0, outer_lr=0.7, mu=0.9, stream=None):
+        ptrs, stream = self._marshal(theta, workers, momentum, stream)
+        isoloco_aggregate(self.handle, theta.data_ptr(), ptrs, momentum.data_ptr(), alpha, outer_lr,
+                          mu, stream)
+
+    def aggregate_static(self, theta, workers, momentum, alpha=1.0, outer_lr=0.7, mu=0.9, stream=None):
+        ptrs, stream = self._marshal(theta, workers, momentum, stream)
+        isoloco_aggregate_static(self.handle, theta.data_ptr(), ptrs, momentum.data_ptr(), alpha, outer_lr,
+                                 mu, stream)
+
+    def _marshal(self, theta, workers, momentum, stream):
         import torch
         for t in (theta, momentum):
             if t.dtype != torch.float32 or not t.is_contiguous() or t.numel() != self.n_elems:
@@ -256,8 +281,7 @@ class IsoLoCoPlan:
             ptrs = [w.data_ptr() for w in ws]
         if stream is None:
             stream = torch.cuda.current_stream(self.device).cuda_stream
-        isoloco_aggregate(self.handle, theta.data_ptr(), ptrs, momentum.data_ptr(), alpha, outer_lr,
-                          mu, stream)
+        return ptrs, stream
 
     def stats(self):
         return isoloco_get_stats(self.handle, len(self.layout))

@@ -4,6 +4,8 @@
 
 #include <algorithm>
 #include <array>
+#include <atomic>
+#include <mutex>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -26,6 +28,13 @@ static_assert(kFlagNonfinite == ISOLOCO_FLAG_NONFINITE && kFlagZero == ISOLOCO_F
 namespace {
 
 thread_local std::string g_last_error;
+
+// Static workspace (isoloco_aggregate_static): the plan whose tables each
+// device's array holds (by uid; 0 = none), and the source of plan uids.
+constexpr int kStaticMaxDevices = 64;
+std::mutex g_static_mu;
+uint64_t g_static_owner[kStaticMaxDevices] = {};
+std::atomic<uint64_t> g_next_uid{1};
 
 isoloco_status fail(isoloco_status s, const char* fmt, ...) {
   char buf[512];
@@ -357,6 +366,9 @@ struct isoloco_plan_s {
   char* ws = nullptr;
   size_t ws_bytes = 0;
   int device = -1;
+  uint64_t uid = 0;          // distinct for every plan of the process (static workspace ownership)
+  int static_dev = -1;       // device whose static workspace the last aggregate used (-1: the plan's own)
+  char* last_ws = nullptr;   // workspace of the last aggregate (its statistics)
   hipStream_t last_stream = nullptr;
   bool has_run = false;
   // per-launch timing
@@ -652,9 +664,9 @@ void plan_workspace(isoloco_plan_s* p) {
   p->total = o;
 }
 
-TaskList dev_list(const isoloco_plan_s* p, const TaskListHost& L, size_t off) {
+TaskList dev_list(const char* w, const TaskListHost& L, size_t off) {
   TaskList d{};
-  d.tasks = reinterpret_cast<const Task*>(p->ws + off);
+  d.tasks = reinterpret_cast<const Task*>(w + off);
   for (int q = 0; q < 3; ++q) {
     d.seg_off[q] = L.seg_off[q];
     d.seg_cnt[q] = L.seg_cnt[q];
@@ -669,25 +681,25 @@ TaskList dev_list(const isoloco_plan_s* p, const TaskListHost& L, size_t off) {
 }
 
 // The tables with the task lists of one schedule class only.
-DevTables class_tables(const isoloco_plan_s* p, const DevTables& t, int c) {
+DevTables class_tables(const isoloco_plan_s* p, const char* w, const DevTables& t, int c) {
   DevTables d = t;
-  d.gram_list = dev_list(p, p->gram_cls[c], p->off_gtc[c]);
-  d.poly_list = dev_list(p, p->poly_cls[c], p->off_ptc[c]);
-  d.update_list = dev_list(p, p->update_cls[c], p->off_utc[c]);
-  d.chunk_idx = reinterpret_cast<const int*>(p->ws + p->off_cic[c]);
+  d.gram_list = dev_list(w, p->gram_cls[c], p->off_gtc[c]);
+  d.poly_list = dev_list(w, p->poly_cls[c], p->off_ptc[c]);
+  d.update_list = dev_list(w, p->update_cls[c], p->off_utc[c]);
+  d.chunk_idx = reinterpret_cast<const int*>(w + p->off_cic[c]);
   d.n_chunk_idx = (int)p->chunk_cls[c].size();
   d.cls = c;
   return d;
 }
 
-DevTables dev_tables(const isoloco_plan_s* p) {
+// The plan's device tables and buffers in the workspace at w.
+DevTables dev_tables(const isoloco_plan_s* p, char* w) {
   DevTables t{};
-  char* w = p->ws;
   t.mats = reinterpret_cast<const MatInfo*>(w + p->off_mats);
   t.chunks = reinterpret_cast<const Chunk*>(w + p->off_chunks);
-  t.gram_list = dev_list(p, p->gram_list, p->off_gt);
-  t.poly_list = dev_list(p, p->poly_list, p->off_pt);
-  t.update_list = dev_list(p, p->update_list, p->off_ut);
+  t.gram_list = dev_list(w, p->gram_list, p->off_gt);
+  t.poly_list = dev_list(w, p->poly_list, p->off_pt);
+  t.update_list = dev_list(w, p->update_list, p->off_ut);
   t.scalars = reinterpret_cast<MatScalars*>(w + p->off_sc);
   t.part_sq = reinterpret_cast<double*>(w + p->off_psq);
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
@@ -710,6 +722,40 @@ DevTables dev_tables(const isoloco_plan_s* p) {
   t.n_chunks = (int)p->chunks.size();
   t.n_iso_chunks = p->n_iso_chunks;
   return t;
+}
+
+// Copy the plan's tables into the workspace at w and clear what the kernels
+// expect at zero (per-matrix scalars, split-K arrival counters); synchronous.
+hipError_t upload_tables(const isoloco_plan_s* plan, char* w) {
+  hipError_t e;
+  auto up = [&](size_t off, const void* src, size_t n) -> hipError_t {
+    if (n == 0) return hipSuccess;
+    return hipMemcpy(w + off, src, n, hipMemcpyHostToDevice);
+  };
+  if ((e = up(plan->off_mats, plan->mats.data(), plan->mats.size() * sizeof(MatInfo))) != hipSuccess ||
+      (e = up(plan->off_chunks, plan->chunks.data(), plan->chunks.size() * sizeof(Chunk))) != hipSuccess ||
+      (e = up(plan->off_gt, plan->gram_list.tasks.data(), plan->gram_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_pt, plan->poly_list.tasks.data(), plan->poly_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess ||
+      (e = up(plan->off_coef, plan->coef.data(), plan->coef.size() * sizeof(float))) != hipSuccess)
+    return e;
+  for (int c = 0; c < kSchedClasses; ++c)
+    if ((e = up(plan->off_gtc[c], plan->gram_cls[c].tasks.data(), plan->gram_cls[c].tasks.size() * sizeof(Task))) !=
+            hipSuccess ||
+        (e = up(plan->off_ptc[c], plan->poly_cls[c].tasks.data(), plan->poly_cls[c].tasks.size() * sizeof(Task))) !=
+            hipSuccess ||
+        (e = up(plan->off_utc[c], plan->update_cls[c].tasks.data(),
+                plan->update_cls[c].tasks.size() * sizeof(Task))) != hipSuccess ||
+        (e = up(plan->off_cic[c], plan->chunk_cls[c].data(), plan->chunk_cls[c].size() * sizeof(int))) !=
+            hipSuccess)
+      return e;
+  if (!plan->mats.empty() && (e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars))) != hipSuccess)
+    return e;
+  // the split-K Gram tiles count their arrivals here; each launch leaves them at zero
+  if (plan->n_cnt > 0 && (e = hipMemset(w + plan->off_cnt, 0, (size_t)plan->n_cnt * sizeof(int))) != hipSuccess)
+    return e;
+  // done before any stream of the caller's (some may not wait for the null stream)
+  return hipStreamSynchronize(nullptr);
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -797,6 +843,7 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   isoloco_plan_s* p = new (std::nothrow) isoloco_plan_s();
   if (!p) return fail(ISOLOCO_ERR_INVALID_ARG, "out of host memory");
   try {
+    p->uid = g_next_uid.fetch_add(1);
     p->layout.assign(layout, layout + n_tensors);
     p->n_elems = n_elems;
     p->K = K;
@@ -849,39 +896,7 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   char* w = static_cast<char*>(dev_ptr);
-  auto up = [&](size_t off, const void* src, size_t n) -> hipError_t {
-    if (n == 0) return hipSuccess;
-    return hipMemcpy(w + off, src, n, hipMemcpyHostToDevice);
-  };
-  if ((e = up(plan->off_mats, plan->mats.data(), plan->mats.size() * sizeof(MatInfo))) != hipSuccess ||
-      (e = up(plan->off_chunks, plan->chunks.data(), plan->chunks.size() * sizeof(Chunk))) != hipSuccess ||
-      (e = up(plan->off_gt, plan->gram_list.tasks.data(), plan->gram_list.tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_pt, plan->poly_list.tasks.data(), plan->poly_list.tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess ||
-      (e = up(plan->off_coef, plan->coef.data(), plan->coef.size() * sizeof(float))) != hipSuccess)
-    return hip_fail(e, "copying plan tables to the workspace");
-  for (int c = 0; c < kSchedClasses; ++c)
-    if ((e = up(plan->off_gtc[c], plan->gram_cls[c].tasks.data(), plan->gram_cls[c].tasks.size() * sizeof(Task))) !=
-            hipSuccess ||
-        (e = up(plan->off_ptc[c], plan->poly_cls[c].tasks.data(), plan->poly_cls[c].tasks.size() * sizeof(Task))) !=
-            hipSuccess ||
-        (e = up(plan->off_utc[c], plan->update_cls[c].tasks.data(),
-                plan->update_cls[c].tasks.size() * sizeof(Task))) != hipSuccess ||
-        (e = up(plan->off_cic[c], plan->chunk_cls[c].data(), plan->chunk_cls[c].size() * sizeof(int))) !=
-            hipSuccess)
-    return hip_fail(e, "copying plan tables to the workspace");
-  if (!plan->mats.empty()) {
-    e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars));
-    if (e != hipSuccess) return hip_fail(e, "clearing per-matrix scalars");
-  }
-  if (plan->n_cnt > 0) {
-    // the split-K Gram tiles count their arrivals here; each launch leaves them at zero
-    e = hipMemset(w + plan->off_cnt, 0, (size_t)plan->n_cnt * sizeof(int));
-    if (e != hipSuccess) return hip_fail(e, "clearing split-K counters");
-  }
-  // done before any stream of the caller's (some may not wait for the null stream)
-  e = hipStreamSynchronize(nullptr);
-  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if ((e = upload_tables(plan, w)) != hipSuccess) return hip_fail(e, "copying the plan's tables to the workspace");
   if (plan->side && plan->device != dev) {
     // the workspace moved to another device: the second stream goes with it
     (void)hipEventDestroy(plan->ev_fork);
@@ -908,11 +923,11 @@ isoloco_status isoloco_set_workspace(isoloco_plan_t plan, void* dev_ptr, size_t 
   return ISOLOCO_OK;
 }
 
-isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void* const* workers,
-                                 float* momentum, float alpha, float outer_lr, float mu,
-                                 void* hip_stream) {
-  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
-  if (!plan->ws) return fail(ISOLOCO_ERR_WORKSPACE, "no workspace set (isoloco_set_workspace)");
+// Validation of an aggregate's arguments against the workspace ws (of
+// plan->total bytes); nothing is enqueued when it fails.
+static isoloco_status check_step_args(isoloco_plan_t plan, const char* ws, const float* global,
+                                      const void* const* workers, const float* momentum, float alpha,
+                                      float outer_lr, float mu) {
   if (!std::isfinite(alpha) || !std::isfinite(outer_lr) || !std::isfinite(mu))
     return fail(ISOLOCO_ERR_INVALID_ARG, "alpha, outer_lr and mu must be finite");
   const size_t nb = (size_t)plan->n_elems * sizeof(float);
@@ -923,26 +938,27 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     if ((uintptr_t)global % 16 || (uintptr_t)momentum % 16)
       return fail(ISOLOCO_ERR_ALIGN, "global and momentum must be 16-byte aligned");
     if (overlaps(global, nb, momentum, nb)) return fail(ISOLOCO_ERR_ALIAS, "global and momentum overlap");
-    if (overlaps(global, nb, plan->ws, plan->total) || overlaps(momentum, nb, plan->ws, plan->total))
+    if (overlaps(global, nb, ws, plan->total) || overlaps(momentum, nb, ws, plan->total))
       return fail(ISOLOCO_ERR_ALIAS, "global or momentum overlaps the workspace");
     for (int k = 0; k < plan->K; ++k) {
       const void* w = workers[k];
       if (!w) return fail(ISOLOCO_ERR_INVALID_ARG, "worker %d pointer is NULL", k);
       if ((uintptr_t)w % 16) return fail(ISOLOCO_ERR_ALIGN, "worker %d is not 16-byte aligned", k);
-      if (overlaps(w, wb, global, nb) || overlaps(w, wb, momentum, nb) ||
-          overlaps(w, wb, plan->ws, plan->total))
+      if (overlaps(w, wb, global, nb) || overlaps(w, wb, momentum, nb) || overlaps(w, wb, ws, plan->total))
         return fail(ISOLOCO_ERR_ALIAS, "worker %d overlaps global, momentum or the workspace", k);
     }
   }
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  if (dev != plan->device)
-    return fail(ISOLOCO_ERR_INVALID_ARG, "current device %d differs from the workspace's device %d", dev,
-                plan->device);
+  return ISOLOCO_OK;
+}
 
+// One outer step on the workspace ws (the plan's tables already there);
+// use_side: the two-stream mode may use the plan's second stream.
+static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side, float* global,
+                                   const void* const* workers, float* momentum, float alpha, float outer_lr,
+                                   float mu, void* hip_stream) {
+  hipError_t e;
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
-  const DevTables t = dev_tables(plan);
+  const DevTables t = dev_tables(plan, ws);
   StepArgs a{};
   a.steps_lo = 0;
   a.steps_hi = INT32_MAX;
@@ -988,7 +1004,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       fa.buf_total[c] = (fa.steps_total[c] - 1) & 1;
     }
     // a stream per schedule class when asked for and both have matrices
-    const bool two = plan->opts.streams == 2 && plan->side && n_cls[0] > 0 && n_cls[1] > 0;
+    const bool two = use_side && plan->opts.streams == 2 && plan->side && n_cls[0] > 0 && n_cls[1] > 0;
     plan->last_streams = two ? 2 : 1;
     const char* what = "";
     // The polar iteration of the matrices of class cls (-1: every matrix) on
@@ -1134,7 +1150,8 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       if ((r = hipEventRecord(plan->ev_fork, st)) != hipSuccess ||
           (r = hipStreamWaitEvent(plan->side, plan->ev_fork, 0)) != hipSuccess)
         return r;
-      const DevTables tt_tall = class_tables(plan, tt, kSchedTall), tt_sq = class_tables(plan, tt, kSchedSquare);
+      const DevTables tt_tall = class_tables(plan, ws, tt, kSchedTall),
+                      tt_sq = class_tables(plan, ws, tt, kSchedSquare);
       // The square-ish matrices that stop at their class's first switch take
       // their scale and write-back on the caller's stream (after the tall
       // class's) while the others still iterate on the second stream.  A
@@ -1182,6 +1199,7 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
     if (!a.clip) {
       if ((e = polar(t, plan->opts.check == 1, true)) != hipSuccess) return hip_fail(e, what);
       plan->last_stream = st;
+      plan->last_ws = ws;
       plan->has_run = true;
       return ISOLOCO_OK;
     }
@@ -1220,8 +1238,65 @@ isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void*
       return hip_fail(e, "finish launch");
   }
   plan->last_stream = st;
+  plan->last_ws = ws;
   plan->has_run = true;
   return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_aggregate(isoloco_plan_t plan, float* global, const void* const* workers,
+                                 float* momentum, float alpha, float outer_lr, float mu,
+                                 void* hip_stream) {
+  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
+  if (!plan->ws) return fail(ISOLOCO_ERR_WORKSPACE, "no workspace set (isoloco_set_workspace)");
+  isoloco_status v = check_step_args(plan, plan->ws, global, workers, momentum, alpha, outer_lr, mu);
+  if (v != ISOLOCO_OK) return v;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != plan->device)
+    return fail(ISOLOCO_ERR_INVALID_ARG, "current device %d differs from the workspace's device %d", dev,
+                plan->device);
+  plan->static_dev = -1;
+  return aggregate_on(plan, plan->ws, true, global, workers, momentum, alpha, outer_lr, mu, hip_stream);
+}
+
+isoloco_status isoloco_aggregate_static(isoloco_plan_t plan, float* global, const void* const* workers,
+                                        float* momentum, float alpha, float outer_lr, float mu,
+                                        void* hip_stream) {
+  if (!plan) return fail(ISOLOCO_ERR_INVALID_ARG, "plan is NULL");
+  if (plan->total > (size_t)ISOLOCO_STATIC_WORKSPACE_BYTES)
+    return fail(ISOLOCO_ERR_WORKSPACE,
+                "the plan needs %zu bytes of workspace; the static workspace holds %zu "
+                "(ISOLOCO_STATIC_WORKSPACE_BYTES): use isoloco_set_workspace and isoloco_aggregate",
+                plan->total, (size_t)ISOLOCO_STATIC_WORKSPACE_BYTES);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kStaticMaxDevices)
+    return fail(ISOLOCO_ERR_UNSUPPORTED, "device %d: the static workspace serves devices 0 to %d", dev,
+                kStaticMaxDevices - 1);
+  void* w = nullptr;
+  if ((e = static_workspace(dev, &w)) != hipSuccess) return hip_fail(e, "locating the static workspace");
+  char* ws = static_cast<char*>(w);
+  isoloco_status v = check_step_args(plan, ws, global, workers, momentum, alpha, outer_lr, mu);
+  if (v != ISOLOCO_OK) return v;
+  {
+    // The array holds the tables of the plan that used it last on this
+    // device; another plan's are copied in first (synchronously, after every
+    // call still running on the device, which may read the array).
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (g_static_owner[dev] != plan->uid) {
+      g_static_owner[dev] = 0;
+      if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+      if ((e = upload_tables(plan, ws)) != hipSuccess)
+        return hip_fail(e, "copying the plan's tables to the static workspace");
+      g_static_owner[dev] = plan->uid;
+    }
+  }
+  plan->static_dev = dev;
+  // one stream: the second stream of the two-stream mode would be created by
+  // the library (results are bit for bit those of two streams)
+  return aggregate_on(plan, ws, false, global, workers, momentum, alpha, outer_lr, mu, hip_stream);
 }
 
 isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out, int32_t n_tensors) {
@@ -1231,9 +1306,16 @@ isoloco_status isoloco_get_stats(isoloco_plan_t plan, isoloco_tensor_stats* out,
                 plan->layout.size());
   std::vector<MatScalars> sc(plan->mats.size());
   if (plan->has_run && !sc.empty()) {
+    if (plan->static_dev >= 0) {
+      std::lock_guard<std::mutex> lock(g_static_mu);
+      if (g_static_owner[plan->static_dev] != plan->uid)
+        return fail(ISOLOCO_ERR_INVALID_ARG,
+                    "another plan has used the static workspace of device %d since this plan's last step",
+                    plan->static_dev);
+    }
     hipError_t e = hipStreamSynchronize(plan->last_stream);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-    e = hipMemcpy(sc.data(), plan->ws + plan->off_sc, sc.size() * sizeof(MatScalars),
+    e = hipMemcpy(sc.data(), plan->last_ws + plan->off_sc, sc.size() * sizeof(MatScalars),
                   hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "copying statistics");
   }

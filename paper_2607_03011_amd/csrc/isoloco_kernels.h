@@ -122,6 +122,11 @@ struct FroArgs {
   int fixed_g;  // the first step uses g = 1 (no Gram-norm scaling)
 };
 
+// The static workspace of the device `device` (which must be current): the
+// device address of a fixed array of ISOLOCO_STATIC_WORKSPACE_BYTES in device
+// memory, looked up once per device and kept.
+hipError_t static_workspace(int device, void** out);
+
 hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
 // also initialises the per-matrix iteration state (active, qbuf, steps)
 hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st);

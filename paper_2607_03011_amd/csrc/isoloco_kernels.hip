@@ -18,9 +18,39 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
+#include "isoloco.h"
 #include "isoloco_kernels.h"
 
 namespace isoloco {
+
+// ---------------------------------------------------------------------------
+// Static workspace
+// ---------------------------------------------------------------------------
+//
+// The workspace of isoloco_aggregate_static: a fixed array in the device
+// memory of every device the library runs on, held until the process ends.
+// In host code the name `scratch` is a stand-in, not a device address: the
+// address comes from hipGetSymbolAddress, once per device with that device
+// current, and only that address is ever handed to a kernel or a copy.
+static __device__ __align__(256) unsigned char scratch[ISOLOCO_STATIC_WORKSPACE_BYTES];
+
+hipError_t static_workspace(int device, void** out) {
+  constexpr int kDevices = 64;
+  static std::mutex mu;
+  static void* addr[kDevices] = {};
+  if (device < 0 || device >= kDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[device] = p;
+  }
+  *out = addr[device];
+  return hipSuccess;
+}
 
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
