@@ -132,6 +132,26 @@ def copy_ceiling_gbs(torch, dev, nbytes, reps=5):
     return 8.0 * n / (best * 1e-3) / 1e9
 
 
+def worker_sum_ceiling_gbs(torch, workers, reps=5):
+    """Bandwidth of torch.sum over the worker dimension of the [K, n] replicas
+    (the reduction's reads and the write of one n-vector, no other
+    arithmetic), timed with events on the current stream: the best of `reps`,
+    in GB/s."""
+    out = torch.empty(workers.shape[1], dtype=torch.float32, device=workers.device)
+    nbytes = workers.numel() * workers.element_size() + out.numel() * 4
+    torch.sum(workers, dim=0, dtype=torch.float32, out=out)
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.sum(workers, dim=0, dtype=torch.float32, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del out
+    return nbytes / (best * 1e-3) / 1e9
+
+
 def cpu_baseline(cfg, theta, workers, mom, budget_s, variant=None):
     """The float64 oracle timed on the host on a bounded sample of the step:
     all 1-D tensors plus one tensor of each 2-D shape, extrapolated to the whole
@@ -314,6 +334,7 @@ def main():
     rbytes = reduce_bytes(cfg.layout, cfg.n_elems, cfg.K, wbytes)
     red_gbs = rbytes / (per["reduce_ms"] * 1e-3) / 1e9
     copy_gbs = copy_ceiling_gbs(torch, dev, rbytes)
+    sum_gbs = worker_sum_ceiling_gbs(torch, workers)
     fbytes = finish_bytes(cfg.layout)
     fin_gbs = fbytes / (per["finish_ms"] * 1e-3) / 1e9
     gbytes = gemm_bytes_per_step(cfg.layout, st)
@@ -365,7 +386,12 @@ def main():
                             "copy_ceiling_gbs": round(copy_gbs, 1),
                             "frac_of_copy_ceiling": round(red_gbs / copy_gbs, 4),
                             "copy_ceiling_note": "same run: a device-to-device copy moving the same bytes "
-                                                 "(half read, half written), best of 5"},
+                                                 "(half read, half written), best of 5",
+                            "worker_sum_ceiling_gbs": round(sum_gbs, 1),
+                            "frac_of_worker_sum_ceiling": round(red_gbs / sum_gbs, 4),
+                            "worker_sum_ceiling_note": "same run: torch.sum of the K replicas over the worker "
+                                                       "dimension (the reduction's reads, one vector written), "
+                                                       "best of 5"},
         "roofline_finish": {"bound": "hbm", "kernel": "finish_kernel", "achieved": round(fin_gbs, 1),
                             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(fin_gbs / PEAK_HBM_GBS, 4),
                             "traffic": mt["finish_bytes_per_step"] if measured else None,

@@ -86,6 +86,18 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
 
+// Word 3 of a raw buffer resource on CDNA3/CDNA4 (32-bit data format, no
+// swizzle; the range check compares byte offsets with the record count).
+constexpr int kBufferFlags = 0x00020000;
+// Cache policy of the buffer loads of data read once (the "nt" bit).
+constexpr int kStreamed = 2;
+
+// A buffer resource over `bytes` bytes from p: loads at byte offsets at or
+// past `bytes` return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stream_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufferFlags);
+}
+
 // ---------------------------------------------------------------------------
 // K-way reduction
 // ---------------------------------------------------------------------------
@@ -96,6 +108,16 @@ struct WorkerLoad;
 template <>
 struct WorkerLoad<0> {
   static constexpr int kVec = 4;  // elements per 16-byte access
+  static constexpr int kBytes = 4;
+  // 16 bytes at byte offset voff + soff of a stream
+  __device__ static __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, kStreamed));
+  }
+  // the 16 bytes of elements i .. i + kVec - 1, undecoded
+  __device__ static __forceinline__ u32x4 raw(const void* p, int64_t i) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const float*>(p) + i));
+  }
+  __device__ static __forceinline__ float decode(const u32x4& v, int r) { return __uint_as_float(v[r]); }
   __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
     // replicas are read once: non-temporal loads keep them from displacing cached data
     const floatx4 v = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(static_cast<const float*>(p) + i));
@@ -105,11 +127,29 @@ struct WorkerLoad<0> {
     return static_cast<const float*>(p)[i];
   }
   __device__ static __forceinline__ void quad(const void* p, int64_t i, float* out) { vec(p, i, out); }
+  // four elements, undecoded (16 bytes)
+  typedef u32x4 Quad;
+  __device__ static __forceinline__ Quad load_quad(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return load16(r, voff, soff);
+  }
+  __device__ static __forceinline__ Quad raw_quad(const void* p, int64_t i) { return raw(p, i); }
+  __device__ static __forceinline__ float decode_quad(const Quad& v, int r) { return __uint_as_float(v[r]); }
 };
 
 template <>
 struct WorkerLoad<1> {
   static constexpr int kVec = 8;
+  static constexpr int kBytes = 2;
+  __device__ static __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, kStreamed));
+  }
+  __device__ static __forceinline__ u32x4 raw(const void* p, int64_t i) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p) + i));
+  }
+  // element r of the 8 bfloat16 values in v
+  __device__ static __forceinline__ float decode(const u32x4& v, int r) {
+    return (r & 1) ? __uint_as_float(v[r >> 1] & 0xffff0000u) : __uint_as_float(v[r >> 1] << 16);
+  }
   __device__ static __forceinline__ void vec(const void* p, int64_t i, float* out) {
     const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p) + i));
     const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
@@ -121,6 +161,17 @@ struct WorkerLoad<1> {
   }
   __device__ static __forceinline__ float one(const void* p, int64_t i) {
     return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+  }
+  // four elements, undecoded (8 bytes)
+  typedef u32x2 Quad;
+  __device__ static __forceinline__ Quad load_quad(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, kStreamed));
+  }
+  __device__ static __forceinline__ Quad raw_quad(const void* p, int64_t i) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(static_cast<const uint16_t*>(p) + i));
+  }
+  __device__ static __forceinline__ float decode_quad(const Quad& v, int r) {
+    return (r & 1) ? __uint_as_float(v[r >> 1] & 0xffff0000u) : __uint_as_float(v[r >> 1] << 16);
   }
   // four elements (8 bytes)
   __device__ static __forceinline__ void quad(const void* p, int64_t i, float* out) {
@@ -142,57 +193,121 @@ __device__ __forceinline__ int64_t chunk_ws(const Chunk& c, int i) {
 // the banks.
 typedef float TileLds[kTileRows][kTileCols + 1];
 
-// Delta of a tile of a tall row-major tensor, written column-major: each
-// thread reduces 4 consecutive stored elements of a row (a wave covers two
-// rows of 128 columns), the tile goes through LDS, and each thread writes 4
-// consecutive rows of a column (eight threads per 128-byte column segment).
-// Returns the thread's share of sum Delta^2.
+// The replicas are streamed once, and the writes are what costs: the same
+// loads with a store per 16-byte group run at 5.5 TB/s, the whole chunk held
+// in registers and written at its end at 5.9 TB/s (probe on the 109.5M
+// workload's bytes; reads alone reach 7.0 TB/s).  So every thread holds
+// kSlots groups of its workgroup's chunk, walks the workers in groups whose
+// loads are all in flight together (16 loads of 16 bytes per thread), and
+// stores after the last worker, with non-temporal stores for Delta (read
+// back only by the next kernels, from HBM).  Each element still sums
+// theta - theta_k in worker order.
 template <int WDT>
+struct ReduceShape {
+  static constexpr int kVec = WorkerLoad<WDT>::kVec;                    // elements per 16-byte load
+  static constexpr int kSlots = kChunk / (kStreamThreads * kVec);       // 4 (fp32) or 2 (bf16)
+  static constexpr int kGroup = 16 / kSlots;                            // workers per group
+};
+
+// Delta of a tile of a tall row-major tensor, written column-major: each
+// thread reduces 8 groups of 4 consecutive stored elements of a row (a wave
+// covers one row of 256 columns per group), the tile goes through LDS, and
+// each thread writes 4 consecutive rows of a column (eight threads per
+// 128-byte column segment).  Returns the thread's share of sum Delta^2.
+// FULL: a whole kTileRows x kTileCols tile (no load needs a predicate).
+template <int WDT, bool FULL>
 __device__ __forceinline__ double reduce_tile(const Chunk& c, const float* __restrict__ theta,
                                               float* __restrict__ mom, float* __restrict__ delta,
                                               const WorkerPtrs& w, int K, float inv_k, float mu, int heavy_ball,
                                               int target_update, TileLds& tl) {
   using WL = WorkerLoad<WDT>;
+  constexpr int S = kTileRows * (kTileCols / 4) / kStreamThreads;  // groups of 4 per thread
+  constexpr int G = (WDT == 0 ? 16 : 32) / S;  // workers in flight: 256 bytes of loads per thread
   const int TR = c.rows, TC = c.cols;
   double sq = 0.0;
-  for (int it = threadIdx.x; it < TR * (kTileCols / 4); it += kStreamThreads) {
-    const int rr = it / (kTileCols / 4), col = 4 * (it % (kTileCols / 4));
-    if (col >= TC) continue;
-    const int64_t e = c.src + (int64_t)rr * c.src_ld + col;
-    const int nq = min(4, TC - col);
-    float acc[4] = {0.f, 0.f, 0.f, 0.f}, th[4] = {0.f, 0.f, 0.f, 0.f};
-    if (c.vec) {
-      const floatx4 t4 = *reinterpret_cast<const floatx4*>(theta + e);
-      th[0] = t4[0]; th[1] = t4[1]; th[2] = t4[2]; th[3] = t4[3];
-#pragma unroll 1
-      for (int k0 = 0; k0 < K; k0 += 8) {
-        float wv[8][4];
+  if (c.vec) {
+    // thread t: quad column 4 (t % 32) of rows t / 32 + 8 q (one 32-bit lane
+    // offset for every slot and stream; the slot's row step is a scalar
+    // offset); loads past the tile's span return zero, so none needs a
+    // predicate (quads right of a narrower tile read the tensor's next row
+    // and are not used)
+    constexpr int kRowsPerSlot = kStreamThreads / (kTileCols / 4);
+    const int r0 = threadIdx.x / (kTileCols / 4), col = 4 * (threadIdx.x % (kTileCols / 4));
+    const uint32_t span = (uint32_t)((TR - 1) * c.src_ld + TC);
+    const uint32_t lane = (uint32_t)(r0 * c.src_ld + col);
+    const uint32_t step = (uint32_t)(kRowsPerSlot * c.src_ld);
+    bool on[S];
+    float th[S][4], acc[S][4];
+    const __amdgpu_buffer_rsrc_t rt = stream_rsrc(theta + c.src, 4 * span);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (k0 + j < K) WL::quad(w.p[k0 + j], e, wv[j]);
+    for (int q = 0; q < S; ++q) {
+      on[q] = FULL || (r0 + kRowsPerSlot * q < TR && col < TC);
+      const floatx4 t4 = __builtin_bit_cast(floatx4, WorkerLoad<0>::load16(rt, 4 * lane, 4 * step * q));
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (k0 + j < K) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) acc[q] += th[q] - wv[j][q];
-          }
-      }
-    } else {
-      for (int q = 0; q < nq; ++q) {
-        th[q] = theta[e + q];
-        for (int k = 0; k < K; ++k) acc[q] += th[q] - WL::one(w.p[k], e + q);
+      for (int r = 0; r < 4; ++r) {
+        th[q][r] = t4[r];
+        acc[q][r] = 0.f;
       }
     }
-    for (int q = 0; q < nq; ++q) {
-      float a = acc[q] * inv_k;
-      if (target_update) {
-        // B <- mu B + Delta now; the polar input is the update itself
-        const float bn = mu * mom[e + q] + a;
-        mom[e + q] = bn;
-        a = heavy_ball ? bn : a + mu * bn;
+#pragma unroll 1
+    for (int k0 = 0; k0 < K; k0 += G) {
+      // (a last group past K loads worker K - 1 again and does not add it)
+      __amdgpu_buffer_rsrc_t rw[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+        rw[j] = stream_rsrc(static_cast<const char*>(w.p[min(k0 + j, K - 1)]) + WL::kBytes * c.src,
+                            WL::kBytes * span);
+      typename WL::Quad wv[G][S];
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+#pragma unroll
+        for (int q = 0; q < S; ++q) wv[j][q] = WL::load_quad(rw[j], WL::kBytes * lane, WL::kBytes * step * q);
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+        if (k0 + j < K) {
+#pragma unroll
+          for (int q = 0; q < S; ++q)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[q][r] += th[q][r] - WL::decode_quad(wv[j][q], r);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+      if (!on[q]) continue;
+      const int rr = r0 + kRowsPerSlot * q;
+      const int64_t e = c.src + (int64_t)rr * c.src_ld + col;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float a = acc[q][r] * inv_k;
+        if (target_update) {
+          // B <- mu B + Delta now; the polar input is the update itself
+          const float bn = mu * mom[e + r] + a;
+          mom[e + r] = bn;
+          a = heavy_ball ? bn : a + mu * bn;
+        }
+        tl[rr][col + r] = a;
+        sq += (double)a * a;
       }
-      tl[rr][col + q] = a;
-      sq += (double)a * a;
+    }
+  } else {
+    for (int it = threadIdx.x; it < TR * (kTileCols / 4); it += kStreamThreads) {
+      const int rr = it / (kTileCols / 4), col = 4 * (it % (kTileCols / 4));
+      if (col >= TC) continue;
+      const int64_t e = c.src + (int64_t)rr * c.src_ld + col;
+      const int nq = min(4, TC - col);
+      for (int q = 0; q < nq; ++q) {
+        const float th = theta[e + q];
+        float acc = 0.f;
+        for (int k = 0; k < K; ++k) acc += th - WL::one(w.p[k], e + q);
+        float a = acc * inv_k;
+        if (target_update) {
+          const float bn = mu * mom[e + q] + a;
+          mom[e + q] = bn;
+          a = heavy_ball ? bn : a + mu * bn;
+        }
+        tl[rr][col + q] = a;
+        sq += (double)a * a;
+      }
     }
   }
   __syncthreads();
@@ -202,9 +317,119 @@ __device__ __forceinline__ double reduce_tile(const Chunk& c, const float* __res
     float* dst = delta + c.ws + (int64_t)cc * c.ws_ld + r;
     if (c.vec) {
       const floatx4 o = {tl[r][cc], tl[r + 1][cc], tl[r + 2][cc], tl[r + 3][cc]};
-      *reinterpret_cast<floatx4*>(dst) = o;
+      __builtin_nontemporal_store(o, reinterpret_cast<floatx4*>(dst));
     } else {
       for (int q = 0; q < 4 && r + q < TR; ++q) dst[q] = tl[r + q][cc];
+    }
+  }
+  return sq;
+}
+
+// The vectorised part of a contiguous chunk: Delta of elements [0, V * (count / V))
+// (ISO: stored to the workspace, returns the thread's share of sum Delta^2;
+// AVG: Nesterov in place).  FULL: the chunk has kChunk elements, so every
+// slot is inside it and no load needs a predicate.
+template <int WDT, bool FULL>
+__device__ __forceinline__ double reduce_run(const Chunk& c, float* __restrict__ theta, float* __restrict__ mom,
+                                             float* __restrict__ delta, const WorkerPtrs& w, int K, float inv_k,
+                                             float lr, float mu, int heavy_ball, int target_update, bool iso) {
+  using WL = WorkerLoad<WDT>;
+  constexpr int V = WL::kVec;
+  constexpr int S = ReduceShape<WDT>::kSlots;
+  constexpr int G = ReduceShape<WDT>::kGroup;
+  // slot q of thread t: elements V (t + 256 q) .. +V-1 of the chunk, at byte
+  // offset 16 t + 4096 q of a replica (one 32-bit lane offset for every slot
+  // and stream; the slot's step is a scalar offset) and twice that for
+  // bfloat16 replicas in theta; loads past the chunk return zero, so none
+  // needs a predicate
+  const int nv = c.count / V;
+  const uint32_t lane = 16u * threadIdx.x;
+  constexpr uint32_t kSlotBytes = 16u * kStreamThreads;
+  bool on[S];
+  float th[S][V], acc[S][V];
+  const __amdgpu_buffer_rsrc_t rt = stream_rsrc(theta + c.src, 4u * (uint32_t)(nv * V));
+#pragma unroll
+  for (int q = 0; q < S; ++q) {
+    on[q] = FULL || (int)(threadIdx.x + q * kStreamThreads) < nv;
+#pragma unroll
+    for (int r = 0; r < V; r += 4) {
+      const floatx4 t4 = __builtin_bit_cast(
+          floatx4, WorkerLoad<0>::load16(rt, lane * (V / 4) + 16u * (r / 4), kSlotBytes * (V / 4) * q));
+      th[q][r] = t4[0]; th[q][r + 1] = t4[1]; th[q][r + 2] = t4[2]; th[q][r + 3] = t4[3];
+    }
+#pragma unroll
+    for (int r = 0; r < V; ++r) acc[q][r] = 0.f;
+  }
+  // workers in groups of G: the group's S * G 16-byte loads are all issued
+  // before any of them is consumed (differences summed in worker order)
+#pragma unroll 1
+  for (int k0 = 0; k0 < K; k0 += G) {
+    // (a last group past K loads worker K - 1 again and does not add it)
+    __amdgpu_buffer_rsrc_t rw[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+      rw[j] = stream_rsrc(static_cast<const char*>(w.p[min(k0 + j, K - 1)]) + WL::kBytes * c.src,
+                          WL::kBytes * (uint32_t)(nv * V));
+    // the loads stay undecoded until they are added (bf16: half the registers)
+    u32x4 wv[G][S];
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int q = 0; q < S; ++q) wv[j][q] = WL::load16(rw[j], lane, kSlotBytes * q);
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+      if (k0 + j < K) {
+#pragma unroll
+        for (int q = 0; q < S; ++q)
+#pragma unroll
+          for (int r = 0; r < V; ++r) acc[q][r] += th[q][r] - WL::decode(wv[j][q], r);
+      }
+  }
+  double sq = 0.0;
+#pragma unroll
+  for (int q = 0; q < S; ++q) {
+    if (!on[q]) continue;
+    const int v = threadIdx.x + q * kStreamThreads;
+    const int64_t e = c.src + (int64_t)v * V;
+#pragma unroll
+    for (int r = 0; r < V; ++r) acc[q][r] *= inv_k;
+    if (iso) {
+      float* dst = delta + c.ws + (int64_t)v * V;
+      if (target_update) {
+        // B <- mu B + Delta now; the polar input is the update itself
+#pragma unroll
+        for (int r0 = 0; r0 < V; r0 += 4) {
+          floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + r0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float bn = mu * b4[r] + acc[q][r0 + r];
+            b4[r] = bn;
+            acc[q][r0 + r] = heavy_ball ? bn : acc[q][r0 + r] + mu * bn;
+          }
+          *reinterpret_cast<floatx4*>(mom + e + r0) = b4;
+        }
+      }
+#pragma unroll
+      for (int r0 = 0; r0 < V; r0 += 4) {
+        const floatx4 o = {acc[q][r0], acc[q][r0 + 1], acc[q][r0 + 2], acc[q][r0 + 3]};
+        __builtin_nontemporal_store(o, reinterpret_cast<floatx4*>(dst + r0));
+        sq += (double)o[0] * o[0] + (double)o[1] * o[1] + (double)o[2] * o[2] + (double)o[3] * o[3];
+      }
+    } else {
+#pragma unroll
+      for (int r0 = 0; r0 < V; r0 += 4) {
+        floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + r0);
+        floatx4 t4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = acc[q][r0 + r];
+          const float bn = mu * b4[r] + d;
+          b4[r] = bn;
+          t4[r] = th[q][r0 + r] - lr * (heavy_ball ? bn : d + mu * bn);
+        }
+        *reinterpret_cast<floatx4*>(mom + e + r0) = b4;
+        *reinterpret_cast<floatx4*>(theta + e + r0) = t4;
+      }
     }
   }
   return sq;
@@ -228,77 +453,20 @@ reduce_kernel(const Chunk* __restrict__ chunks, float* __restrict__ theta,
   int done = 0;
   if (c.rows) {
     // a tile of a tall row-major tensor (always corrected): Delta column-major
-    sq = reduce_tile<WDT>(c, theta, mom, delta, w, K, inv_k, mu, heavy_ball, target_update, tl);
+    if (c.rows == kTileRows && c.cols == kTileCols)
+      sq = reduce_tile<WDT, true>(c, theta, mom, delta, w, K, inv_k, mu, heavy_ball, target_update, tl);
+    else
+      sq = reduce_tile<WDT, false>(c, theta, mom, delta, w, K, inv_k, mu, heavy_ball, target_update, tl);
     done = c.count;
   } else if (c.vec) {
+    // a whole chunk takes the path without per-slot predicates (its loads
+    // are then issued back to back); a shorter last chunk of a tensor the
+    // predicated one
+    if (c.count == kChunk)
+      sq = reduce_run<WDT, true>(c, theta, mom, delta, w, K, inv_k, lr, mu, heavy_ball, target_update, iso);
+    else
+      sq = reduce_run<WDT, false>(c, theta, mom, delta, w, K, inv_k, lr, mu, heavy_ball, target_update, iso);
     const int nv = c.count / V;
-    for (int v = threadIdx.x; v < nv; v += kStreamThreads) {
-      const int64_t e = c.src + (int64_t)v * V;
-      float th[V], acc[V];
-#pragma unroll
-      for (int q = 0; q < V; q += 4) {
-        const floatx4 t4 = *reinterpret_cast<const floatx4*>(theta + e + q);
-        th[q] = t4[0]; th[q + 1] = t4[1]; th[q + 2] = t4[2]; th[q + 3] = t4[3];
-      }
-#pragma unroll
-      for (int q = 0; q < V; ++q) acc[q] = 0.f;
-      // workers in groups of 8: the group's 16-byte loads are all issued
-      // before any of them is consumed (differences summed in worker order)
-#pragma unroll 1
-      for (int k0 = 0; k0 < K; k0 += 8) {
-        float wv[8][V];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (k0 + j < K) WL::vec(w.p[k0 + j], e, wv[j]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (k0 + j < K) {
-#pragma unroll
-            for (int q = 0; q < V; ++q) acc[q] += th[q] - wv[j][q];
-          }
-      }
-#pragma unroll
-      for (int q = 0; q < V; ++q) acc[q] *= inv_k;
-      if (iso) {
-        float* dst = delta + c.ws + (int64_t)v * V;
-        if (target_update) {
-          // B <- mu B + Delta now; the polar input is the update itself
-#pragma unroll
-          for (int q = 0; q < V; q += 4) {
-            floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + q);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float bn = mu * b4[r] + acc[q + r];
-              b4[r] = bn;
-              acc[q + r] = heavy_ball ? bn : acc[q + r] + mu * bn;
-            }
-            *reinterpret_cast<floatx4*>(mom + e + q) = b4;
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < V; q += 4) {
-          floatx4 o = {acc[q], acc[q + 1], acc[q + 2], acc[q + 3]};
-          *reinterpret_cast<floatx4*>(dst + q) = o;
-          sq += (double)acc[q] * acc[q] + (double)acc[q + 1] * acc[q + 1] +
-                (double)acc[q + 2] * acc[q + 2] + (double)acc[q + 3] * acc[q + 3];
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < V; q += 4) {
-          floatx4 b4 = *reinterpret_cast<const floatx4*>(mom + e + q);
-          floatx4 t4;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float d = acc[q + r];
-            const float bn = mu * b4[r] + d;
-            b4[r] = bn;
-            t4[r] = th[q + r] - lr * (heavy_ball ? bn : d + mu * bn);
-          }
-          *reinterpret_cast<floatx4*>(mom + e + q) = b4;
-          *reinterpret_cast<floatx4*>(theta + e + q) = t4;
-        }
-      }
-    }
     done = nv * V;
   }
   for (int i = done + threadIdx.x; i < c.count; i += kStreamThreads) {
@@ -892,9 +1060,6 @@ struct Slab32 {
   floatx4 v[4];
 };
 
-// Word 3 of a raw buffer resource on CDNA3/CDNA4 (32-bit data format, no
-// swizzle; the range check compares byte offsets with the record count).
-constexpr int kBufferFlags = 0x00020000;
 
 // 128 (i) x 32 (k) fp32 slab into registers: thread t owns row i = t % 128
 // and the 16 consecutive k values 16 (t / 128) .. +15, so that its LDS writes
