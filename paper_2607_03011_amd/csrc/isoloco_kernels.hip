@@ -1054,6 +1054,18 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_f32_kernel(GemmArgs g) {
 constexpr int kBK2 = 32;
 constexpr int kLdsK = kBK2 + 8;  // padded row (bf16 elements): 80 bytes
 
+// Element offset within an LDS operand row of its 16-byte k-chunk c (0..3).
+// Rows of LK = 40 bf16 (80 bytes) keep 16-byte accesses to 8 consecutive rows
+// on distinct banks as they are; rows of LK = 32 (64 bytes, no padding:
+// room for two buffers of bf16x5 operands) XOR the chunk position with bits
+// 1-2 of the row to the same effect (a probe of both layouts measured 6%
+// slower reads and 8% slower stores for 64-byte rows).
+template <int LK>
+__device__ __forceinline__ int lds_chunk(int row, int c) {
+  static_assert(LK == kLdsK || LK == kBK2, "80- or 64-byte operand rows");
+  return LK == kBK2 ? ((c ^ ((row >> 1) & 3)) << 3) : (c << 3);
+}
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 struct Slab32 {
@@ -1162,8 +1174,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // and store each part plane as two 16-byte row segments.  SCALED multiplies
 // the values by the operand's scale first (the 1/||Delta||_F of the first
 // polar step; 1 afterwards, when the multiply is left out).
-template <int NS, bool SCALED = false, int ROWS = kBM>
-__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale = 1.f) {
+template <int NS, bool SCALED = false, int ROWS = kBM, int LK = kLdsK>
+__device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[ROWS][LK], float scale = 1.f) {
   const int t = threadIdx.x;
   const int i = t % ROWS, kb = 16 * (t / ROWS);
 #pragma unroll
@@ -1182,7 +1194,8 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[R
       }
     }
 #pragma unroll
-    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x8*>(&planes[p][i][kb + 8 * half]) = part[p];
+    for (int p = 0; p < NS; ++p)
+      *reinterpret_cast<bf16x8*>(&planes[p][i][lds_chunk<LK>(i, (kb >> 3) + half)]) = part[p];
   }
 }
 
@@ -1190,8 +1203,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // The same for registers in the row mapping (thread t: rows t / 8 + (ROWS / 4) q,
 // k = 4 (t % 8) .. +3): 8-byte LDS writes.
-template <int NS, bool SCALED = false, int ROWS = kBM>
-__device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale = 1.f) {
+template <int NS, bool SCALED = false, int ROWS = kBM, int LK = kLdsK>
+__device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[ROWS][LK], float scale = 1.f) {
   const int t = threadIdx.x;
   const int i = t >> 3, kb = 4 * (t & 7);
 #pragma unroll
@@ -1209,15 +1222,17 @@ __device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*plan
         if (p + 1 < NS) x -= __builtin_convertvector(h, floatx2);
       }
     }
+    const int row = i + (ROWS / 4) * q;
 #pragma unroll
-    for (int p = 0; p < NS; ++p) *reinterpret_cast<bf16x4*>(&planes[p][i + (ROWS / 4) * q][kb]) = part[p];
+    for (int p = 0; p < NS; ++p)
+      *reinterpret_cast<bf16x4*>(&planes[p][row][lds_chunk<LK>(row, kb >> 3) + (kb & 7)]) = part[p];
   }
 }
 
-template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED, int ROWS = kBM>
-__device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[ROWS][kLdsK], float scale) {
-  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED, ROWS>(r, planes, scale);
-  else slab32_store<NS, SCALED, ROWS>(r, planes, scale);
+template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED, int ROWS = kBM, int LK = kLdsK>
+__device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[ROWS][LK], float scale) {
+  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED, ROWS, LK>(r, planes, scale);
+  else slab32_store<NS, SCALED, ROWS, LK>(r, planes, scale);
 }
 
 // Split-bf16 arithmetic with NP part products per fp32 product: NP = 3
@@ -1243,8 +1258,8 @@ struct SplitParts {
 // wn = wave % WNC).  SWAP: issue each product as B A instead of A B, so that
 // the accumulators hold the transposed 32 x 32 blocks (4 consecutive output
 // columns per lane).
-template <int NSA, int NSB, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false>
-__device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], const __bf16 (*Bp)[ROWS][kLdsK],
+template <int NSA, int NSB, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false, int LK = kLdsK>
+__device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][LK], const __bf16 (*Bp)[ROWS][LK],
                                              int kk, floatx16 (&acc)[NA][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WNC, wn = wave % WNC;
@@ -1255,13 +1270,13 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][kLdsK], co
   for (int a = 0; a < NA; ++a) {
     const int row = wm * 32 * NA + a * 32 + (lane & 31);
 #pragma unroll
-    for (int p = 0; p < NSA; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][kc]);
+    for (int p = 0; p < NSA; ++p) av[a][p] = *reinterpret_cast<const bf16x8*>(&Ap[p][row][lds_chunk<LK>(row, kc >> 3)]);
   }
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int row = wn * 64 + b * 32 + (lane & 31);
 #pragma unroll
-    for (int p = 0; p < NSB; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][kc]);
+    for (int p = 0; p < NSB; ++p) bv[b][p] = *reinterpret_cast<const bf16x8*>(&Bp[p][row][lds_chunk<LK>(row, kc >> 3)]);
   }
 #pragma unroll
   for (int a = 0; a < NA; ++a)
@@ -1469,11 +1484,22 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
 constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 
+// LDS of the 256 x 256 kernel: bf16x3 double-buffers 80-byte rows (2 x 2 x 2
+// planes of 256 rows: 160 KB); bf16x5 double-buffers 64-byte rows (2 x (3 + 2)
+// planes: 160 KB; with 80-byte rows one buffer only, two barriers per slab:
+// its updates took 2.6x the time of a bf16x3 update for 1.67x the products);
+// bf16x6 keeps one buffer of 80-byte rows.
+template <int NP>
+struct BigLds {
+  static constexpr int nb = NP == 6 ? 1 : 2;            // LDS buffers
+  static constexpr int lk = NP == 5 ? kBK2 : kLdsK;     // row pitch (bf16 elements)
+};
+
 template <int MODE, int NP, int LAYOUT, bool SCALED>
 __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task,
-                                              __bf16 (*Ap)[SplitParts<NP>::a][kBig][kLdsK],
-                                              __bf16 (*Bp)[SplitParts<NP>::b][kBig][kLdsK]) {
-  constexpr int kNa = SplitParts<NP>::a, kNb = SplitParts<NP>::b, NB = SplitParts<NP>::nb;
+                                              __bf16 (*Ap)[SplitParts<NP>::a][kBig][BigLds<NP>::lk],
+                                              __bf16 (*Bp)[SplitParts<NP>::b][kBig][BigLds<NP>::lk]) {
+  constexpr int kNa = SplitParts<NP>::a, kNb = SplitParts<NP>::b, NB = BigLds<NP>::nb, LK = BigLds<NP>::lk;
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
   // update tiles of row-major X' accumulate transposed blocks (16-byte stores)
@@ -1490,34 +1516,34 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
     load_operand<MODE, LAYOUT, true, kBig>(s.A, s.k_begin, s.i0, ra);
     load_operand<MODE, LAYOUT, false, kBig>(s.B, s.k_begin, s.j0, rb);
     if constexpr (NB == 2) {
-      store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
       load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
       load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
       __syncthreads();
       for (int sl = 0; sl + 1 < nslab; ++sl) {
         const int cur = sl & 1;
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 0, acc);
-        store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[cur ^ 1], s.A.scale);
-        store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[cur ^ 1], s.B.scale);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[cur], Bp[cur], 16, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[cur], Bp[cur], 0, acc);
+        store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[cur ^ 1], s.A.scale);
+        store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[cur ^ 1], s.B.scale);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[cur], Bp[cur], 16, acc);
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
         __syncthreads();
       }
       const int last = (nslab - 1) & 1;
-      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 0, acc);
-      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[last], Bp[last], 16, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[last], Bp[last], 0, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[last], Bp[last], 16, acc);
     } else {
       for (int sl = 0; sl < nslab; ++sl) {
         __syncthreads();
-        store_operand<MODE, LAYOUT, true, kNa, SA, kBig>(ra, Ap[0], s.A.scale);
-        store_operand<MODE, LAYOUT, false, kNb, SB, kBig>(rb, Bp[0], s.B.scale);
+        store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
+        store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
         __syncthreads();
         load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 1), s.i0, ra);
         load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 1), s.j0, rb);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 0, acc);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap>(Ap[0], Bp[0], 16, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 0, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 16, acc);
       }
     }
   }
@@ -1529,9 +1555,9 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
 
 template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
-  constexpr int NB = SplitParts<NP>::nb;
-  typedef __bf16 APlanes[SplitParts<NP>::a][kBig][kLdsK];
-  typedef __bf16 BPlanes[SplitParts<NP>::b][kBig][kLdsK];
+  constexpr int NB = BigLds<NP>::nb;
+  typedef __bf16 APlanes[SplitParts<NP>::a][kBig][BigLds<NP>::lk];
+  typedef __bf16 BPlanes[SplitParts<NP>::b][kBig][BigLds<NP>::lk];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   auto run = [&](APlanes* Ap, BPlanes* Bp) {
