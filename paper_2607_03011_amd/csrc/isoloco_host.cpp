@@ -351,7 +351,7 @@ struct isoloco_plan_s {
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
-  size_t off_pnorm = 0, off_cnt = 0, off_coef = 0;
+  size_t off_pnorm = 0, off_cnt = 0, off_mcnt = 0, off_coef = 0;
   size_t off_gtc[kSchedClasses] = {}, off_ptc[kSchedClasses] = {}, off_utc[kSchedClasses] = {};
   size_t off_cic[kSchedClasses] = {};
   // the second stream of the per-class mode, with its fork and join events
@@ -464,6 +464,9 @@ void plan_matrices(isoloco_plan_s* p) {
     int ks = 1;
     if (mi.m >= 4 * mi.n && mi.m > 4096)
       ks = (int)std::min<int64_t>(kMaxKSplit, (mi.m + 1023) / 1024);
+    // the slices of one matrix stay under 2 GiB (the Gram epilogue addresses
+    // them with 32-bit buffer offsets)
+    while (ks > 1 && 4 * (int64_t)ks * mi.n * mi.n >= ((int64_t)1 << 31)) --ks;
     int64_t kchunk = (mi.m + ks - 1) / ks;
     kchunk = (kchunk + 31) / 32 * 32;  // whole K slabs of both product kernels
     ks = (int)((mi.m + kchunk - 1) / kchunk);
@@ -651,6 +654,7 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_ptr = take(p->chunks.size() * sizeof(double));
   p->off_pnorm = take((size_t)p->n_norm * sizeof(double));
   p->off_cnt = take((size_t)p->n_cnt * sizeof(int));
+  p->off_mcnt = take(p->mats.size() * sizeof(int));
   p->off_coef = take(p->coef.size() * sizeof(float));
   p->off_delta = take((size_t)p->n2d * sizeof(float));
   p->off_x0 = take((size_t)p->n2d * sizeof(float));
@@ -705,6 +709,7 @@ DevTables dev_tables(const isoloco_plan_s* p, char* w) {
   t.part_tr = reinterpret_cast<double*>(w + p->off_ptr);
   t.part_norm = reinterpret_cast<double*>(w + p->off_pnorm);
   t.split_cnt = reinterpret_cast<int*>(w + p->off_cnt);
+  t.mat_cnt = reinterpret_cast<int*>(w + p->off_mcnt);
   t.coef = reinterpret_cast<const float*>(w + p->off_coef);
   t.chunk_idx = nullptr;
   t.n_chunk_idx = 0;
@@ -725,7 +730,7 @@ DevTables dev_tables(const isoloco_plan_s* p, char* w) {
 }
 
 // Copy the plan's tables into the workspace at w and clear what the kernels
-// expect at zero (per-matrix scalars, split-K arrival counters); synchronous.
+// expect at zero (per-matrix scalars, arrival counters); synchronous.
 hipError_t upload_tables(const isoloco_plan_s* plan, char* w) {
   hipError_t e;
   auto up = [&](size_t off, const void* src, size_t n) -> hipError_t {
@@ -751,8 +756,11 @@ hipError_t upload_tables(const isoloco_plan_s* plan, char* w) {
       return e;
   if (!plan->mats.empty() && (e = hipMemset(w + plan->off_sc, 0, plan->mats.size() * sizeof(MatScalars))) != hipSuccess)
     return e;
-  // the split-K Gram tiles count their arrivals here; each launch leaves them at zero
+  // the split-K Gram tiles, and the last tiles and trace chunks of each matrix,
+  // count their arrivals here; each launch leaves them at zero
   if (plan->n_cnt > 0 && (e = hipMemset(w + plan->off_cnt, 0, (size_t)plan->n_cnt * sizeof(int))) != hipSuccess)
+    return e;
+  if (!plan->mats.empty() && (e = hipMemset(w + plan->off_mcnt, 0, plan->mats.size() * sizeof(int))) != hipSuccess)
     return e;
   // done before any stream of the caller's (some may not wait for the null stream)
   return hipStreamSynchronize(nullptr);
@@ -1046,10 +1054,14 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
       auto gram = [&](const PolarStep& ps) -> hipError_t {
         return timed_on(s, kPhGram, [&] { return launch_gemm(tt, 0, ps, s); });
       };
-      auto norm = [&](int mode) -> hipError_t {
-        na.mode = mode;
-        na.only_active = 1;
-        return timed_on(s, kPhOther, [&] { return launch_gram_norm(tt, na, s); });
+      na.only_active = 1;
+      // a Gram launch that leaves the norm partials of `mode` also takes the
+      // decisions (in the last tile of each matrix)
+      auto gram_norm = [&](PolarStep ps, int mode) -> hipError_t {
+        ps.norm_mode = mode;
+        ps.norm = na;
+        ps.norm.mode = mode;
+        return gram(ps);
       };
       const float* xin = tt.delta;
       bool have_gram = false;  // the Gram of xin was formed by the last phase end's check
@@ -1061,11 +1073,9 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
         ps.first = (k == 0);
         ps.only_active = 1;
         ps.arith = step_arith(plan->opts.precision, k, kProdGram);
-        // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
-        ps.norm_mode = (k == 0 && !ns5) ? kNormFirst : -1;
         what = "polar step launch";
-        if (!have_gram && (r = gram(ps)) != hipSuccess) return r;
-        if (ps.norm_mode == kNormFirst && (r = norm(kNormFirst)) != hipSuccess) return r;
+        // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
+        if (!have_gram && (r = (k == 0 && !ns5) ? gram_norm(ps, kNormFirst) : gram(ps)) != hipSuccess) return r;
         PolarStep pp = ps, pu = ps;
         pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
         pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
@@ -1093,11 +1103,12 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
           pc.xin = xin;
           pc.only_active = 1;
           pc.arith = step_arith(plan->opts.precision, k + 1, kProdGram);
-          pc.norm_mode = kNormPhase;
-          if ((r = gram(pc)) != hipSuccess) return r;
+          if ((r = gram_norm(pc, kNormPhase)) != hipSuccess) return r;
           have_gram = true;
+        } else {
+          na.mode = kNormPhase;
+          if ((r = timed_on(s, kPhOther, [&] { return launch_gram_norm(tt, na, s); })) != hipSuccess) return r;
         }
-        if ((r = norm(kNormPhase)) != hipSuccess) return r;
         if (ev_switch && *switch_steps == 0 && cls >= 0 && na.action[cls] == kActSwitch) {
           if ((r = hipEventRecord(ev_switch, s)) != hipSuccess) return r;
           *switch_steps = k + 1;
@@ -1115,9 +1126,8 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
         pc.xin = xin;
         pc.only_active = 1;
         pc.arith = step_arith(plan->opts.precision, Sx, kProdGram);
-        pc.norm_mode = kNormPhase;
         what = "check launch";
-        if ((r = gram(pc)) != hipSuccess || (r = norm(kNormPhase)) != hipSuccess) return r;
+        if ((r = gram_norm(pc, kNormPhase)) != hipSuccess) return r;
       }
       return hipSuccess;
     };

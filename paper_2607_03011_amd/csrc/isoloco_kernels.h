@@ -36,6 +36,8 @@ struct DevTables {
   double* part_tr;
   double* part_norm;  // Gram-norm partials, gram_tiles(n) per matrix from MatInfo::norm_off
   int* split_cnt;     // arrival counters of the split-K Gram tiles (zero between launches)
+  int* mat_cnt;       // per-matrix arrival counters of the Gram tiles and the trace chunks
+                      // (zero between launches)
   float* delta;
   float* x[2];
   float* x2;              // clip variants: copy of the polar factor Q (else unused)
@@ -73,21 +75,8 @@ struct StepArgs {
 // Arithmetic of one batched-product launch.
 enum Arith { kArithBf16x3 = 0, kArithBf16x6 = 1, kArithFp32 = 2, kArithBf16x5 = 3 };
 
-struct PolarStep {
-  const float* xin;
-  const float* xin_alt;  // if set, matrix m reads X from xin_alt when its qbuf is 1 (Gram mode)
-  const float* bin;      // if set, the Gram's second operand (same layout as X): X^T B
-  float* xout;
-  int step;         // polar step: the polynomial product takes each matrix's coefficients of this step
-  int first;
-  int only_active;  // 1: skip matrices whose scalars say active == 0
-  int arith;        // Arith
-  int norm_mode = -1;  // Gram only: -1 none, else the NormMode whose tile partials the Gram
-                    // leaves in DevTables::part_norm (kNormFirst: sum A^2, others sum (A - I)^2)
-};
-
-// Gram-norm modes (a Gram launch with norm_mode >= 0 leaves the per-tile
-// partials that gram_norm_final_kernel reads)
+// Gram-norm modes (a Gram launch with norm_mode >= 0 leaves per-tile partials,
+// from which the last tile of each matrix takes its decisions)
 enum NormMode {
   kNormFirst = 0,  // gscale = ||A||_F^(-1/2) of the first step (partials of sum A^2)
   kNormPhase = 1,  // a phase end: resid from sum (A - I)^2, then each class's action
@@ -116,6 +105,21 @@ struct NormArgs {
   int flag_below[kSchedClasses];
 };
 
+struct PolarStep {
+  const float* xin;
+  const float* xin_alt;  // if set, matrix m reads X from xin_alt when its qbuf is 1 (Gram mode)
+  const float* bin;      // if set, the Gram's second operand (same layout as X): X^T B
+  float* xout;
+  int step;         // polar step: the polynomial product takes each matrix's coefficients of this step
+  int first;
+  int only_active;  // 1: skip matrices whose scalars say active == 0
+  int arith;        // Arith
+  int norm_mode = -1;  // Gram only: -1 none, else the NormMode whose tile partials the Gram
+                    // leaves in DevTables::part_norm (kNormFirst: sum A^2, others sum (A - I)^2)
+  NormArgs norm{};  // norm_mode >= 0: the decisions the last tile of each matrix takes
+                    // from those partials (norm.mode == norm_mode)
+};
+
 // Initial per-matrix iteration state: steps and result buffer of each class's full schedule
 struct FroArgs {
   int steps_total[kSchedClasses], buf_total[kSchedClasses];
@@ -132,8 +136,8 @@ hipError_t launch_reduce(const DevTables& t, const StepArgs& a, hipStream_t st);
 hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st);
 // mode: 0 Gram, 1 polynomial, 2 update
 hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStream_t st);
-// per-matrix decisions from the norm partials of the Gram launched before with
-// norm_mode = a.mode
+// the per-matrix decisions of a phase end without a residual check (only
+// kActStop or kActNone actions: no Gram launch to take them)
 hipError_t launch_gram_norm(const DevTables& t, const NormArgs& a, hipStream_t st);
 // the polar factor of matrix m is in t.x[scalars[m].qbuf]; the scale of each
 // correction (a.scale: its mean singular value from <Q, Delta>, or a closed form)

@@ -504,6 +504,32 @@ __device__ __forceinline__ double block_sum_range(const double* part, int begin,
   return block_sum256(s, lds4);
 }
 
+// Partials that one launch's workgroups hand to the last of them to arrive.
+// They are stored and loaded with agent-scope atomics, which the hardware
+// keeps coherent across the XCDs' separate L2 caches by themselves (no
+// writeback or invalidation of a whole L2, which agent-scope release and
+// acquire fences cost on this part).  arrive() waits for the workgroup's own
+// store to complete before it counts itself, so that the workgroup that
+// counts last finds every partial in place; it is called by one thread.
+__device__ __forceinline__ void partial_store(double* p, double v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double partial_load(const double* p) {
+  return __hip_atomic_load(const_cast<double*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Cache policy of buffer accesses at agent scope (the "sc1" bit): coherent
+// across the XCDs like the atomics above.
+constexpr int kAgentCoherent = 16;
+
+// true in the workgroup that is the n-th to arrive at *cnt, which it sets back to zero
+__device__ __forceinline__ bool arrive(int* cnt, int n) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  const bool last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n - 1;
+  asm volatile("" ::: "memory");
+  if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return last;
+}
+
 // ||Delta||_F per matrix (one block per matrix).
 __global__ void __launch_bounds__(256)
 fro_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_sq,
@@ -615,6 +641,7 @@ struct GemmArgs {
   const MatInfo* mats;
   const Task* tasks;
   const MatScalars* sc;
+  MatScalars* sc_out;  // Gram with norm_mode >= 0: the same scalars, which the decisions write
   const float* xin;   // Gram/Update: X input buffer (Delta at step 0)
   const float* xin_alt;  // Gram: if set, matrices whose qbuf is 1 read X here
   const float* bin;      // Gram: if set, the second operand B (C = X^T B)
@@ -623,12 +650,14 @@ struct GemmArgs {
   float* poly;        // n x n polynomial buffers (Poly output, Update input)
   float* gpart;       // split-K Gram partials
   int* split_cnt;     // split-K Gram: arrival counter per output tile
+  int* mat_cnt;       // Gram with norm_mode >= 0: arrival counter per matrix
   double* part_norm;  // Gram: per-tile partial sums of squares (norm_mode >= 0)
   const float* coef;  // Poly: coefficients [class][n_steps][3] of p(x) = ca x + cb x^3 + cc x^5
   int step, n_steps;  // Poly: this step, and the table's steps per class
   int first;          // 1 on the first step (inputs pre-scaled by 1/||Delta||_F, g applied)
   int only_active;    // 1: tasks of matrices that stopped iterating return at once
   int norm_mode;      // Gram: -1, or kNormFirst (sum A^2) / other (sum (A - I)^2) per tile
+  NormArgs na;        // norm_mode >= 0: the decisions of the matrix's last tile (norm_decide)
 };
 
 // Operands, output bounds and K range of one task.
@@ -749,17 +778,52 @@ __device__ __forceinline__ void gemm_acc_init(const GemmArgs& g, const GemmSetup
     }
 }
 
+// The decisions of matrix mi from its Gram's norm partials (see NormMode,
+// NormAction): the partials of its gram_tiles(n) tiles are added in tile order.
+__device__ __forceinline__ void norm_decide(const MatInfo& mi, const double* part, MatScalars& o, const NormArgs& a) {
+  if (a.cls >= 0 && mi.sched != a.cls) return;
+  const int act = a.mode == kNormFirst ? kActNone : a.action[mi.sched];
+  if (a.mode != kNormFirst && act == kActNone) return;
+  if (act == kActStop) {
+    o.active = 0;
+    return;
+  }
+  double s = 0.0;
+  const int nt = gram_tiles(mi.n);
+  for (int x = 0; x < nt; ++x) s += partial_load(part + mi.norm_off + x);
+  if (a.mode == kNormFirst) {
+    o.gscale = ((o.flags & kFlagInput) == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
+    return;
+  }
+  o.resid = (float)sqrt(s / mi.n);
+  if (act == kActSwitch) {
+    // stop at the end of this phase when every singular value is already at 1
+    const bool go_on = (o.flags & kFlagInput) == 0 && !(o.resid <= a.tol_switch);
+    // a matrix that still has a singular value away from 1 after the schedule
+    // for a bound at the float32 resolution of Delta has one below it: its
+    // direction in Q is decided by rounding, not by Delta
+    if (go_on && a.flag_below[mi.sched]) o.flags |= kFlagBelowResolution;
+    o.active = go_on ? 1 : 0;
+    o.steps = go_on ? a.steps_total[mi.sched] : a.steps_here;
+    o.qbuf = go_on ? a.buf_total[mi.sched] : a.buf_here;
+  } else {
+    if (a.flag_unconverged && !(o.resid <= 1e-3f) && (o.flags & kFlagInput) == 0) o.flags |= kFlagNotConverged;
+    o.active = 0;
+  }
+}
+
 // Gram epilogue.  Writes the tile and its mirror image into the n x n Gram
 // buffer and, when the launch asks for it, the tile's share of ||A||_F^2 or
 // ||A - I||_F^2 (twice the tile's sum off the diagonal) into its slot of
-// part_norm, which gram_norm_final_kernel adds up in a fixed order.
+// part_norm.  The last tile of a matrix to arrive (counted per matrix like the
+// split-K slices below) adds the matrix's slots in a fixed order and takes its
+// decisions (norm_decide), so that no launch of its own is needed for them.
 //
 // A split-K matrix first writes this K slice's partial tile into its slice of
-// gpart.  The last of the ksplit workgroups of a tile to arrive (counted by an
-// agent-scope atomic, release before and acquire after it, so that the
-// partials written on other XCDs are visible) adds the slices in slice order,
-// finishes the tile as above and sets the counter back to zero for the next
-// launch.  No workgroup waits for another.  `scratch` is LDS the operand
+// gpart.  The last of the ksplit workgroups of a tile to arrive (arrive(),
+// with the partials stored and loaded at agent scope so that those written on
+// other XCDs are seen) adds the slices in slice order and finishes the tile as
+// above.  No workgroup waits for another.  `scratch` is LDS the operand
 // planes no longer need (at least 40 bytes).
 template <int NA, int WNC>
 __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
@@ -779,11 +843,13 @@ __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup
     for (int b = 0; b < 2; ++b) v[a][b] = acc[a][b];
   if (mi.ksplit > 1) {
     // partial tiles are stored transposed (C(i, j) at j * n + i), so that the
-    // 4 values a lane holds, C(i .. i+3, j), are one 16-byte access
+    // 4 values a lane holds, C(i .. i+3, j), are one 16-byte access; they are
+    // stored and loaded at agent scope (the planner keeps a matrix's slices
+    // under 2 GiB, the range of the buffer offsets)
     const int64_t nn = (int64_t)n * n;
     const bool v4 = (n & 3) == 0;
-    const float* part = g.gpart + mi.part_off;
-    float* mine = g.gpart + mi.part_off + (int64_t)task.ks * nn;
+    const __amdgpu_buffer_rsrc_t pr = stream_rsrc(g.gpart + mi.part_off, (uint32_t)(4 * mi.ksplit * nn));
+    const int64_t mine = (int64_t)task.ks * nn;
 #pragma unroll
     for (int a = 0; a < NA; ++a)
 #pragma unroll
@@ -793,26 +859,24 @@ __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup
 #pragma unroll
         for (int grp = 0; grp < 4; ++grp) {
           const int ibase = s.i0 + wm * 32 * NA + a * 32 + 8 * grp + ib;
-          float* o = mine + (int64_t)j * n + ibase;
+          const int off = (int)(4 * (mine + (int64_t)j * n + ibase));
           if (v4 && ibase + 3 < s.M) {
             const floatx4 q = {v[a][b][4 * grp], v[a][b][4 * grp + 1], v[a][b][4 * grp + 2], v[a][b][4 * grp + 3]};
-            *reinterpret_cast<floatx4*>(o) = q;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, q), pr, off, 0, kAgentCoherent);
           } else {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if (ibase + r < s.M) o[r] = v[a][b][4 * grp + r];
+              if (ibase + r < s.M)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[a][b][4 * grp + r]), pr, off + 4 * r, 0,
+                                                      kAgentCoherent);
           }
         }
       }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's slice is in place
     __syncthreads();  // every wave's partial is out, and the operand planes are free
-    int* cnt = g.split_cnt + mi.cnt_off + tile;
-    if (threadIdx.x == 0)
-      *last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == mi.ksplit - 1;
+    if (threadIdx.x == 0) *last = arrive(g.split_cnt + mi.cnt_off + tile, mi.ksplit);
     __syncthreads();
     if (!*last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     // the slices in slice order; every load of the tile is independent of the
     // sums, so that they can all be in flight together
 #pragma unroll
@@ -832,12 +896,15 @@ __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup
             if (k >= mi.ksplit) break;
             floatx4 x = own;
             if (k != task.ks) {
-              const float* src = part + k * nn + (int64_t)j * n + ibase;
+              const int off = (int)(4 * (k * nn + (int64_t)j * n + ibase));
               if (vec) {
-                x = *reinterpret_cast<const floatx4*>(src);
+                x = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(pr, off, 0, kAgentCoherent));
               } else {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) x[r] = ibase + r < s.M ? src[r] : 0.f;
+                for (int r = 0; r < 4; ++r)
+                  x[r] = ibase + r < s.M
+                             ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(pr, off + 4 * r, 0, kAgentCoherent))
+                             : 0.f;
               }
             }
             t = k == 0 ? x : t + x;
@@ -889,7 +956,10 @@ __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup
   if (want) {
     __syncthreads();  // the operand planes are free (split tiles passed this point already)
     sq = block_sum256(sq, red);
-    if (threadIdx.x == 0) g.part_norm[mi.norm_off + tile] = diag ? sq : 2.0 * sq;
+    if (threadIdx.x == 0) {
+      partial_store(g.part_norm + mi.norm_off + tile, diag ? sq : 2.0 * sq);
+      if (arrive(g.mat_cnt + task.mat, gram_tiles(n))) norm_decide(mi, g.part_norm, g.sc_out[task.mat], g.na);
+    }
   }
 }
 
@@ -1582,53 +1652,39 @@ __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs 
   }
 }
 
-// Per-matrix decisions from the norm partials (see NormMode, NormAction).
+// The per-matrix decisions of a phase end without a Gram launch (kActStop
+// only: nothing to sum).
 __global__ void gram_norm_final_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part,
                                        MatScalars* __restrict__ sc, int n_mat, NormArgs a) {
   const int m = blockIdx.x * blockDim.x + threadIdx.x;
   if (m >= n_mat) return;
-  MatScalars& o = sc[m];
-  if (a.only_active && !o.active) return;
-  const MatInfo mi = mats[m];
-  if (a.cls >= 0 && mi.sched != a.cls) return;
-  const int act = a.mode == kNormFirst ? kActNone : a.action[mi.sched];
-  if (a.mode != kNormFirst && act == kActNone) return;
-  if (act == kActStop) {
-    o.active = 0;
-    return;
-  }
-  double s = 0.0;
-  const int nt = gram_tiles(mi.n);
-  for (int x = 0; x < nt; ++x) s += part[mi.norm_off + x];
-  if (a.mode == kNormFirst) {
-    o.gscale = ((o.flags & kFlagInput) == 0 && s > 0.0) ? (float)(1.0 / sqrt(sqrt(s))) : 0.f;
-    return;
-  }
-  o.resid = (float)sqrt(s / mi.n);
-  if (act == kActSwitch) {
-    // stop at the end of this phase when every singular value is already at 1
-    const bool go_on = (o.flags & kFlagInput) == 0 && !(o.resid <= a.tol_switch);
-    // a matrix that still has a singular value away from 1 after the schedule
-    // for a bound at the float32 resolution of Delta has one below it: its
-    // direction in Q is decided by rounding, not by Delta
-    if (go_on && a.flag_below[mi.sched]) o.flags |= kFlagBelowResolution;
-    o.active = go_on ? 1 : 0;
-    o.steps = go_on ? a.steps_total[mi.sched] : a.steps_here;
-    o.qbuf = go_on ? a.buf_total[mi.sched] : a.buf_here;
-  } else {
-    if (a.flag_unconverged && !(o.resid <= 1e-3f) && (o.flags & kFlagInput) == 0) o.flags |= kFlagNotConverged;
-    o.active = 0;
-  }
+  if (a.only_active && !sc[m].active) return;
+  norm_decide(mats[m], part, sc[m], a);
+}
+
+// The scale of a correction (sigma_bar).  mode 0: <Q, Delta>_F / r, the mean
+// singular value (tr is <Q, Delta>_F); 1: ||Delta||_F / sqrt(r), their RMS;
+// 2: sqrt(rows / cols) of the tensor as stored (Muon's sqrt(fan_out / fan_in)).
+__device__ __forceinline__ void set_sigma(MatScalars& o, const MatInfo& mi, double tr, int mode) {
+  if (o.flags & kFlagNonfinite) o.sigma_bar = __builtin_nanf("");
+  else if (o.flags & kFlagZero) o.sigma_bar = 0.f;
+  else if (mode == 0) o.sigma_bar = (float)(tr / mi.n);
+  else if (mode == 1) o.sigma_bar = (float)((double)o.fro / sqrt((double)mi.n));
+  else o.sigma_bar = (float)(mi.wide ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
 }
 
 // <Q, Delta>_F partial per chunk of a corrected matrix (both in the
 // workspace layout: chunk_ws maps the chunk's elements; groups of 4 are
-// contiguous when c.vec).
+// contiguous when c.vec).  The last chunk of a matrix to arrive (counted in
+// mat_cnt) adds the matrix's partials in a fixed order (that of
+// block_sum_range) and sets its sigma_bar = <Q, Delta>_F / r.
 __global__ void __launch_bounds__(kStreamThreads)
-trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatScalars* __restrict__ sc,
-             const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ delta,
-             double* __restrict__ part_tr, int steps_lo, int steps_hi) {
+trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, const MatInfo* __restrict__ mats,
+             MatScalars* __restrict__ sc, const float* __restrict__ x0, const float* __restrict__ x1,
+             const float* __restrict__ delta, double* __restrict__ part_tr, int* __restrict__ mat_cnt, int steps_lo,
+             int steps_hi) {
   __shared__ double red[4];
+  __shared__ int last;
   const int ci = idx ? idx[blockIdx.x] : (int)blockIdx.x;
   const Chunk c = chunks[ci];
   const int st = sc[c.mat].steps;
@@ -1651,28 +1707,28 @@ trace_kernel(const Chunk* __restrict__ chunks, const int* __restrict__ idx, cons
     s += (double)q[o] * delta[o];
   }
   s = block_sum256(s, red);
-  if (threadIdx.x == 0) part_tr[ci] = s;
+  const MatInfo& mi = mats[c.mat];
+  if (threadIdx.x == 0) {
+    partial_store(part_tr + ci, s);
+    last = arrive(mat_cnt + c.mat, mi.chunk_end - mi.chunk_begin);
+  }
+  __syncthreads();
+  if (!last) return;
+  double t = 0.0;
+  for (int x = mi.chunk_begin + (int)threadIdx.x; x < mi.chunk_end; x += 256) t += partial_load(part_tr + x);
+  t = block_sum256(t, red);
+  if (threadIdx.x == 0) set_sigma(sc[c.mat], mi, t, 0);
 }
 
-// The scale of each correction.  mode 0: <Q, Delta>_F / r, the mean singular
-// value (from the trace partials); 1: ||Delta||_F / sqrt(r), their RMS;
-// 2: sqrt(rows / cols) of the tensor as stored (Muon's sqrt(fan_out / fan_in)).
+// The closed-form scales (modes 1 and 2 of set_sigma), one block per matrix.
 __global__ void __launch_bounds__(256)
-sigma_kernel(const MatInfo* __restrict__ mats, const double* __restrict__ part_tr,
-             MatScalars* __restrict__ sc, int n_mat, int mode, int cls, int steps_lo, int steps_hi) {
-  __shared__ double red[4];
+sigma_kernel(const MatInfo* __restrict__ mats, MatScalars* __restrict__ sc, int n_mat, int mode, int cls,
+             int steps_lo, int steps_hi) {
   const int m = blockIdx.x;
   const MatInfo mi = mats[m];
   if (cls >= 0 && mi.sched != cls) return;
   if (sc[m].steps < steps_lo || sc[m].steps > steps_hi) return;
-  const double s = mode == 0 ? block_sum_range(part_tr, mi.chunk_begin, mi.chunk_end, red) : 0.0;
-  if (threadIdx.x != 0) return;
-  MatScalars& o = sc[m];
-  if (o.flags & kFlagNonfinite) o.sigma_bar = __builtin_nanf("");
-  else if (o.flags & kFlagZero) o.sigma_bar = 0.f;
-  else if (mode == 0) o.sigma_bar = (float)(s / mi.n);
-  else if (mode == 1) o.sigma_bar = (float)((double)o.fro / sqrt((double)mi.n));
-  else o.sigma_bar = (float)(mi.wide ? sqrt((double)mi.n / mi.m) : sqrt((double)mi.m / mi.n));
+  if (threadIdx.x == 0) set_sigma(sc[m], mi, 0.0, mode);
 }
 
 // One element of the write-back: D = f p;  B <- mu B + D;  theta <- theta - lr (D + mu B)
@@ -1914,8 +1970,11 @@ hipError_t launch_gemm(const DevTables& t, int mode, const PolarStep& p, hipStre
   g.poly = t.poly;
   g.gpart = t.gpart;
   g.split_cnt = t.split_cnt;
+  g.mat_cnt = t.mat_cnt;
+  g.sc_out = t.scalars;
   g.part_norm = t.part_norm;
   g.norm_mode = mode == kGram ? p.norm_mode : -1;
+  g.na = p.norm;
   g.coef = t.coef;
   g.step = p.step;
   g.n_steps = t.n_steps;
@@ -1939,10 +1998,11 @@ hipError_t launch_scale(const DevTables& t, const StepArgs& a, hipStream_t st) {
   const int n = t.chunk_idx ? t.n_chunk_idx : t.n_iso_chunks;
   if (n == 0) return hipSuccess;
   if (a.scale == 0)
-    hipLaunchKernelGGL(trace_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.scalars,
-                       t.x[0], t.x[1], t.delta, t.part_tr, a.steps_lo, a.steps_hi);
-  hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.part_tr, t.scalars, t.n_mat,
-                     a.scale, t.cls, a.steps_lo, a.steps_hi);
+    hipLaunchKernelGGL(trace_kernel, dim3(n), dim3(kStreamThreads), 0, st, t.chunks, t.chunk_idx, t.mats,
+                       t.scalars, t.x[0], t.x[1], t.delta, t.part_tr, t.mat_cnt, a.steps_lo, a.steps_hi);
+  else
+    hipLaunchKernelGGL(sigma_kernel, dim3(t.n_mat), dim3(256), 0, st, t.mats, t.scalars, t.n_mat, a.scale, t.cls,
+                       a.steps_lo, a.steps_hi);
   return hipGetLastError();
 }
 
