@@ -33,15 +33,25 @@ PARTS = {"mixed": (5, 3), "bf16x3": (3, 3), "bf16x6": (6, 6), "fp32": (1, 1)}
 X6_STEPS = 3
 
 
-def gemm_flops_per_step(layout, stats, check, precision):
+def factored_count(m, n, steps, factored):
+    """Steps that a matrix took on n x n factors: those strictly inside the
+    tall class's window [first, end) (step first forms X_s's Gram and its
+    polynomial as usual), for a tall matrix (m >= 2n) that ran the window."""
+    first, end = factored
+    return end - first - 1 if end and m >= 2 * n and steps >= end else 0
+
+
+def gemm_flops_per_step(layout, stats, check, precision, factored=(0, 0)):
     """Algorithmic flops of the batched products of one outer step, returned as
     (fp32-equivalent flops, MFMA flops actually issued).  Per polar step of an
     m x n matrix (m >= n): the symmetric Gram X^T X (n (n+1) m: each of the
     n (n+1)/2 distinct entries is a length-m dot product), the symmetric
     polynomial A A (n (n+1) n) and the update X P (2 m n^2).  A matrix that took
     s steps forms s + 1 Grams with the check (the last one measures Q^T Q), s
-    polynomials and s updates.  Split-bf16 products issue one MFMA product per
-    part product (3, 5 or 6)."""
+    polynomials and s updates.  A factored step of a tall matrix replaces its
+    Gram and update by the n x n products A M (2 n^3), M B and M P (symmetric,
+    n (n+1) n each).  Split-bf16 products issue one MFMA product per part
+    product (3, 5 or 6)."""
     early, late = PARTS[precision]
     f = 0
     fm = 0
@@ -54,24 +64,31 @@ def gemm_flops_per_step(layout, stats, check, precision):
         upd = 2 * m * n * n
         s = st.steps
         e = min(s, X6_STEPS)
-        f += s * (gram + poly + upd) + (gram if check else 0)
-        fm += s * (gram + poly) * late + (e * early + (s - e) * late) * upd + (gram * late if check else 0)
+        k = factored_count(m, n, s, factored)
+        nn = 2 * n ** 3 + 2 * n * (n + 1) * n
+        f += s * (gram + poly + upd) + (gram if check else 0) + k * (nn - gram - upd)
+        fm += (s * (gram + poly) * late + (e * early + (s - e) * late) * upd + (gram * late if check else 0)
+               + k * (nn - gram - upd) * late)
     return f, fm
 
 
-def gemm_bytes_per_step(layout, stats):
+def gemm_bytes_per_step(layout, stats, factored=(0, 0)):
     """Algorithmic HBM bytes of the batched products of one outer step: per
     polar step of an m x n matrix (m >= n) the Gram reads X and writes A
     (4mn + 4n^2; a split-K Gram also writes and re-reads its slices), the
     polynomial reads A and writes P (8n^2), the update reads X and P and
-    writes X' (8mn + 4n^2); s steps form s + 1 Grams."""
+    writes X' (8mn + 4n^2); s steps form s + 1 Grams.  A factored step reads
+    two n x n operands and writes one in each of A M, M B and M P (36 n^2) in
+    place of its Gram and update."""
     b = 0
     for (_, r, c, kind), st in zip(layout, stats):
         if kind != 0:
             continue
         m, n = max(r, c), min(r, c)
         s = st.steps
+        k = factored_count(m, n, s, factored)
         b += (s + 1) * (4 * m * n + 4 * n * n) + s * (8 * n * n) + s * (8 * m * n + 4 * n * n)
+        b += k * (36 * n * n - (4 * m * n + 4 * n * n) - (8 * m * n + 4 * n * n))
     return b
 
 
@@ -215,6 +232,8 @@ def main():
                          "clip_low: Section 4.5 (only the singular values above / below the mean set to it)")
     ap.add_argument("--streams", type=int, default=0, choices=[0, 1, 2],
                     help="streams of the polar iteration (0: the library's default)")
+    ap.add_argument("--factored", type=int, default=0, choices=[0, 1, 2],
+                    help="tall matrices' factored steps: 1 on, 2 off (0: the library's default, on)")
     ap.add_argument("--phase-tall", type=float, nargs=3, default=[0.0, 0.0, 0.0],
                     help="phase bounds of the polar schedule of tall matrices, m >= 2n (0: the library's "
                          "default, negative: end of the list; a negative first bound: one phase)")
@@ -248,7 +267,8 @@ def main():
              "clip_high": dict(clip=iso.ISOLOCO_CLIP_HIGH), "clip_low": dict(clip=iso.ISOLOCO_CLIP_LOW)}[args.variant]
     plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, wdt, opts=dict(precision=prec, phase_tall=tuple(args.phase_tall),
                                                                        phase_square=tuple(args.phase_square),
-                                                                       streams=args.streams, **vopts),
+                                                                       streams=args.streams, factored=args.factored,
+                                                                       **vopts),
                            device=dev)
     phase_ends = {"square": plan.schedule_phases(tall=0), "tall": plan.schedule_phases(tall=1)}
     stream = torch.cuda.current_stream(dev)
@@ -315,7 +335,8 @@ def main():
     n_below = sum(1 for s, t in zip(st, cfg.layout) if t[3] == 0 and s.flags & iso.ISOLOCO_FLAG_BELOW_RESOLUTION)
     n_unconv = sum(1 for s, t in zip(st, cfg.layout) if t[3] == 0 and s.flags & iso.ISOLOCO_FLAG_NOT_CONVERGED)
 
-    flops, mfma_flops = gemm_flops_per_step(cfg.layout, st, True, args.precision)
+    factored = plan.factored_steps()
+    flops, mfma_flops = gemm_flops_per_step(cfg.layout, st, True, args.precision, factored)
     steps_hist = {}
     for sti, t in zip(st, cfg.layout):
         if t[3] == 0:
@@ -337,7 +358,7 @@ def main():
     sum_gbs = worker_sum_ceiling_gbs(torch, workers)
     fbytes = finish_bytes(cfg.layout)
     fin_gbs = fbytes / (per["finish_ms"] * 1e-3) / 1e9
-    gbytes = gemm_bytes_per_step(cfg.layout, st)
+    gbytes = gemm_bytes_per_step(cfg.layout, st, factored)
     mt = MEASURED_TRAFFIC
     measured = (mt["sources_sha256"] == sources_sha256() and mt["workload"] == args.workload
                 and mt["precision"] == args.precision and args.variant == "exact")
@@ -360,7 +381,8 @@ def main():
         "config": {"workload": cfg.name, "K": cfg.K, "params": cfg.n_params,
                    "matrices": sum(1 for t in cfg.layout if t[3] == 0), "worker_dtype": cfg.worker_dtype,
                    "variant": args.variant,
-                   "polar_phase_ends": phase_ends, "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
+                   "polar_phase_ends": phase_ends, "tall_factored_steps": list(factored),
+                   "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
         "roofline": {"bound": "mfma", "kernel": "batched polar products (gemm_%s: Gram, polynomial, update)" %
                      ("f32_kernel" if args.precision == "fp32" else "bf16_kernel, gemm_bf16_big_kernel"),
                      "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",

@@ -145,6 +145,17 @@ typedef struct {
                         scale), so that each fills the other's launch gaps and last waves;
                         0 (default): 2 when the corrected matrices hold at most 2^28
                         elements, else 1 (large products compete for the caches instead)  */
+  int32_t factored;  /* 1: the tall matrices take the steps from s to the end of their first
+                        phase on n x n factors: with A = X_s^T X_s, X_k = X_s M gives
+                        X_k^T X_k = M A M, so each step is M <- M p_k(M A M) (n x n products
+                        only) and X = X_s M is formed once at the phase end, where the check
+                        runs as before (Section 4.3's polar factor by polynomial steps,
+                        reorganised; the same steps and coefficients).  s is the first step
+                        after which the phase's lower bound has grown to 1/4 (so that A is
+                        well conditioned; 4 for the default phases), moved on by one so that
+                        the phase end - s is odd, with at least 3 steps left; 2: every step
+                        on the m x n iterate; 0 (default): 1.  Not with ORTH_NS5
+                        (isoloco_factored_steps reports the steps)                        */
 } isoloco_options;
 
 #define ISOLOCO_PREC_MIXED 0
@@ -275,6 +286,10 @@ isoloco_status isoloco_schedule(isoloco_plan_t plan, int32_t tall, double* coeff
  * entries; *n_phases receives the count.  Host only. */
 isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t tall, int32_t* ends, int32_t max_phases,
                                        int32_t* n_phases);
+
+/* The steps [*first, *end) that the tall matrices take on n x n factors
+ * (isoloco_options.factored); both 0 when none.  Host only. */
+isoloco_status isoloco_factored_steps(isoloco_plan_t plan, int32_t* first, int32_t* end);
 
 /* Per-kernel timing of the last aggregate, measured with HIP events recorded
  * on the aggregate's stream around every launch (enable first; the events

@@ -16,6 +16,7 @@ __all__ = [
     "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
     "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
     "isoloco_timing", "isoloco_aggregate_static", "ISOLOCO_STATIC_WORKSPACE_BYTES",
+    "isoloco_factored_steps",
     "IsoLoCoPlan", "LIB_PATH", "EXPORTED_SYMBOLS",
 ]
 
@@ -51,7 +52,7 @@ EXPORTED_SYMBOLS = (
     "isoloco_plan", "isoloco_workspace_size", "isoloco_set_workspace", "isoloco_aggregate",
     "isoloco_get_stats", "isoloco_schedule", "isoloco_schedule_phases", "isoloco_plan_destroy",
     "isoloco_status_string", "isoloco_last_error", "isoloco_enable_timing", "isoloco_get_timing",
-    "isoloco_aggregate_static",
+    "isoloco_aggregate_static", "isoloco_factored_steps",
 )
 
 
@@ -65,7 +66,8 @@ class isoloco_options(ctypes.Structure):
                 ("check", ctypes.c_int32), ("precision", ctypes.c_int32),
                 ("orth", ctypes.c_int32), ("scale", ctypes.c_int32), ("momentum", ctypes.c_int32),
                 ("target", ctypes.c_int32), ("clip", ctypes.c_int32), ("phase_tall", ctypes.c_float * 3),
-                ("phase_square", ctypes.c_float * 3), ("streams", ctypes.c_int32)]
+                ("phase_square", ctypes.c_float * 3), ("streams", ctypes.c_int32),
+                ("factored", ctypes.c_int32)]
 
 
 class isoloco_tensor_stats(ctypes.Structure):
@@ -109,6 +111,7 @@ _sig = {
                                         ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "isoloco_schedule_phases": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                                ctypes.POINTER(ctypes.c_int32)]),
+    "isoloco_factored_steps": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]),
     "isoloco_plan_destroy": (ctypes.c_int, [_P]),
     "isoloco_enable_timing": (ctypes.c_int, [_P, ctypes.c_int32]),
     "isoloco_get_timing": (ctypes.c_int, [_P, ctypes.POINTER(isoloco_timing)]),
@@ -210,6 +213,14 @@ def isoloco_schedule_phases(plan, max_phases=16, tall=0):
     return [buf[i] for i in range(min(n.value, max_phases))]
 
 
+def isoloco_factored_steps(plan):
+    """The steps [first, end) that the tall matrices take on n x n factors ((0, 0): none)."""
+    a = ctypes.c_int32()
+    b = ctypes.c_int32()
+    _check(_lib.isoloco_factored_steps(plan, ctypes.byref(a), ctypes.byref(b)), "isoloco_factored_steps")
+    return a.value, b.value
+
+
 def isoloco_enable_timing(plan, enable=True):
     _check(_lib.isoloco_enable_timing(plan, 1 if enable else 0), "isoloco_enable_timing")
 
@@ -300,6 +311,9 @@ class IsoLoCoPlan:
 
     def schedule_phases(self, tall=0):
         return isoloco_schedule_phases(self.handle, tall=tall)
+
+    def factored_steps(self):
+        return isoloco_factored_steps(self.handle)
 
     def close(self):
         if self.handle is not None:

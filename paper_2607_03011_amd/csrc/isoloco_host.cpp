@@ -86,6 +86,18 @@ constexpr float kResolutionBound = 2e-8f;
 constexpr float kSwitchTol = 5e-5f;
 // Default streams = 2 for plans whose corrected matrices hold at most this many elements.
 constexpr int64_t kTwoStreamMaxElems = (int64_t)1 << 28;
+// The tall class iterates on n x n factors from step s to the end of its
+// first phase: X_k = X_s M with A = X_s^T X_s makes X_k^T X_k = M A M, so
+// those steps need n x n products only (M <- M p(M A M)), and X = X_s M is
+// formed once at the phase end.  A carries the squared condition number of
+// X_s and rounding errors of A reach M A M amplified by ||M||^2, about
+// 1 / l_s^2 for the image l_s of the phase's lower bound after s steps; s is
+// the first step with l_s >= kFactorMinBound.  Split-bf16 emulation of the
+// 2048 x 768 workload matrices and of planted spectra (sigma_min 1e-2 ..
+// 1e-8) under the default first phase (bound 1e-3) matched the plain
+// iteration's accuracy and step counts from step 4 on (l_4 = 0.30), while
+// from step 3 (l_3 = 0.08) or 2 (0.02) the results were worse or diverged.
+constexpr double kFactorMinBound = 0.25;
 // In the mixed precision mode the update products of the first kX6Steps steps
 // use bf16x5 (X in 3 bf16 parts, P' in 2), everything else bf16x3.  Those
 // early updates X' = X P' carry the large coefficients of the steps that
@@ -347,11 +359,19 @@ struct isoloco_plan_s {
   std::vector<float> phase_bound[kSchedClasses];  // the bound each phase was built for
   int n_steps = 0;            // longest schedule: polar steps the launch sequence runs
   std::vector<float> coef;    // device table: [class][n_steps][3], padded with each class's last step
+  // The tall class's factored steps [cont_from, cont_to) (both 0: none): each
+  // tall matrix as an n x n operand (cmats, same sq_off as in mats) and the
+  // Gram and update task lists over those
+  int cont_from = 0, cont_to = 0;
+  std::vector<MatInfo> cmats;
+  TaskListHost cont_gram, cont_update;
   int64_t n2d = 0;   // elements of one Delta / X buffer
   int64_t nsq = 0;   // elements of one Gram / polynomial buffer
+  int64_t nsq_tall = 0;  // the tall matrices' part of it (their n x n buffers come first)
   int64_t npart = 0; // elements of the split-K partial buffer
   size_t off_mats = 0, off_chunks = 0, off_gt = 0, off_pt = 0, off_ut = 0, off_sc = 0;
   size_t off_pnorm = 0, off_cnt = 0, off_mcnt = 0, off_coef = 0;
+  size_t off_cm = 0, off_cgt = 0, off_cut = 0, off_cx = 0, off_cy = 0;  // factored steps
   size_t off_gtc[kSchedClasses] = {}, off_ptc[kSchedClasses] = {}, off_utc[kSchedClasses] = {};
   size_t off_cic[kSchedClasses] = {};
   // the second stream of the per-class mode, with its fork and join events
@@ -451,7 +471,6 @@ void plan_matrices(isoloco_plan_s* p) {
     mi.n = (int32_t)std::min(T.rows, T.cols);
     mi.src_off = T.offset;
     mi.ws_off = ws;
-    mi.sq_off = sq;
     mi.vec = (mi.m % 4 == 0 && mi.n % 4 == 0) ? 1 : 0;
     mi.tensor = (int32_t)t;
     mi.sched = mi.m >= 2 * (int64_t)mi.n ? kSchedTall : kSchedSquare;
@@ -516,7 +535,32 @@ void plan_matrices(isoloco_plan_s* p) {
     p->mat_of_tensor[t] = (int)p->mats.size();
     p->mats.push_back(mi);
     ws += (cnt + 63) / 64 * 64;
-    sq += ((int64_t)mi.n * mi.n + 63) / 64 * 64;
+  }
+  // the n x n buffers of the tall matrices first: the factored steps' own
+  // buffers then cover [0, nsq_tall) only
+  for (int pass = 0; pass < 2; ++pass) {
+    for (MatInfo& mi : p->mats)
+      if ((mi.sched == kSchedTall) == (pass == 0)) {
+        mi.sq_off = sq;
+        sq += ((int64_t)mi.n * mi.n + 63) / 64 * 64;
+      }
+    if (pass == 0) p->nsq_tall = sq;
+  }
+  // each tall matrix as an n x n operand of the factored steps: column-major
+  // like the iterates, at its own sq_off in every n x n buffer, one K slice
+  for (const MatInfo& mi : p->mats) {
+    if (mi.sched != kSchedTall) continue;
+    MatInfo c = mi;
+    c.m = mi.n;
+    c.ws_off = mi.sq_off;
+    c.ksplit = 1;
+    c.kchunk = (mi.n + 31) / 32 * 32;
+    c.part_off = 0;
+    c.cnt_off = -1;
+    c.vec = mi.n % 4 == 0 ? 1 : 0;
+    c.wide = 0;
+    c.chunk_begin = c.chunk_end = 0;
+    p->cmats.push_back(c);
   }
   p->n_iso_chunks = (int)p->chunks.size();
   for (int i = 0; i < p->n_iso_chunks; ++i) p->chunk_cls[p->mats[p->chunks[i].mat].sched].push_back(i);
@@ -546,10 +590,11 @@ void plan_matrices(isoloco_plan_s* p) {
   // the rest.  (The planner makes every iterate column-major; the kernels
   // take either layout, per task in the shared segment 0.)
   std::vector<Task> seg[3], big[2], rem[3];
+  const std::vector<MatInfo>* table = &p->mats;  // the matrices the tasks index
   auto flush = [&](TaskListHost& L, bool by_slice) {
     L.tasks.clear();
     auto append = [&](std::vector<Task>& v, int& off, int& cnt) {
-      const std::vector<Task> o = xcd_order(p->mats, v, by_slice);
+      const std::vector<Task> o = xcd_order(*table, v, by_slice);
       off = (int)L.tasks.size();
       cnt = (int)o.size();
       L.tasks.insert(L.tasks.end(), o.begin(), o.end());
@@ -583,16 +628,18 @@ void plan_matrices(isoloco_plan_s* p) {
   };
   // The lists of every matrix (one stream), and of each schedule class alone
   // (a stream per class).
-  auto build_lists = [&](int cls, TaskListHost& G, TaskListHost& P, TaskListHost& U) {
+  auto build_lists = [&](const std::vector<MatInfo>& mats, int cls, TaskListHost& G, TaskListHost& P,
+                         TaskListHost& U) {
+    table = &mats;
     split_layouts = false;
     std::vector<int> order;
-    for (size_t i = 0; i < p->mats.size(); ++i)
-      if (cls < 0 || p->mats[i].sched == cls) order.push_back((int)i);
+    for (size_t i = 0; i < mats.size(); ++i)
+      if (cls < 0 || mats[i].sched == cls) order.push_back((int)i);
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
-      return (int64_t)p->mats[a].kchunk > (int64_t)p->mats[b].kchunk;
+      return (int64_t)mats[a].kchunk > (int64_t)mats[b].kchunk;
     });
     for (int mi : order) {
-      const MatInfo& M = p->mats[mi];
+      const MatInfo& M = mats[mi];
       const int T = (M.n + kBM - 1) / kBM;
       // the Gram matrix is symmetric: tiles on and above the diagonal only
       for (int ks = 0; ks < M.ksplit; ++ks) {
@@ -604,9 +651,9 @@ void plan_matrices(isoloco_plan_s* p) {
       }
     }
     flush(G, true);
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->mats[a].n > p->mats[b].n; });
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return mats[a].n > mats[b].n; });
     for (int mi : order) {
-      const MatInfo& M = p->mats[mi];
+      const MatInfo& M = mats[mi];
       const int T = (M.n + kBM - 1) / kBM;
       const bool kin = M.n % 32 == 0;
       for (int a = 0; a < T; ++a)
@@ -616,7 +663,7 @@ void plan_matrices(isoloco_plan_s* p) {
     flush(P, false);
     split_layouts = true;
     for (int mi : order) {
-      const MatInfo& M = p->mats[mi];
+      const MatInfo& M = mats[mi];
       const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
       const int TM2 = M.m / 256, TN2 = M.n / 256;
       const bool kin = M.n % 32 == 0;
@@ -627,8 +674,11 @@ void plan_matrices(isoloco_plan_s* p) {
     }
     flush(U, false);
   };
-  build_lists(-1, p->gram_list, p->poly_list, p->update_list);
-  for (int c = 0; c < kSchedClasses; ++c) build_lists(c, p->gram_cls[c], p->poly_cls[c], p->update_cls[c]);
+  build_lists(p->mats, -1, p->gram_list, p->poly_list, p->update_list);
+  for (int c = 0; c < kSchedClasses; ++c)
+    build_lists(p->mats, c, p->gram_cls[c], p->poly_cls[c], p->update_cls[c]);
+  TaskListHost unused;
+  build_lists(p->cmats, -1, p->cont_gram, unused, p->cont_update);
 }
 
 void plan_workspace(isoloco_plan_s* p) {
@@ -665,6 +715,12 @@ void plan_workspace(isoloco_plan_s* p) {
   p->off_gram = take((size_t)p->nsq * sizeof(float));
   p->off_poly = take((size_t)p->nsq * sizeof(float));
   p->off_gpart = take((size_t)p->npart * sizeof(float));
+  const bool cont = p->cont_to > 0;
+  p->off_cm = take(cont ? p->cmats.size() * sizeof(MatInfo) : 0);
+  p->off_cgt = take(cont ? p->cont_gram.tasks.size() * sizeof(Task) : 0);
+  p->off_cut = take(cont ? p->cont_update.tasks.size() * sizeof(Task) : 0);
+  p->off_cx = take(cont ? (size_t)p->nsq_tall * sizeof(float) : 0);
+  p->off_cy = take(cont ? (size_t)p->nsq_tall * sizeof(float) : 0);
   p->total = o;
 }
 
@@ -693,6 +749,19 @@ DevTables class_tables(const isoloco_plan_s* p, const char* w, const DevTables& 
   d.chunk_idx = reinterpret_cast<const int*>(w + p->off_cic[c]);
   d.n_chunk_idx = (int)p->chunk_cls[c].size();
   d.cls = c;
+  return d;
+}
+
+// The tables of the factored steps: every tall matrix as an n x n operand
+// (cmats), with the Gram and update lists over those; the buffers are set
+// per launch.
+DevTables cont_tables(const isoloco_plan_s* p, const char* w, const DevTables& t) {
+  DevTables d = t;
+  d.mats = reinterpret_cast<const MatInfo*>(w + p->off_cm);
+  d.gram_list = dev_list(w, p->cont_gram, p->off_cgt);
+  d.update_list = dev_list(w, p->cont_update, p->off_cut);
+  d.poly_list = TaskList{};
+  d.n_mat = (int)p->cmats.size();
   return d;
 }
 
@@ -743,6 +812,13 @@ hipError_t upload_tables(const isoloco_plan_s* plan, char* w) {
       (e = up(plan->off_pt, plan->poly_list.tasks.data(), plan->poly_list.tasks.size() * sizeof(Task))) != hipSuccess ||
       (e = up(plan->off_ut, plan->update_list.tasks.data(), plan->update_list.tasks.size() * sizeof(Task))) != hipSuccess ||
       (e = up(plan->off_coef, plan->coef.data(), plan->coef.size() * sizeof(float))) != hipSuccess)
+    return e;
+  if (plan->cont_to > 0 &&
+      ((e = up(plan->off_cm, plan->cmats.data(), plan->cmats.size() * sizeof(MatInfo))) != hipSuccess ||
+       (e = up(plan->off_cgt, plan->cont_gram.tasks.data(), plan->cont_gram.tasks.size() * sizeof(Task))) !=
+           hipSuccess ||
+       (e = up(plan->off_cut, plan->cont_update.tasks.data(), plan->cont_update.tasks.size() * sizeof(Task))) !=
+           hipSuccess))
     return e;
   for (int c = 0; c < kSchedClasses; ++c)
     if ((e = up(plan->off_gtc[c], plan->gram_cls[c].tasks.data(), plan->gram_cls[c].tasks.size() * sizeof(Task))) !=
@@ -801,6 +877,8 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
   }
   if (o.streams != 0 && o.streams != 1 && o.streams != 2)
     return fail(ISOLOCO_ERR_INVALID_ARG, "streams must be 0, 1 or 2");
+  if (o.factored == 0) o.factored = 1;
+  if (o.factored != 1 && o.factored != 2) return fail(ISOLOCO_ERR_INVALID_ARG, "factored must be 0, 1 or 2");
   if (o.max_steps < 1 || o.max_steps > 200)
     return fail(ISOLOCO_ERR_INVALID_ARG, "max_steps = %d outside [1, 200]", o.max_steps);
   if (!(o.ell0 > 0.f && o.ell0 < 1.f)) return fail(ISOLOCO_ERR_INVALID_ARG, "ell0 must be in (0, 1)");
@@ -872,6 +950,25 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
                    p->phase_bound[c]);
     p->n_steps = 0;
     for (int c = 0; c < kSchedClasses; ++c) p->n_steps = std::max(p->n_steps, p->phase_end[c].back());
+    // The tall class's factored steps: from the first step s whose image of
+    // the first phase's bound reaches kFactorMinBound to the end of that
+    // phase.  X_s and the phase's result sit in different X buffers (the
+    // result of step k goes to x[k & 1]), so s and the phase end differ in
+    // parity (s moves on by one if not), and at least two steps remain after
+    // s, else nothing is saved.
+    if (o.factored != 2 && o.orth == ISOLOCO_ORTH_POLAR && !p->cmats.empty()) {
+      const std::vector<double>& sc = p->sched[kSchedTall];
+      const int e1 = p->phase_end[kSchedTall][0];
+      double l = p->phase_bound[kSchedTall][0];
+      for (int k = 1; k <= e1 - 3; ++k) {
+        l = peval(&sc[3 * (k - 1)], l);
+        if (l >= kFactorMinBound && (e1 - k) % 2 == 1) {
+          p->cont_from = k;
+          p->cont_to = e1;
+          break;
+        }
+      }
+    }
     p->coef.assign((size_t)kSchedClasses * p->n_steps * 3, 0.f);
     for (int c = 0; c < kSchedClasses; ++c)
       for (int k = 0; k < p->n_steps; ++k) {
@@ -1063,6 +1160,61 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
         ps.norm.mode = mode;
         return gram(ps);
       };
+      // Steps cont_from .. cont_to - 1 of the tall matrices on n x n factors,
+      // after step s = cont_from's Gram A = X_s^T X_s (in tt.gram, left there
+      // throughout): M = p_s(A), then for each step k B = A M, A_k = M B,
+      // P = p_k(A_k), M <- M P, and at the end X = X_s M in the buffer that
+      // step cont_to - 1 writes.  M and A_k take turns in the plan's two n x n
+      // buffers of the tall matrices, B and P the polynomial buffer.  The
+      // n x n launches run every tall matrix (only_active = 0: none has
+      // stopped before its first phase end).
+      const int prec = plan->opts.precision;
+      auto factored_steps = [&](const PolarStep& ps) -> hipError_t {
+        hipError_t q;
+        const DevTables tc = cont_tables(plan, ws, tt);
+        float* cur = reinterpret_cast<float*>(ws + plan->off_cx);
+        float* oth = reinterpret_cast<float*>(ws + plan->off_cy);
+        DevTables t1 = tt;
+        t1.poly = cur;
+        PolarStep p1 = ps;
+        p1.arith = step_arith(prec, ps.step, kProdPoly);
+        if ((q = timed_on(s, kPhPoly, [&] { return launch_gemm(t1, 1, p1, s); })) != hipSuccess) return q;
+        for (int k = plan->cont_from + 1; k < plan->cont_to; ++k) {
+          DevTables ta = tc, tb = tc, tp = tt;
+          ta.poly = cur;  // B = A M
+          tb.gram = oth;  // A_k = M^T B (M symmetric), then M P
+          tp.gram = oth;  // P = p_k(A_k)
+          PolarStep pa{}, pb{}, pp{};
+          pa.xin = tt.gram;
+          pa.xout = tt.poly;
+          pa.step = k;
+          pa.arith = step_arith(prec, k, kProdUpdate);
+          pb.xin = cur;
+          pb.bin = tt.poly;
+          pb.step = k;
+          pb.arith = step_arith(prec, k, kProdGram);
+          pp.step = k;
+          pp.only_active = 1;
+          pp.arith = step_arith(prec, k, kProdPoly);
+          if ((q = timed_on(s, kPhUpdate, [&] { return launch_gemm(ta, 2, pa, s); })) != hipSuccess ||
+              (q = timed_on(s, kPhGram, [&] { return launch_gemm(tb, 0, pb, s); })) != hipSuccess ||
+              (q = timed_on(s, kPhPoly, [&] { return launch_gemm(tp, 1, pp, s); })) != hipSuccess ||
+              (q = timed_on(s, kPhGram, [&] { return launch_gemm(tb, 0, pb, s); })) != hipSuccess)
+            return q;
+          std::swap(cur, oth);
+        }
+        DevTables tq = tt;
+        tq.poly = cur;
+        PolarStep pq{};
+        pq.xin = ps.xin;
+        pq.xout = tt.x[(plan->cont_to - 1) & 1];
+        pq.step = plan->cont_to - 1;
+        pq.only_active = 1;
+        pq.arith = step_arith(prec, plan->cont_to - 1, kProdUpdate);
+        return timed_on(s, kPhUpdate, [&] { return launch_gemm(tq, 2, pq, s); });
+      };
+      const bool factored =
+          plan->cont_to > 0 && (cls == kSchedTall || (cls < 0 && n_cls[kSchedSquare] == 0));
       const float* xin = tt.delta;
       bool have_gram = false;  // the Gram of xin was formed by the last phase end's check
       for (int k = 0; k < Sx; ++k) {
@@ -1076,13 +1228,19 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
         what = "polar step launch";
         // (the fast variant keeps X0 = Delta / ||Delta||_F: no Gram-norm scaling)
         if (!have_gram && (r = (k == 0 && !ns5) ? gram_norm(ps, kNormFirst) : gram(ps)) != hipSuccess) return r;
-        PolarStep pp = ps, pu = ps;
-        pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
-        pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
-        if ((r = timed_on(s, kPhPoly, [&] { return launch_gemm(tt, 1, pp, s); })) != hipSuccess ||
-            (r = timed_on(s, kPhUpdate, [&] { return launch_gemm(tt, 2, pu, s); })) != hipSuccess)
-          return r;
-        xin = ps.xout;
+        if (factored && k == plan->cont_from) {
+          if ((r = factored_steps(ps)) != hipSuccess) return r;
+          k = plan->cont_to - 1;
+          xin = tt.x[k & 1];
+        } else {
+          PolarStep pp = ps, pu = ps;
+          pp.arith = step_arith(plan->opts.precision, k, kProdPoly);
+          pu.arith = step_arith(plan->opts.precision, k, kProdUpdate);
+          if ((r = timed_on(s, kPhPoly, [&] { return launch_gemm(tt, 1, pp, s); })) != hipSuccess ||
+              (r = timed_on(s, kPhUpdate, [&] { return launch_gemm(tt, 2, pu, s); })) != hipSuccess)
+            return r;
+          xin = ps.xout;
+        }
         have_gram = false;
         bool any = false, residual = false;
         for (int c = 0; c < kSchedClasses; ++c) {
@@ -1152,7 +1310,16 @@ static isoloco_status aggregate_on(isoloco_plan_t plan, char* ws, bool use_side,
       what = "fro launch";
       if ((r = timed(kPhOther, [&] { return launch_fro(tt, fa, st); })) != hipSuccess) return r;
       if (!two) {
-        if ((r = iterate(tt, check, -1, st)) != hipSuccess) return r;
+        if (plan->cont_to > 0 && n_cls[kSchedTall] > 0 && n_cls[kSchedSquare] > 0) {
+          // the tall class's factored steps need launches of its own: the
+          // classes one after the other (each matrix's arithmetic is that of
+          // the shared launches)
+          if ((r = iterate(class_tables(plan, ws, tt, kSchedTall), check, kSchedTall, st)) != hipSuccess ||
+              (r = iterate(class_tables(plan, ws, tt, kSchedSquare), check, kSchedSquare, st)) != hipSuccess)
+            return r;
+        } else if ((r = iterate(tt, check, -1, st)) != hipSuccess) {
+          return r;
+        }
         return with_tail ? tail(tt, st) : hipSuccess;
       }
       // fork: the second stream waits for the scalars; join at the end
@@ -1369,6 +1536,13 @@ isoloco_status isoloco_schedule_phases(isoloco_plan_t plan, int32_t tall, int32_
   *n_phases = n;
   if (ends)
     for (int i = 0; i < std::min<int>(n, std::max(max_phases, 0)); ++i) ends[i] = pe[i];
+  return ISOLOCO_OK;
+}
+
+isoloco_status isoloco_factored_steps(isoloco_plan_t plan, int32_t* first, int32_t* end) {
+  if (!plan || !first || !end) return fail(ISOLOCO_ERR_INVALID_ARG, "NULL argument");
+  *first = plan->cont_from;
+  *end = plan->cont_to;
   return ISOLOCO_OK;
 }
 

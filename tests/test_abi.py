@@ -62,7 +62,8 @@ def test_plan_rejects(layout, n, K, dtype, err):
                                   dict(phase_square=(1e-4, 1e-5, float("nan"))), dict(streams=3), dict(orth=2),
                                   dict(scale=3), dict(momentum=-1),
                                   dict(target=2), dict(orth=1), dict(orth=1, scale=0), dict(clip=3),
-                                  dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1)])
+                                  dict(clip=1, scale=1), dict(clip=2, orth=1, scale=1), dict(factored=3),
+                                  dict(factored=-1)])
 def test_plan_rejects_options(opts):
     with pytest.raises(iso.IsoLoCoError) as ei:
         iso.isoloco_plan(LAY, 8256, 4, 0, opts)
@@ -244,3 +245,49 @@ def test_variant_options_accepted():
     for o in [dict(scale=1), dict(scale=2), dict(momentum=1), dict(target=1), dict(target=1, momentum=1),
               dict(orth=1, scale=1, momentum=1, target=1), dict(clip=1), dict(clip=2, momentum=1, target=1)]:
         iso.isoloco_plan_destroy(iso.isoloco_plan(LAY, 8256, 4, 0, o))
+
+
+def _expected_window(sched, e1, b0, min_bound=0.25):
+    """The first step k after which the image of the first phase's bound b0
+    reaches 1/4, with e1 - k odd (X_k and the phase's result in different
+    buffers) and at least 3 steps left; (0, 0) if none."""
+    lo = b0
+    for k in range(1, e1 - 2):
+        a, b, c = sched[k - 1]
+        lo = lo * (a + lo * lo * (b + lo * lo * c))
+        if lo >= min_bound and (e1 - k) % 2 == 1:
+            return k, e1
+    return 0, 0
+
+
+def test_factored_steps_window():
+    """The tall class takes the steps from s to the end of its first phase on
+    n x n factors, where s is the first step after which the phase's lower
+    bound has grown to 1/4 (4 with the default phases) and s, e1 differ in
+    parity; a single phase for [1e-10, 1] starts late."""
+    lay = [(0, 256, 64, 0), (16384, 64, 64, 0), (20480, 64, 1, 1)]  # tall, square, vector
+    h = iso.isoloco_plan(lay, 20544, 4)
+    assert iso.isoloco_schedule_phases(h, tall=1)[0] == 7
+    assert iso.isoloco_factored_steps(h) == (4, 7)
+    iso.isoloco_plan_destroy(h)
+    parities = set()
+    for b0 in (0.5, 0.1, 3e-2, 1e-2, 3e-3, 1e-3, 3e-4, 1e-4, 1e-5, 1e-7, 1e-8, -1.0):
+        h = iso.isoloco_plan(lay, 20544, 4, 0, dict(phase_tall=(b0, -1.0, 0)))
+        e1 = iso.isoloco_schedule_phases(h, tall=1)[0]
+        sched = iso.isoloco_schedule(h, tall=1)
+        first, end = iso.isoloco_factored_steps(h)
+        iso.isoloco_plan_destroy(h)
+        want = _expected_window(sched, e1, b0 if b0 > 0 else 1e-10)
+        assert (first, end) == want, (b0, e1, first, end)
+        if end:
+            parities.add(e1 % 2)
+            assert end - first >= 3
+        if b0 == 1e-3:
+            assert first == 4
+        if b0 < 0:  # one phase for [1e-10, 1]: its bound grows slowly
+            assert first == 0 or first >= 10
+    assert parities == {0, 1}
+    for opts, layout in ((dict(factored=2), lay), (dict(orth=1, scale=1), lay), ({}, [(0, 64, 64, 0)])):
+        h = iso.isoloco_plan(layout, 20544, 4, 0, opts)
+        assert iso.isoloco_factored_steps(h) == (0, 0), opts
+        iso.isoloco_plan_destroy(h)
