@@ -96,9 +96,9 @@ def gemm_bytes_per_step(layout, stats, factored=(0, 0)):
 # device copy; summaries in profiles/) for the default workload and precision.  It is
 # reported only while the kernel and planner sources are the ones it was measured on.
 MEASURED_TRAFFIC = {
-    "sources_sha256": "c1a6e58a7b0979696379fa59ce953d717adf5ce67dca3e3b82ed720cbfc3124d",
+    "sources_sha256": "3ca8733d67249518fce6c70bca91f9e67607cfc6b9c4978287d4257c08f10256",
     "workload": "llama-12L-d768-V32000-K16", "precision": "mixed",
-    "gemm_bytes_per_step": 25.61e9, "reduce_bytes_per_launch": 7.891e9, "finish_bytes_per_step": 2.197e9,
+    "gemm_bytes_per_step": 24.10e9, "reduce_bytes_per_launch": 7.890e9, "finish_bytes_per_step": 2.197e9,
 }
 
 
@@ -212,6 +212,50 @@ def cpu_baseline(cfg, theta, workers, mom, budget_s, variant=None):
                        len(os.sched_getaffinity(0)))}
 
 
+def _oracle_tensor(job):
+    """One tensor of the float64 oracle's outer step (a pool worker): its CPU seconds."""
+    import oracle
+    lay, th, ws, mo, alpha, lr, mu, variant = job
+    t0 = time.process_time()
+    oracle.outer_step([lay], th, ws, mo, alpha, lr, mu, variant=variant)
+    return time.process_time() - t0
+
+
+def cpu_full_step(cfg, theta, workers, mom, variant=None):
+    """The float64 oracle on every tensor of the step, in a pool of freshly
+    started processes (nothing forked after the GPU was used; one thread each,
+    as many as the host's cores up to 16, a one-GPU machine's CPU share), largest
+    tensors first: the step's wall time, with its total CPU time."""
+    import multiprocessing as mp
+    th = theta.cpu().numpy()
+    mo = mom.cpu().numpy()
+    jobs = []
+    for off, r, c, kind in sorted(cfg.layout, key=lambda t: -t[1] * t[2]):
+        sl = slice(off, off + r * c)
+        ws = list(workers[:, sl].float().cpu().numpy())
+        jobs.append(((0, r, c, kind), th[sl], ws, mo[sl], cfg.alpha, cfg.outer_lr, cfg.mu, variant))
+    procs = max(1, min(16, len(os.sched_getaffinity(0)), len(jobs)))
+    saved = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS")}
+    os.environ["OMP_NUM_THREADS"] = "1"  # read by the children's libraries as they load
+    os.environ["OPENBLAS_NUM_THREADS"] = "1"
+    try:
+        t0 = time.time()
+        with mp.get_context("spawn").Pool(procs) as pool:
+            cpu = pool.map(_oracle_tensor, jobs, chunksize=1)
+        wall = time.time() - t0
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    return {"value": wall * 1e3, "unit": "ms per outer step (whole step, wall clock)", "cores": procs,
+            "kind": "oracle",
+            "sample": "float64 oracle on all %d tensors of the step in %d single-threaded processes, largest "
+                      "first (%.1f s of CPU time in total; the largest tensor alone %.1f s)" %
+                      (len(jobs), procs, sum(cpu), max(cpu))}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -222,6 +266,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="time the oracle on the whole step (a process pool) instead of the bounded sample")
     ap.add_argument("--precision", choices=["mixed", "bf16x3", "bf16x6", "fp32"], default="mixed",
                     help="arithmetic of the polar iteration's matrix products")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -432,7 +478,9 @@ def main():
     if not args.no_cpu_baseline:
         ovar = {"exact": None, "fast": {"orth": "ns5", "scale": "rms"}, "clip_high": {"clip": "high"},
                 "clip_low": {"clip": "low"}}[args.variant]
-        out["cpu_baseline"] = cpu_baseline(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget, ovar)
+        base = cpu_full_step if args.cpu_full else cpu_baseline
+        out["cpu_baseline"] = (base(cfg, theta0, workers, torch.zeros_like(mom), ovar) if args.cpu_full else
+                               base(cfg, theta0, workers, torch.zeros_like(mom), args.cpu_budget, ovar))
     plan.close()
     print(json.dumps(out), flush=True)
 
