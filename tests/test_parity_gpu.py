@@ -392,6 +392,25 @@ def test_config1_full_block(iso):
     _run_and_compare(iso, WORKLOADS[BLOCK], select=None)
 
 
+def test_config1_three_chained_steps(iso):
+    """One d = 768 decoder block over three chained outer steps on one plan:
+    each step starts from the GPU's theta and B of the step before (B != 0
+    from step 2 on) with fresh replicas, the oracle getting the same inputs
+    (shared-input parity, every tensor; a matrix flagged below resolution,
+    which this seed's first step has, is reported and must stay orthonormal
+    and finite)."""
+    from workload import WORKLOADS, BLOCK
+    cfg = WORKLOADS[BLOCK]
+    dev = torch.device("cuda", 0)
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, iso.ISOLOCO_F32, device=dev)
+    theta = mom = None
+    for step in (1, 2, 3):
+        theta, mom, _ = _run_and_compare(iso, cfg, seed=5, step=step, theta=theta, mom=mom, plan=plan,
+                                         check_q=step == 1, max_flagged=1)
+        assert mom.abs().max().item() > 0
+    plan.close()
+
+
 def _one_of_each_shape(lay):
     sample = [i for i, t in enumerate(lay) if t[3] == KIND_AVG]
     seen = set()
@@ -500,12 +519,13 @@ def test_config3_full_size_sampled(iso):
 @pytest.mark.timeout(900)
 def test_config4_full_size_sampled(iso):
     """16 blocks d = 2048 / FFN 5632 + 32000 x 2048 (888M parameters), K = 64
-    bf16 replicas (114 GB in HBM): 1-D tensors, one square and one tall
-    matrix against the oracle, properties for all 113 matrices."""
+    bf16 replicas (114 GB in HBM): 1-D tensors, one matrix of each shape
+    (square, tall, wide-stored and the 32000 x 2048 embedding) against the
+    oracle, properties for all 113 matrices."""
     from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
     cfg = WORKLOADS[LLAMA_888M]
     sample = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_AVG]
-    for shape in ((2048, 2048), (5632, 2048)):
+    for shape in ((2048, 2048), (5632, 2048), (2048, 5632), (32000, 2048)):
         sample.append(next(i for i, t in enumerate(cfg.layout) if (t[1], t[2]) == shape))
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True,
                                                       max_flagged=1)
