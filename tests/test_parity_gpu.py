@@ -303,26 +303,32 @@ def test_uncovered_elements_untouched(iso):
     plan.close()
 
 
-def test_zero_and_nonfinite_tensors(iso):
+@pytest.mark.parametrize("shape,third", [((64, 48), (70, 40)), ((192, 48), (200, 40))], ids=["square", "tall"])
+def test_zero_and_nonfinite_tensors(iso, shape, third):
+    """A zero and a non-finite Delta are flagged (sigma_bar 0: theta unchanged;
+    NaN propagates through that tensor only), the other tensors of the step
+    are unaffected; with tall shapes through the factored steps too."""
     from workload import ReplicaGenerator, custom_layout
-    lay, n = custom_layout([(64, 48, KIND_ISO), (64, 48, KIND_ISO), (70, 40, KIND_ISO), (20, 1, KIND_AVG)], align=4)
+    r, c = shape
+    lay, n = custom_layout([(r, c, KIND_ISO), (r, c, KIND_ISO), third + (KIND_ISO,), (20, 1, KIND_AVG)], align=4)
     cfg = _cfg(lay, n, K=3)
     dev = torch.device("cuda", 0)
     gen = ReplicaGenerator(cfg, seed=2, device=dev)
     theta, mom = gen.init_state()
     workers = gen.workers(theta, 1)
     o0, o1, o2 = lay[0][0], lay[1][0], lay[2][0]
-    workers[:, o0:o0 + 64 * 48] = theta[o0:o0 + 64 * 48]      # Delta = 0
-    workers[1, o1 + 17] = float("nan")                         # non-finite input
+    workers[:, o0:o0 + r * c] = theta[o0:o0 + r * c]      # Delta = 0
+    workers[1, o1 + 17] = float("nan")                     # non-finite input
     th0 = theta.clone()
     plan = iso.IsoLoCoPlan(lay, n, 3, iso.ISOLOCO_F32, device=dev)
+    print("case: zero and non-finite %dx%d, factored steps %s" % (r, c, plan.factored_steps()), flush=True)
     plan.aggregate(theta, workers, mom, 1.0, 0.7, 0.9)
     torch.cuda.synchronize()
     st = plan.stats()
     assert st[0].flags & iso.ISOLOCO_FLAG_ZERO and st[0].sigma_bar == 0.0
-    assert torch.equal(theta[o0:o0 + 64 * 48], th0[o0:o0 + 64 * 48])
+    assert torch.equal(theta[o0:o0 + r * c], th0[o0:o0 + r * c])
     assert st[1].flags & iso.ISOLOCO_FLAG_NONFINITE
-    assert bool(torch.isnan(theta[o1:o1 + 64 * 48]).all())
+    assert bool(torch.isnan(theta[o1:o1 + r * c]).all())
     # the other tensors are unaffected
     assert st[2].flags == 0 and bool(torch.isfinite(theta[o2:]).all())
     plan.close()
