@@ -275,6 +275,43 @@ def test_unaligned_offsets_and_odd_shapes(iso):
     _run_and_compare(iso, _cfg(lay, n, K=4, dtype="bf16", c=1e-2), seed=3)
 
 
+def _random_shapes(rng):
+    """5 to 9 tensors: tall (m >= 2n, stored either way), square-ish (n <= m <
+    2n) and 1-D, with odd sizes from 1 up to several tiles."""
+    shapes = []
+    for _ in range(int(rng.integers(5, 10))):
+        u = rng.random()
+        if u < 0.25:
+            shapes.append((int(rng.integers(1, 700)), 1, KIND_AVG))
+        elif u < 0.6:
+            n = int(rng.integers(1, 200))
+            m = int(rng.integers(2 * n, 2 * n + 600))
+            shapes.append((m, n, KIND_ISO) if rng.random() < 0.5 else (n, m, KIND_ISO))
+        else:
+            n = int(rng.integers(2, 400))
+            m = int(rng.integers(n, 2 * n))
+            shapes.append((m, n, KIND_ISO) if rng.random() < 0.5 else (n, m, KIND_ISO))
+    return shapes
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_layouts(iso, seed):
+    """Seeded random layouts packed without alignment, K from 1 to 6, float32
+    or bfloat16 replicas, the mixed, fp32 or bf16x6 products (bf16x3 is
+    specified for spectra above about 1e-4 only), every tensor against the
+    oracle."""
+    from workload import custom_layout
+    rng = np.random.default_rng(1000 + seed)
+    shapes = _random_shapes(rng)
+    lay, n = custom_layout(shapes, align=1)
+    K = int(rng.integers(1, 7))
+    dtype = "f32" if rng.random() < 0.6 else "bf16"
+    precision = int(rng.choice([0, 1, 3]))
+    print("case: seed %d K %d %s precision %d shapes %s" % (seed, K, dtype, precision, shapes), flush=True)
+    _run_and_compare(iso, _cfg(lay, n, K=K, dtype=dtype), seed=seed, opts=dict(precision=precision),
+                     max_flagged=1)
+
+
 def test_single_worker(iso):
     from workload import custom_layout
     lay, n = custom_layout([(96, 80, KIND_ISO), (80, 1, KIND_AVG)], align=4)
