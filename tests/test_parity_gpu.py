@@ -435,6 +435,18 @@ def test_config1_full_block(iso):
     _run_and_compare(iso, WORKLOADS[BLOCK], select=None)
 
 
+def test_config1_variance_reading(iso):
+    """The generator's noise N(0, 1e-4) read as a variance (standard deviation
+    1e-2) instead of a standard deviation: one d = 768 block whose
+    pseudo-gradients are noise-dominated (condition numbers of about 1e3
+    instead of 1e5 - 1e6), every tensor against the oracle."""
+    import dataclasses
+    from workload import WORKLOADS, BLOCK
+    cfg = dataclasses.replace(WORKLOADS[BLOCK], noise_std=1e-2)
+    _, _, st = _run_and_compare(iso, cfg, seed=7)
+    print("steps per matrix:", [s_.steps for s_, t in zip(st, cfg.layout) if t[3] == KIND_ISO], flush=True)
+
+
 def test_config1_three_chained_steps(iso):
     """One d = 768 decoder block over three chained outer steps on one plan:
     each step starts from the GPU's theta and B of the step before (B != 0
