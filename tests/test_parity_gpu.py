@@ -435,6 +435,43 @@ def test_config1_full_block(iso):
     _run_and_compare(iso, WORKLOADS[BLOCK], select=None)
 
 
+@pytest.mark.timeout(900)
+def test_config1_free_running_trajectory(iso):
+    """Ten outer steps of one d = 768 block (K = 8) as two free-running
+    trajectories: the GPU's from its own theta and B, the float64 oracle's from
+    its own, each step's replicas drawn around each trajectory's own theta
+    with the same pseudo-gradients.  Reported, not gated (the gate is the
+    per-step shared-input parity): the relative difference of the accumulated
+    update theta_t - theta_0 and of B after every step, which grows only by
+    the rounding each step adds."""
+    from workload import WORKLOADS, BLOCK, ReplicaGenerator
+    from _helpers import workers_host, oracle_per_tensor_spawned
+    cfg = WORKLOADS[BLOCK]
+    dev = torch.device("cuda", 0)
+    gen = ReplicaGenerator(cfg, seed=3, device=dev)
+    theta, mom = gen.init_state()
+    th0 = theta.double().cpu().numpy()
+    th_o, b_o = th0.copy(), np.zeros_like(th0)
+    plan = iso.IsoLoCoPlan(cfg.layout, cfg.n_elems, cfg.K, iso.ISOLOCO_F32, device=dev)
+    print("case: free-running trajectories, one d768 block, K = 8, seed 3", flush=True)
+    for step in range(1, 11):
+        plan.aggregate(theta, gen.workers(theta, step), mom, cfg.alpha, cfg.outer_lr, cfg.mu)
+        w_o = workers_host(gen.workers(torch.tensor(th_o, dtype=torch.float32, device=dev), step))
+        inputs = [((off, r, c, k), th_o[off:off + r * c], [w[off:off + r * c] for w in w_o], b_o[off:off + r * c])
+                  for off, r, c, k in cfg.layout]
+        res = oracle_per_tensor_spawned(inputs, cfg.alpha, cfg.outer_lr, cfg.mu)
+        for (off, r, c, k), (t_new, b_new, _) in zip(cfg.layout, res):
+            th_o[off:off + r * c] = t_new
+            b_o[off:off + r * c] = b_new
+        torch.cuda.synchronize()
+        th_g = theta.double().cpu().numpy()
+        b_g = mom.double().cpu().numpy()
+        assert np.isfinite(th_g).all() and np.isfinite(b_g).all()
+        print("step %d: update theta_t - theta_0 %.2e, B %.2e (relative Frobenius, GPU vs oracle)" %
+              (step, relF(th_g - th0, th_o - th0), relF(b_g, b_o)), flush=True)
+    plan.close()
+
+
 def test_config1_variance_reading(iso):
     """The generator's noise N(0, 1e-4) read as a variance (standard deviation
     1e-2) instead of a standard deviation: one d = 768 block whose
