@@ -297,11 +297,15 @@ isoloco_status isoloco_factored_steps(isoloco_plan_t plan, int32_t* first, int32
 typedef struct {
   float total_ms;   /* first launch start to last launch end                       */
   float reduce_ms;  /* K-way reduction (+ Nesterov of the uncorrected tensors)     */
-  float gram_ms;    /* batched Gram products X^T X, all steps (+ the check)        */
+  float gram_ms;    /* batched Gram products X^T X, all steps (+ the check, and the
+                       per-matrix decisions their last tiles take); with factored
+                       steps also their n x n products M B and M P                 */
   float poly_ms;    /* batched polynomial products b A + c A^2, all steps          */
-  float update_ms;  /* batched updates X <- a X + X P, all steps                   */
+  float update_ms;  /* batched updates X <- X P, all steps (with factored steps
+                       also their n x n products A M)                              */
   float finish_ms;  /* fused Nesterov write-back of the corrected tensors          */
-  float other_ms;   /* norms, trace and sigma_bar                                  */
+  float other_ms;   /* ||Delta||_F per matrix, the trace with sigma_bar, a phase end
+                       without a check, the clip variants' composition             */
   int32_t gram_launches, poly_launches, update_launches, launches;
   float products_busy_ms; /* union of the Gram, polynomial and update launches' intervals:
                         the time some product runs (with two streams the launches overlap,
