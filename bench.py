@@ -434,7 +434,8 @@ def main():
                      "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(gemm_tfs / peak, 4),
                      "work": "the method's products as fp32 flops (symmetric Gram n(n+1)m, polynomial "
-                             "n(n+1)n, update 2mn^2 per polar step) over the time some product runs",
+                             "n(n+1)n, update 2mn^2 per polar step; a factored step of a tall matrix: "
+                             "A M 2n^3, M B and M P n(n+1)n each) over the time some product runs",
                      "traffic": mt["gemm_bytes_per_step"] if measured else None,
                      "traffic_unit": "HBM bytes per step over all product launches",
                      "traffic_source": ("stored: rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE on these sources "
