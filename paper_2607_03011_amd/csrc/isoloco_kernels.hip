@@ -1125,15 +1125,30 @@ constexpr int kBK2 = 32;
 constexpr int kLdsK = kBK2 + 8;  // padded row (bf16 elements): 80 bytes
 
 // Element offset within an LDS operand row of its 16-byte k-chunk c (0..3).
-// Rows of LK = 40 bf16 (80 bytes) keep 16-byte accesses to 8 consecutive rows
-// on distinct banks as they are; rows of LK = 32 (64 bytes, no padding:
-// room for two buffers of bf16x5 operands) XOR the chunk position with bits
-// 1-2 of the row to the same effect (a probe of both layouts measured 6%
-// slower reads and 8% slower stores for 64-byte rows).
+// Rows of LK = 40 bf16 (80 bytes) keep 16-byte accesses to 16 consecutive
+// rows on distinct banks as they are (an LDS of 64 banks serves 16 lanes of a
+// 16-byte access per pass).  Rows of LK = 32 (64 bytes, no padding: room for
+// two buffers of bf16x5 operands) XOR the chunk position with bits 1-2 of the
+// row XOR bits 2-3: the four rows that share a set of 16 banks (r, r + 4,
+// r + 8, r + 12) then take four different chunk positions.  (Bits 1-2 alone
+// spread 8 consecutive rows only, which leaves 2-way conflicts on 64 banks.)
 template <int LK>
 __device__ __forceinline__ int lds_chunk(int row, int c) {
   static_assert(LK == kLdsK || LK == kBK2, "80- or 64-byte operand rows");
-  return LK == kBK2 ? ((c ^ ((row >> 1) & 3)) << 3) : (c << 3);
+  return LK == kBK2 ? ((c ^ (((row >> 1) ^ (row >> 2)) & 3)) << 3) : (c << 3);
+}
+
+// Row of the slab covered by thread t's group of eight lanes in the row
+// mapping (each group stores one row's 64 bytes of a plane with 8-byte
+// writes).  With 80-byte LDS rows, rows r and r + 1 share banks, so the
+// groups take t / 8 with bits 0-1 and 2-3 swapped: the groups of one pass
+// (two of 16 lanes, or four of 32) store rows r, r + 4, r + 8, r + 12, which
+// fall on distinct banks.  64-byte rows keep t / 8 (their chunk swizzle
+// spreads consecutive rows already).
+template <int LK>
+__device__ __forceinline__ int rowmap_row(int t) {
+  const int g = t >> 3;
+  return LK == kBK2 ? g : (g & ~15) | ((g & 3) << 2) | ((g >> 2) & 3);
 }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -1153,7 +1168,7 @@ struct Slab32 {
 // columns and K range are all inside the matrix, with m, n multiples of 4).
 // ROWS = 128 (256 threads) or 256 (512 threads): the slab is ROWS x 32 and
 // every thread holds 16 of its values.
-template <bool ICONTIG, int ROWS = kBM>
+template <bool ICONTIG, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int i0, Slab32& r) {
   const int t = threadIdx.x;
   // Buffer loads: a uniform resource for the operand's matrix, one 32-bit lane
@@ -1179,9 +1194,9 @@ __device__ __forceinline__ void slab32_load_fast(const Operand& op, int k0, int 
   } else {
     // element (k, i) at base + i s_i + k: row mapping -- eight lanes cover the
     // slab's 128 contiguous bytes of one row, a wave eight rows per load
-    // (thread t: rows i0 + t / 8 + (ROWS / 4) q, k = k0 + 4 (t % 8) .. +3), so
-    // that a load touches 8 cache lines instead of 64
-    const int vo = 4 * ((i0 + (t >> 3)) * (int)op.s_i + 4 * (t & 7));
+    // (thread t: rows i0 + rowmap_row(t) + (ROWS / 4) q, k = k0 + 4 (t % 8)
+    // .. +3), so that a load touches 8 cache lines instead of 64
+    const int vo = 4 * ((i0 + rowmap_row<LK>(t)) * (int)op.s_i + 4 * (t & 7));
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       r.v[q] = __builtin_bit_cast(
@@ -1231,11 +1246,11 @@ struct OperandLayout {
   static constexpr bool rowmap = LAYOUT != kGeneric && !icontig;
 };
 
-template <int MODE, int LAYOUT, bool IS_A, int ROWS = kBM>
+template <int MODE, int LAYOUT, bool IS_A, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, Slab32& r) {
   static_assert(LAYOUT != kGeneric || ROWS == kBM, "ragged tiles use the 128-row kernel");
   if (LAYOUT == kGeneric) slab32_load(op, k0, i0, r);
-  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig, ROWS>(op, k0, i0, r);
+  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig, ROWS, LK>(op, k0, i0, r);
 }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -1271,12 +1286,12 @@ __device__ __forceinline__ void slab32_store(const Slab32& r, __bf16 (*planes)[R
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
-// The same for registers in the row mapping (thread t: rows t / 8 + (ROWS / 4) q,
-// k = 4 (t % 8) .. +3): 8-byte LDS writes.
+// The same for registers in the row mapping (thread t: rows rowmap_row(t) +
+// (ROWS / 4) q, k = 4 (t % 8) .. +3): 8-byte LDS writes.
 template <int NS, bool SCALED = false, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*planes)[ROWS][LK], float scale = 1.f) {
   const int t = threadIdx.x;
-  const int i = t >> 3, kb = 4 * (t & 7);
+  const int i = rowmap_row<LK>(t), kb = 4 * (t & 7);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     bf16x4 part[NS];
@@ -1583,13 +1598,13 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
     const int klast = s.k_begin + (nslab - 1) * kBK2;
     auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
     Slab32 ra, rb;
-    load_operand<MODE, LAYOUT, true, kBig>(s.A, s.k_begin, s.i0, ra);
-    load_operand<MODE, LAYOUT, false, kBig>(s.B, s.k_begin, s.j0, rb);
+    load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, s.k_begin, s.i0, ra);
+    load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, s.k_begin, s.j0, rb);
     if constexpr (NB == 2) {
       store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
       store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
-      load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(1), s.i0, ra);
-      load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(1), s.j0, rb);
+      load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(1), s.i0, ra);
+      load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(1), s.j0, rb);
       __syncthreads();
       for (int sl = 0; sl + 1 < nslab; ++sl) {
         const int cur = sl & 1;
@@ -1597,8 +1612,8 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
         store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[cur ^ 1], s.A.scale);
         store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[cur ^ 1], s.B.scale);
         mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[cur], Bp[cur], 16, acc);
-        load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 2), s.i0, ra);
-        load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 2), s.j0, rb);
+        load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(sl + 2), s.i0, ra);
+        load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(sl + 2), s.j0, rb);
         __syncthreads();
       }
       const int last = (nslab - 1) & 1;
@@ -1610,8 +1625,8 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
         store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
         store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
         __syncthreads();
-        load_operand<MODE, LAYOUT, true, kBig>(s.A, kat(sl + 1), s.i0, ra);
-        load_operand<MODE, LAYOUT, false, kBig>(s.B, kat(sl + 1), s.j0, rb);
+        load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(sl + 1), s.i0, ra);
+        load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(sl + 1), s.j0, rb);
         mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 0, acc);
         mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 16, acc);
       }
