@@ -98,9 +98,9 @@ def gemm_bytes_per_step(layout, stats, factored=(0, 0)):
 # device copy; summaries in profiles/) for the default workload and precision.  It is
 # reported only while the kernel and planner sources are the ones it was measured on.
 MEASURED_TRAFFIC = {
-    "sources_sha256": "3ca8733d67249518fce6c70bca91f9e67607cfc6b9c4978287d4257c08f10256",
+    "sources_sha256": "eefd9c8201a195f90b21da8323abf88e1a74efb563ab9da4e34f5c4d829e8b13",
     "workload": "llama-12L-d768-V32000-K16", "precision": "mixed",
-    "gemm_bytes_per_step": 24.10e9, "reduce_bytes_per_launch": 7.890e9, "finish_bytes_per_step": 2.197e9,
+    "gemm_bytes_per_step": 24.06e9, "reduce_bytes_per_launch": 7.890e9, "finish_bytes_per_step": 2.197e9,
 }
 
 
