@@ -281,15 +281,15 @@ std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<
     groups.push_back({i, j});
     i = j;
   }
-  // shape class of a group: the matrix shape and layout, the group's size and,
-  // for a K slice, its length
+  // shape class of a group: the matrix shape, the group's size and, for a K
+  // slice, its length
   auto key = [&](const Group& g) {
     const MatInfo& M = mats[in[g.begin].mat];
     const int64_t kb = (int64_t)in[g.begin].ks * M.kchunk;
     const int64_t klen = by_slice ? std::min<int64_t>(M.m, kb + M.kchunk) - kb : 0;
-    return std::array<int64_t, 5>{M.m, M.n, M.trans, (int64_t)(g.end - g.begin), klen};
+    return std::array<int64_t, 4>{M.m, M.n, (int64_t)(g.end - g.begin), klen};
   };
-  std::vector<std::array<int64_t, 5>> keys;
+  std::vector<std::array<int64_t, 4>> keys;
   std::vector<std::vector<size_t>> classes;
   for (size_t gi = 0; gi < groups.size(); ++gi) {
     const auto k = key(groups[gi]);
@@ -328,12 +328,12 @@ std::vector<Task> xcd_order(const std::vector<MatInfo>& mats, const std::vector<
 
 struct TaskListHost {
   std::vector<Task> tasks;
-  int seg_off[3] = {0, 0, 0};
-  int seg_cnt[3] = {0, 0, 0};
-  int big_off[2] = {0, 0};
-  int big_cnt[2] = {0, 0};
-  int rem_off[3] = {0, 0, 0};
-  int rem_cnt[3] = {0, 0, 0};
+  int seg_off[2] = {0, 0};
+  int seg_cnt[2] = {0, 0};
+  int big_off = 0;
+  int big_cnt = 0;
+  int rem_off[2] = {0, 0};
+  int rem_cnt[2] = {0, 0};
 };
 
 struct isoloco_plan_s {
@@ -464,7 +464,6 @@ void plan_matrices(isoloco_plan_s* p) {
     // transposed one -- the same bytes again; a tall tensor (rows > cols) is
     // cut into tiles that the reduction writes, and the write-back reads,
     // transposed through LDS.
-    mi.trans = 1;
     mi.wide = T.rows < T.cols ? 1 : 0;
     const bool tiled = T.rows > T.cols;
     mi.m = (int32_t)std::max(T.rows, T.cols);
@@ -582,14 +581,12 @@ void plan_matrices(isoloco_plan_s* p) {
   p->nsq = sq;
   p->npart = part;
 
-  // Work lists, longest tasks first, each in three segments (interior tiles of
-  // row-major iterates, interior tiles of column-major iterates, ragged
-  // tiles), each segment reordered for the XCD round robin of the dispatcher.
-  // Next to this cover by 128 x 128 tiles, the split-bf16 kernels use
-  // interior 256 x 256 tiles where a matrix has them and 128 x 128 tiles for
-  // the rest.  (The planner makes every iterate column-major; the kernels
-  // take either layout, per task in the shared segment 0.)
-  std::vector<Task> seg[3], big[2], rem[3];
+  // Work lists, longest tasks first, each in two segments (interior tiles,
+  // ragged tiles), each segment reordered for the XCD round robin of the
+  // dispatcher.  Next to this cover by 128 x 128 tiles, the split-bf16
+  // kernels use interior 256 x 256 tiles where a matrix has them and
+  // 128 x 128 tiles for the rest.
+  std::vector<Task> seg[2], big, rem[2];
   const std::vector<MatInfo>* table = &p->mats;  // the matrices the tasks index
   auto flush = [&](TaskListHost& L, bool by_slice) {
     L.tasks.clear();
@@ -600,23 +597,14 @@ void plan_matrices(isoloco_plan_s* p) {
       L.tasks.insert(L.tasks.end(), o.begin(), o.end());
       v.clear();
     };
-    for (int q = 0; q < 3; ++q) append(seg[q], L.seg_off[q], L.seg_cnt[q]);
-    for (int q = 0; q < 2; ++q) append(big[q], L.big_off[q], L.big_cnt[q]);
-    for (int q = 0; q < 3; ++q) append(rem[q], L.rem_off[q], L.rem_cnt[q]);
+    for (int q = 0; q < 2; ++q) append(seg[q], L.seg_off[q], L.seg_cnt[q]);
+    append(big, L.big_off, L.big_cnt);
+    for (int q = 0; q < 2; ++q) append(rem[q], L.rem_off[q], L.rem_cnt[q]);
   };
   // The interior kernels address a matrix with 32-bit byte offsets: matrices
   // of 2^29 elements or more take the generic kernel.
   auto fast_ok = [](const MatInfo& M) { return M.vec && (int64_t)M.m * M.n < ((int64_t)1 << 29); };
-  // Interior tiles of column-major iterates go to segment 1 of the update
-  // list (a launch of their own) and share segment 0 with row-major ones in
-  // the Gram and polynomial lists (one launch; the kernel picks the loaders
-  // per task).  With row-major and column-major iterates mixed, these were
-  // the choices measured fastest (one Gram launch: 0.1 ms per outer step
-  // faster on the 109.5M workload; one update launch: 0.5 ms slower).
-  bool split_layouts = false;
-  auto segment = [&](const MatInfo& M, bool interior) {
-    return !(interior && fast_ok(M)) ? 2 : (split_layouts && M.trans ? 1 : 0);
-  };
+  auto segment = [&](const MatInfo& M, bool interior) { return interior && fast_ok(M) ? 0 : 1; };
   // a 128 x 128 tile goes to the full cover and, unless the 256 x 256 tile
   // (a / 2, b / 2) covers it (that tile is listed once, with its first
   // 128 x 128 tile), to the remainder
@@ -624,14 +612,13 @@ void plan_matrices(isoloco_plan_s* p) {
     seg[segment(M, interior)].push_back(tk);
     if (!covered) rem[segment(M, interior)].push_back(tk);
     else if (tk.tm % 2 == 0 && tk.tn % 2 == 0)
-      big[split_layouts && M.trans ? 1 : 0].push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
+      big.push_back(Task{tk.mat, tk.tm / 2, tk.tn / 2, tk.ks});
   };
   // The lists of every matrix (one stream), and of each schedule class alone
   // (a stream per class).
   auto build_lists = [&](const std::vector<MatInfo>& mats, int cls, TaskListHost& G, TaskListHost& P,
                          TaskListHost& U) {
     table = &mats;
-    split_layouts = false;
     std::vector<int> order;
     for (size_t i = 0; i < mats.size(); ++i)
       if (cls < 0 || mats[i].sched == cls) order.push_back((int)i);
@@ -661,7 +648,6 @@ void plan_matrices(isoloco_plan_s* p) {
           put(M, (b + 1) * kBM <= M.n && kin, false, Task{mi, a, b, 0});
     }
     flush(P, false);
-    split_layouts = true;
     for (int mi : order) {
       const MatInfo& M = mats[mi];
       const int TM = (M.m + kBM - 1) / kBM, TN = (M.n + kBN - 1) / kBN;
@@ -727,16 +713,14 @@ void plan_workspace(isoloco_plan_s* p) {
 TaskList dev_list(const char* w, const TaskListHost& L, size_t off) {
   TaskList d{};
   d.tasks = reinterpret_cast<const Task*>(w + off);
-  for (int q = 0; q < 3; ++q) {
+  for (int q = 0; q < 2; ++q) {
     d.seg_off[q] = L.seg_off[q];
     d.seg_cnt[q] = L.seg_cnt[q];
     d.rem_off[q] = L.rem_off[q];
     d.rem_cnt[q] = L.rem_cnt[q];
   }
-  for (int q = 0; q < 2; ++q) {
-    d.big_off[q] = L.big_off[q];
-    d.big_cnt[q] = L.big_cnt[q];
-  }
+  d.big_off = L.big_off;
+  d.big_cnt = L.big_cnt;
   return d;
 }
 

@@ -15,14 +15,18 @@ namespace isoloco {
 // storage order like the 128 x 128 ones) plus, in segments as above, the
 // 128 x 128 tiles they leave uncovered; the Gram and polynomial lists have no
 // 256 x 256 tiles (rem = seg).
+// A product's work list: the 128 x 128 cover (segment 0 interior tiles,
+// segment 1 ragged tiles and matrices too large for 32-bit offsets), and for
+// the split-bf16 kernels the interior 256 x 256 tiles plus the 128 x 128 tiles
+// they leave over (same segments).
 struct TaskList {
   const Task* tasks;
-  int seg_off[3];
-  int seg_cnt[3];
-  int big_off[2];
-  int big_cnt[2];
-  int rem_off[3];
-  int rem_cnt[3];
+  int seg_off[2];
+  int seg_cnt[2];
+  int big_off;
+  int big_cnt;
+  int rem_off[2];
+  int rem_cnt[2];
 };
 
 // Device tables and buffers inside the caller's workspace, plus the host copies

@@ -680,8 +680,9 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
   s.mi = g.mats[task.mat];
   const MatInfo& mi = s.mi;
   const int m = mi.m, n = mi.n;
-  s.sr = mi.trans ? 1 : n;
-  s.sc = mi.trans ? m : 1;
+  // every iterate is column-major in tall coordinates: X[r][c] at r + c m
+  s.sr = 1;
+  s.sc = m;
   const bool vec = mi.vec != 0;
   s.xscale = 1.f;
   s.gs = 1.f;
@@ -694,7 +695,7 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     const float* x = ((g.xin_alt && g.sc[task.mat].qbuf) ? g.xin_alt : g.xin) + mi.ws_off;
     s.k_begin = task.ks * mi.kchunk;
     s.k_end = min(m, s.k_begin + mi.kchunk);
-    s.A = {x, s.sr, s.sc, s.k_end, n, !mi.trans, vec, s.xscale};
+    s.A = {x, s.sr, s.sc, s.k_end, n, false, vec, s.xscale};
     s.B = s.A;
     if (g.bin) s.B.base = g.bin + mi.ws_off;
     s.M = n;
@@ -715,7 +716,7 @@ __device__ __forceinline__ GemmSetup gemm_setup(const GemmArgs& g, const Task& t
     s.k_end = n;
   } else {
     const float* x = g.xin + mi.ws_off;
-    s.A = {x, s.sc, s.sr, n, m, mi.trans != 0, vec, s.xscale};
+    s.A = {x, s.sc, s.sr, n, m, true, vec, s.xscale};
     const float* p = g.poly + mi.sq_off;
     s.B = {p, (int64_t)n, 1, n, n, true, (n & 3) == 0, 1.f};
     s.M = m;
@@ -968,39 +969,13 @@ __device__ __forceinline__ void gram_epilogue(const GemmArgs& g, const GemmSetup
 // acc[a][b][r] holds C(i, j) with
 //   i = i0 + wm*32*NA + a*32 + 8*(r/4) + 4*(lane/32) + r%4,  j = j0 + wn*64 + b*32 + lane%32
 // (the 32 x 32 accumulator layout of the fp32 and bf16 MFMA instructions).
-template <int MODE, int NA = 2, int WNC = 2, bool SWAP = false, bool VEC = false>
+// Interior update tiles of the split-bf16 kernels store through
+// store_update_colmajor instead.
+template <int MODE, int NA = 2, int WNC = 2>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const GemmSetup& s, const Task& task,
                                               const floatx16 (&acc)[NA][2], void* scratch = nullptr) {
   if constexpr (MODE == kGram) {
     gram_epilogue<NA, WNC>(g, s, task, acc, scratch);
-    return;
-  }
-  if (MODE == kUpdate && VEC) {
-    // Interior update tile: 16-byte stores.  Row-major X' (SWAP, transposed
-    // accumulators): lane holds X'(i, j .. j+3); column-major X' (i contiguous):
-    // lane holds X'(i .. i+3, j).
-    float* xo = g.xout + s.mi.ws_off;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave / WNC, wn = wave % WNC;
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-          const floatx4 v = {acc[a][b][4 * grp], acc[a][b][4 * grp + 1], acc[a][b][4 * grp + 2],
-                             acc[a][b][4 * grp + 3]};
-          const int off4 = 8 * grp + 4 * (lane >> 5);
-          if (SWAP) {
-            const int i = s.i0 + wm * 32 * NA + a * 32 + (lane & 31);
-            const int j = s.j0 + wn * 64 + b * 32 + off4;
-            *reinterpret_cast<floatx4*>(xo + (int64_t)i * s.sr + j) = v;
-          } else {
-            const int i = s.i0 + wm * 32 * NA + a * 32 + off4;
-            const int j = s.j0 + wn * 64 + b * 32 + (lane & 31);
-            *reinterpret_cast<floatx4*>(xo + i + (int64_t)j * s.sc) = v;
-          }
-        }
     return;
   }
   const MatInfo& mi = s.mi;
@@ -1232,25 +1207,26 @@ __device__ __forceinline__ void slab32_load(const Operand& op, int k0, int i0, S
 
 // Loader selected at compile time: LAYOUT kGeneric uses runtime layout and
 // bounds; the fast layouts fix the contiguity of the A and B operands.
-enum TileLayout { kGeneric = 0, kFastT0 = 1, kFastT1 = 2, kFastAny = 3 };
+// kFast: interior tiles, unchecked buffer loads of the operands' fixed
+// layout; kGeneric: ragged tiles and matrices too large for 32-bit offsets,
+// bounds-checked loads of either layout.
+enum TileLayout { kGeneric = 0, kFast = 1 };
 
-// Gram: both operands X[k][i]: i-contiguous for row-major storage (T0),
-// k-contiguous for column-major storage (T1).  Poly: A[k][i] read as A[i][k]
-// (symmetric), k-contiguous.  Update: A = X[i][k] (k-contiguous for T0,
-// i-contiguous for T1), B = P[k][j], i-contiguous.  k-contiguous interior
+// Operands of the interior tiles (the iterates column-major): Gram, both X[k][i]
+// with k contiguous; Poly, A[k][i] read as A[i][k] (symmetric), k-contiguous;
+// Update, A = X[i][k] and B = P[k][j], both i-contiguous.  k-contiguous
 // operands use the row mapping of the registers.
-template <int MODE, int LAYOUT, bool IS_A>
+template <int MODE, int LAYOUT>
 struct OperandLayout {
-  static constexpr bool icontig =
-      MODE == kGram ? (LAYOUT == kFastT0) : MODE == kPoly ? false : (IS_A ? (LAYOUT == kFastT1) : true);
+  static constexpr bool icontig = MODE == kUpdate;
   static constexpr bool rowmap = LAYOUT != kGeneric && !icontig;
 };
 
-template <int MODE, int LAYOUT, bool IS_A, int ROWS = kBM, int LK = kLdsK>
+template <int MODE, int LAYOUT, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void load_operand(const Operand& op, int k0, int i0, Slab32& r) {
   static_assert(LAYOUT != kGeneric || ROWS == kBM, "ragged tiles use the 128-row kernel");
   if (LAYOUT == kGeneric) slab32_load(op, k0, i0, r);
-  else slab32_load_fast<OperandLayout<MODE, LAYOUT, IS_A>::icontig, ROWS, LK>(op, k0, i0, r);
+  else slab32_load_fast<OperandLayout<MODE, LAYOUT>::icontig, ROWS, LK>(op, k0, i0, r);
 }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -1314,9 +1290,9 @@ __device__ __forceinline__ void slab32_store_rows(const Slab32& r, __bf16 (*plan
   }
 }
 
-template <int MODE, int LAYOUT, bool IS_A, int NS, bool SCALED, int ROWS = kBM, int LK = kLdsK>
+template <int MODE, int LAYOUT, int NS, bool SCALED, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void store_operand(const Slab32& r, __bf16 (*planes)[ROWS][LK], float scale) {
-  if (OperandLayout<MODE, LAYOUT, IS_A>::rowmap) slab32_store_rows<NS, SCALED, ROWS, LK>(r, planes, scale);
+  if (OperandLayout<MODE, LAYOUT>::rowmap) slab32_store_rows<NS, SCALED, ROWS, LK>(r, planes, scale);
   else slab32_store<NS, SCALED, ROWS, LK>(r, planes, scale);
 }
 
@@ -1340,10 +1316,8 @@ struct SplitParts {
 // One k16 substep of a wave's (32 NA) x 64 tile: read the operand fragments
 // of the NSA / NSB planes from LDS and issue the part products (smallest
 // order first).  WNC waves span the block's columns (wm = wave / WNC,
-// wn = wave % WNC).  SWAP: issue each product as B A instead of A B, so that
-// the accumulators hold the transposed 32 x 32 blocks (4 consecutive output
-// columns per lane).
-template <int NSA, int NSB, int NA = 2, int WNC = 2, int ROWS = kBM, bool SWAP = false, int LK = kLdsK>
+// wn = wave % WNC).
+template <int NSA, int NSB, int NA = 2, int WNC = 2, int ROWS = kBM, int LK = kLdsK>
 __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][LK], const __bf16 (*Bp)[ROWS][LK],
                                              int kk, floatx16 (&acc)[NA][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1373,8 +1347,7 @@ __device__ __forceinline__ void mfma_substep(const __bf16 (*Ap)[ROWS][LK], const
         for (int pa = ord; pa >= 0; --pa) {
           const int pb = ord - pa;
           if (pa >= NSA || pb >= NSB) continue;
-          acc[a][b] = SWAP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bv[b][pb], av[a][pa], acc[a][b], 0, 0, 0)
-                           : __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][pb], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a][pa], bv[b][pb], acc[a][b], 0, 0, 0);
         }
 }
 
@@ -1436,8 +1409,6 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
   // only X operands carry a scale (Gram: both, Update: A)
   constexpr bool SA = SCALED && MODE != kPoly;
   constexpr bool SB = SCALED && MODE == kGram;
-  // interior update tiles of row-major X' accumulate transposed blocks (16-byte stores)
-  constexpr bool kSwap = MODE == kUpdate && LAYOUT == kFastT0;
   const GemmSetup s = gemm_setup<MODE>(g, task);
   // SAME: a diagonal tile of a symmetric product, whose two operand panels
   // coincide -- loaded, split and stored once, read as both operands
@@ -1452,8 +1423,8 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
   const int klast = s.k_begin + (nslab - 1) * kBK2;
   Slab32 ra, rb;
   if (nslab > 0) {
-  load_operand<MODE, LAYOUT, true>(s.A, s.k_begin, s.i0, ra);
-  if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, s.k_begin, s.j0, rb);
+  load_operand<MODE, LAYOUT>(s.A, s.k_begin, s.i0, ra);
+  if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, s.k_begin, s.j0, rb);
   if (NB == 2) {
     // Registers hold two slabs in flight: at the top of the products of slab
     // sl, slab sl + 1 is in (ra1, rb1) and slab sl + 2 in (ra, rb).  Each
@@ -1463,65 +1434,65 @@ __device__ __forceinline__ void bf16_tile(const GemmArgs& g, const Task& task,
     // roles are static.
     auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
     Slab32 ra1, rb1;
-    load_operand<MODE, LAYOUT, true>(s.A, kat(1), s.i0, ra1);
-    if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(1), s.j0, rb1);
-    store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-    if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
-    load_operand<MODE, LAYOUT, true>(s.A, kat(2), s.i0, ra);
-    if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(2), s.j0, rb);
+    load_operand<MODE, LAYOUT>(s.A, kat(1), s.i0, ra1);
+    if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, kat(1), s.j0, rb1);
+    store_operand<MODE, LAYOUT, kNa, SA>(ra, Ap[0], s.A.scale);
+    if constexpr (!SAME) store_operand<MODE, LAYOUT, kNb, SB>(rb, Bp[0], s.B.scale);
+    load_operand<MODE, LAYOUT>(s.A, kat(2), s.i0, ra);
+    if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, kat(2), s.j0, rb);
     __syncthreads();
     int sl = 0;
     for (; sl + 2 < nslab; sl += 2) {
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
-      store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
-      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
-      load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 3), s.i0, ra1);
-      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 3), s.j0, rb1);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 0, acc);
+      store_operand<MODE, LAYOUT, kNa, SA>(ra1, Ap[1], s.A.scale);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 16, acc);
+      load_operand<MODE, LAYOUT>(s.A, kat(sl + 3), s.i0, ra1);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, kat(sl + 3), s.j0, rb1);
       __syncthreads();
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], bpl(1), 0, acc);
-      store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[1], bpl(1), 16, acc);
-      load_operand<MODE, LAYOUT, true>(s.A, kat(sl + 4), s.i0, ra);
-      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, kat(sl + 4), s.j0, rb);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[1], bpl(1), 0, acc);
+      store_operand<MODE, LAYOUT, kNa, SA>(ra, Ap[0], s.A.scale);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, kNb, SB>(rb, Bp[0], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[1], bpl(1), 16, acc);
+      load_operand<MODE, LAYOUT>(s.A, kat(sl + 4), s.i0, ra);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, kat(sl + 4), s.j0, rb);
       __syncthreads();
     }
     // one or two slabs remain: slab sl in buffer 0, slab sl + 1 in (ra1, rb1)
     int last = 0;
     if (sl + 1 < nslab) {
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
-      store_operand<MODE, LAYOUT, true, kNa, SA>(ra1, Ap[1], s.A.scale);
-      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb1, Bp[1], s.B.scale);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 0, acc);
+      store_operand<MODE, LAYOUT, kNa, SA>(ra1, Ap[1], s.A.scale);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, kNb, SB>(rb1, Bp[1], s.B.scale);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 16, acc);
       __syncthreads();
       last = 1;
     }
-    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], bpl(last), 0, acc);
-    mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[last], bpl(last), 16, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[last], bpl(last), 0, acc);
+    mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[last], bpl(last), 16, acc);
   } else {
     for (int sl = 0; sl < nslab; ++sl) {
       __syncthreads();
-      store_operand<MODE, LAYOUT, true, kNa, SA>(ra, Ap[0], s.A.scale);
-      if constexpr (!SAME) store_operand<MODE, LAYOUT, false, kNb, SB>(rb, Bp[0], s.B.scale);
+      store_operand<MODE, LAYOUT, kNa, SA>(ra, Ap[0], s.A.scale);
+      if constexpr (!SAME) store_operand<MODE, LAYOUT, kNb, SB>(rb, Bp[0], s.B.scale);
       __syncthreads();
       const int k1 = min(s.k_begin + (sl + 1) * kBK2, klast);
-      load_operand<MODE, LAYOUT, true>(s.A, k1, s.i0, ra);
-      if constexpr (!SAME) load_operand<MODE, LAYOUT, false>(s.B, k1, s.j0, rb);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 0, acc);
-      mfma_substep<kNa, kNb, 2, 2, kBM, kSwap>(Ap[0], bpl(0), 16, acc);
+      load_operand<MODE, LAYOUT>(s.A, k1, s.i0, ra);
+      if constexpr (!SAME) load_operand<MODE, LAYOUT>(s.B, k1, s.j0, rb);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 0, acc);
+      mfma_substep<kNa, kNb, 2, 2, kBM>(Ap[0], bpl(0), 16, acc);
     }
   }
   }
-  if constexpr (MODE == kUpdate && LAYOUT == kFastT1)
+  if constexpr (MODE == kUpdate && LAYOUT == kFast)
     store_update_colmajor<2, 2>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
   else
-    gemm_epilogue<MODE, 2, 2, kSwap, LAYOUT != kGeneric>(g, s, task, acc, &Ap[0][0][0][0]);
+    gemm_epilogue<MODE, 2, 2>(g, s, task, acc, &Ap[0][0][0][0]);
 }
 
-// The interior tiles of row-major (T0) and column-major (T1) iterates share one
-// launch (kFastAny picks the loaders per task), so that neither layout class
-// forms a launch of its own with a ragged tail.
+// 128 x 128 tiles: the interior tiles (kFast; the diagonal tiles of the
+// symmetric products stage their one operand panel once) or the ragged ones
+// (kGeneric).
 template <int MODE, int NP, int LAYOUT, bool SCALED>
 __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) {
   constexpr int NB = SplitParts<NP>::nb;
@@ -1530,15 +1501,10 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
   auto run = [&](APlanes* Ap, BPlanes* Bp) {
-    if constexpr (LAYOUT == kFastAny) {
-      const bool same = MODE != kUpdate && task.tm == task.tn && (MODE == kPoly || !g.bin);
-      if (g.mats[task.mat].trans) {
-        if (same) bf16_tile<MODE, NP, kFastT1, SCALED, MODE != kUpdate>(g, task, Ap, Bp);
-        else bf16_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
-      } else {
-        if (same) bf16_tile<MODE, NP, kFastT0, SCALED, MODE != kUpdate>(g, task, Ap, Bp);
-        else bf16_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
-      }
+    if constexpr (LAYOUT == kFast && MODE != kUpdate) {
+      const bool same = task.tm == task.tn && (MODE == kPoly || !g.bin);
+      if (same) bf16_tile<MODE, NP, kFast, SCALED, true>(g, task, Ap, Bp);
+      else bf16_tile<MODE, NP, kFast, SCALED>(g, task, Ap, Bp);
     } else {
       bf16_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
     }
@@ -1562,10 +1528,12 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_bf16_kernel(GemmArgs g) 
 // feeds twice as many products as on 128 x 128 tiles -- half the global
 // loads, splits, LDS writes and barriers per product.  bf16x3 double-buffers
 // LDS (2 buffers x 2 planes x 512 rows x 80 bytes: the whole 160 KB of the
-// CU) with one slab in flight in registers (issued after the split of the
-// previous one, landing during the second half of the current slab's
-// products); bf16x5 and bf16x6 keep one buffer of 3 + 2 or 3 + 3 planes
-// (100 or 120 KB) and two barriers per slab.
+// CU) with one slab in flight in registers, issued where the compiler frees
+// its registers during the current slab's products; bf16x5 double-buffers
+// 64-byte rows (BigLds); bf16x6 keeps one buffer of 3 + 3 planes (120 KB)
+// and two barriers per slab.  Update products only (the planner lists
+// 256 x 256 tiles for them alone), interior tiles of the column-major
+// iterates.
 constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 
@@ -1580,15 +1548,15 @@ struct BigLds {
   static constexpr int lk = NP == 5 ? kBK2 : kLdsK;     // row pitch (bf16 elements)
 };
 
-template <int MODE, int NP, int LAYOUT, bool SCALED>
+template <int MODE, int NP, bool SCALED>
 __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& task,
                                               __bf16 (*Ap)[SplitParts<NP>::a][kBig][BigLds<NP>::lk],
                                               __bf16 (*Bp)[SplitParts<NP>::b][kBig][BigLds<NP>::lk]) {
+  static_assert(MODE == kUpdate, "256 x 256 tiles serve the update products");
+  constexpr int LAYOUT = kFast;
   constexpr int kNa = SplitParts<NP>::a, kNb = SplitParts<NP>::b, NB = BigLds<NP>::nb, LK = BigLds<NP>::lk;
-  constexpr bool SA = SCALED && MODE != kPoly;
-  constexpr bool SB = SCALED && MODE == kGram;
-  // update tiles of row-major X' accumulate transposed blocks (16-byte stores)
-  constexpr bool kSwap = MODE == kUpdate && LAYOUT == kFastT0;
+  constexpr bool SA = SCALED;  // the X operand carries the first step's scale
+  constexpr bool SB = false;
   const GemmSetup s = gemm_setup<MODE, kBig>(g, task);
   floatx16 acc[4][2];
   gemm_acc_init<MODE, 4, 4>(g, s, acc);
@@ -1598,73 +1566,57 @@ __device__ __forceinline__ void bf16_big_tile(const GemmArgs& g, const Task& tas
     const int klast = s.k_begin + (nslab - 1) * kBK2;
     auto kat = [&](int sl) { return min(s.k_begin + sl * kBK2, klast); };
     Slab32 ra, rb;
-    load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, s.k_begin, s.i0, ra);
-    load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, s.k_begin, s.j0, rb);
+    load_operand<MODE, LAYOUT, kBig, LK>(s.A, s.k_begin, s.i0, ra);
+    load_operand<MODE, LAYOUT, kBig, LK>(s.B, s.k_begin, s.j0, rb);
     if constexpr (NB == 2) {
-      store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
-      store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
-      load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(1), s.i0, ra);
-      load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(1), s.j0, rb);
+      store_operand<MODE, LAYOUT, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
+      store_operand<MODE, LAYOUT, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
+      load_operand<MODE, LAYOUT, kBig, LK>(s.A, kat(1), s.i0, ra);
+      load_operand<MODE, LAYOUT, kBig, LK>(s.B, kat(1), s.j0, rb);
       __syncthreads();
       for (int sl = 0; sl + 1 < nslab; ++sl) {
         const int cur = sl & 1;
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[cur], Bp[cur], 0, acc);
-        store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[cur ^ 1], s.A.scale);
-        store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[cur ^ 1], s.B.scale);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[cur], Bp[cur], 16, acc);
-        load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(sl + 2), s.i0, ra);
-        load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(sl + 2), s.j0, rb);
+        mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[cur], Bp[cur], 0, acc);
+        store_operand<MODE, LAYOUT, kNa, SA, kBig, LK>(ra, Ap[cur ^ 1], s.A.scale);
+        store_operand<MODE, LAYOUT, kNb, SB, kBig, LK>(rb, Bp[cur ^ 1], s.B.scale);
+        mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[cur], Bp[cur], 16, acc);
+        load_operand<MODE, LAYOUT, kBig, LK>(s.A, kat(sl + 2), s.i0, ra);
+        load_operand<MODE, LAYOUT, kBig, LK>(s.B, kat(sl + 2), s.j0, rb);
         __syncthreads();
       }
       const int last = (nslab - 1) & 1;
-      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[last], Bp[last], 0, acc);
-      mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[last], Bp[last], 16, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[last], Bp[last], 0, acc);
+      mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[last], Bp[last], 16, acc);
     } else {
       for (int sl = 0; sl < nslab; ++sl) {
         __syncthreads();
-        store_operand<MODE, LAYOUT, true, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
-        store_operand<MODE, LAYOUT, false, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
+        store_operand<MODE, LAYOUT, kNa, SA, kBig, LK>(ra, Ap[0], s.A.scale);
+        store_operand<MODE, LAYOUT, kNb, SB, kBig, LK>(rb, Bp[0], s.B.scale);
         __syncthreads();
-        load_operand<MODE, LAYOUT, true, kBig, LK>(s.A, kat(sl + 1), s.i0, ra);
-        load_operand<MODE, LAYOUT, false, kBig, LK>(s.B, kat(sl + 1), s.j0, rb);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 0, acc);
-        mfma_substep<kNa, kNb, 4, 4, kBig, kSwap, LK>(Ap[0], Bp[0], 16, acc);
+        load_operand<MODE, LAYOUT, kBig, LK>(s.A, kat(sl + 1), s.i0, ra);
+        load_operand<MODE, LAYOUT, kBig, LK>(s.B, kat(sl + 1), s.j0, rb);
+        mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[0], Bp[0], 0, acc);
+        mfma_substep<kNa, kNb, 4, 4, kBig, LK>(Ap[0], Bp[0], 16, acc);
       }
     }
   }
-  if constexpr (MODE == kUpdate && LAYOUT == kFastT1)
-    store_update_colmajor<4, 4>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
-  else
-    gemm_epilogue<MODE, 4, 4, kSwap, true>(g, s, task, acc);
+  store_update_colmajor<4, 4>(g, s, acc, reinterpret_cast<float*>(&Ap[0][0][0][0]));
 }
 
-template <int MODE, int NP, int LAYOUT, bool SCALED>
+template <int MODE, int NP, bool SCALED>
 __global__ void __launch_bounds__(kBigThreads, 1) gemm_bf16_big_kernel(GemmArgs g) {
   constexpr int NB = BigLds<NP>::nb;
   typedef __bf16 APlanes[SplitParts<NP>::a][kBig][BigLds<NP>::lk];
   typedef __bf16 BPlanes[SplitParts<NP>::b][kBig][BigLds<NP>::lk];
   const Task task = g.tasks[blockIdx.x];
   if (task.mat < 0 || (g.only_active && !g.sc[task.mat].active)) return;
-  auto run = [&](APlanes* Ap, BPlanes* Bp) {
-    if constexpr (LAYOUT == kFastAny) {
-      if (g.mats[task.mat].trans) bf16_big_tile<MODE, NP, kFastT1, SCALED>(g, task, Ap, Bp);
-      else bf16_big_tile<MODE, NP, kFastT0, SCALED>(g, task, Ap, Bp);
-    } else {
-      bf16_big_tile<MODE, NP, LAYOUT, SCALED>(g, task, Ap, Bp);
-    }
-  };
-  if constexpr (MODE == kUpdate) {
-    // one block for the operand planes and, after the products, the staging
-    // of the output tile
-    constexpr size_t kPlanes = NB * (sizeof(APlanes) + sizeof(BPlanes));
-    constexpr size_t kStage = stage_floats<4>(kBigThreads / 64) * sizeof(float);
-    __shared__ __attribute__((aligned(16))) char lds[kPlanes > kStage ? kPlanes : kStage];
-    run(reinterpret_cast<APlanes*>(lds), reinterpret_cast<BPlanes*>(lds + NB * sizeof(APlanes)));
-  } else {
-    __shared__ __attribute__((aligned(16))) APlanes Ap[NB];
-    __shared__ __attribute__((aligned(16))) BPlanes Bp[NB];
-    run(Ap, Bp);
-  }
+  // one block for the operand planes and, after the products, the staging
+  // of the output tile
+  constexpr size_t kPlanes = NB * (sizeof(APlanes) + sizeof(BPlanes));
+  constexpr size_t kStage = stage_floats<4>(kBigThreads / 64) * sizeof(float);
+  __shared__ __attribute__((aligned(16))) char lds[kPlanes > kStage ? kPlanes : kStage];
+  bf16_big_tile<MODE, NP, SCALED>(g, task, reinterpret_cast<APlanes*>(lds),
+                                  reinterpret_cast<BPlanes*>(lds + NB * sizeof(APlanes)));
 }
 
 // The per-matrix decisions of a phase end without a Gram launch (kActStop
@@ -1902,27 +1854,19 @@ hipError_t launch_fro(const DevTables& t, const FroArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// segment 0: interior tiles; segment 1: ragged tiles (bounds-checked loads)
 template <int MODE, int NP, bool SCALED>
 static void launch_bf16_segments(const Task* tasks, const int* off, const int* cnt, const GemmArgs& g0,
                                  hipStream_t st) {
   GemmArgs g = g0;
   const dim3 block(kGemmThreads);
-  // segment 0 holds both storage orders unless segment 1 takes the
-  // column-major tiles (then each has a launch of its own)
-  if (cnt[0] && cnt[1]) {
+  if (cnt[0]) {
     g.tasks = tasks + off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastT0, SCALED>), dim3(cnt[0]), block, 0, st, g);
-  } else if (cnt[0]) {
-    g.tasks = tasks + off[0];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastAny, SCALED>), dim3(cnt[0]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFast, SCALED>), dim3(cnt[0]), block, 0, st, g);
   }
   if (cnt[1]) {
     g.tasks = tasks + off[1];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kFastT1, SCALED>), dim3(cnt[1]), block, 0, st, g);
-  }
-  if (cnt[2]) {
-    g.tasks = tasks + off[2];
-    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kGeneric, SCALED>), dim3(cnt[2]), block, 0, st, g);
+    hipLaunchKernelGGL((gemm_bf16_kernel<MODE, NP, kGeneric, SCALED>), dim3(cnt[1]), block, 0, st, g);
   }
 }
 
@@ -1934,17 +1878,10 @@ static void launch_big_cover(const TaskList& L, const GemmArgs& g0, hipStream_t 
   const dim3 block(kBigThreads);
   // (the planner lists 256 x 256 tiles for the update products only)
   if constexpr (MODE == kUpdate) {
-  if (L.big_cnt[0] && L.big_cnt[1]) {
-    g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT0, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
-  } else if (L.big_cnt[0]) {
-    g.tasks = L.tasks + L.big_off[0];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastAny, SCALED>), dim3(L.big_cnt[0]), block, 0, st, g);
-  }
-  if (L.big_cnt[1]) {
-    g.tasks = L.tasks + L.big_off[1];
-    hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, kFastT1, SCALED>), dim3(L.big_cnt[1]), block, 0, st, g);
-  }
+    if (L.big_cnt) {
+      g.tasks = L.tasks + L.big_off;
+      hipLaunchKernelGGL((gemm_bf16_big_kernel<MODE, NP, SCALED>), dim3(L.big_cnt), block, 0, st, g);
+    }
   }
   launch_bf16_segments<MODE, NP, SCALED>(L.tasks, L.rem_off, L.rem_cnt, g0, st);
 }
@@ -1962,7 +1899,7 @@ static void launch_mode(const TaskList& L, const GemmArgs& g0, int arith, hipStr
   if (arith == kArithFp32) {
     GemmArgs g = g0;
     g.tasks = L.tasks;
-    const int n = L.seg_cnt[0] + L.seg_cnt[1] + L.seg_cnt[2];
+    const int n = L.seg_cnt[0] + L.seg_cnt[1];
     if (n) hipLaunchKernelGGL(gemm_f32_kernel<MODE>, dim3(n), dim3(kGemmThreads), 0, st, g);
   } else if (arith == kArithBf16x6) {
     launch_bf16<MODE, 6>(L, g0, st);

@@ -27,21 +27,18 @@ constexpr int kSchedClasses = 2;
 constexpr int kSchedSquare = 0;
 constexpr int kSchedTall = 1;
 
-// One corrected matrix.  "Tall" coordinates: X is m x n with m >= n; the
-// element X[r][c] sits at ws_off + r * sr + c * sc in the workspace buffers,
-// with (sr, sc) = (n, 1) if trans == 0 and (1, m) (column-major) if trans ==
-// 1, which the planner sets for every matrix: a tensor stored wide is then in
-// its own row-major layout, a square one in its row-major bytes (read
-// column-major they are its transpose, whose polar factor is the transposed
-// one: the same bytes), and a tall one (rows > cols) is transposed tile by
-// tile by the streaming kernels.
+// One corrected matrix.  "Tall" coordinates: X is m x n with m >= n, stored
+// column-major: X[r][c] at ws_off + r + c * m in the workspace buffers.  A
+// tensor stored wide is then in its own row-major layout, a square one in
+// its row-major bytes (read column-major they are its transpose, whose polar
+// factor is the transposed one: the same bytes), and a tall one (rows >
+// cols) is transposed tile by tile by the streaming kernels.
 struct MatInfo {
   int64_t ws_off;    // element offset in the Delta / X buffers (64-element aligned)
   int64_t src_off;   // element offset in theta / momentum / workers
   int64_t sq_off;    // element offset of this matrix's n x n buffers (Gram, polynomial)
   int64_t part_off;  // element offset of the split-K Gram partials (ksplit * n * n)
   int32_t m, n;      // tall shape
-  int32_t trans;     // 1: column-major in tall coordinates
   int32_t ksplit;    // number of K slices of the Gram product (1 = no split)
   int32_t kchunk;    // rows of X per K slice (multiple of kBK)
   int32_t vec;       // 1 if m and n are multiples of 4 (vector loads allowed)
