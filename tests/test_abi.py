@@ -219,7 +219,7 @@ def test_schedule_length_default():
 
 
 def test_big_layout_plans_quickly():
-    from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
+    from workload import WORKLOADS, LLAMA_110M, LLAMA_341M, LLAMA_888M
     for name in (LLAMA_110M, LLAMA_341M, LLAMA_888M):
         c = WORKLOADS[name]
         h = iso.isoloco_plan(c.layout, c.n_elems, c.K, 0 if c.worker_dtype == "f32" else 1)

@@ -8,7 +8,6 @@ smaller input (another plan: its tables are copied into the array first),
 then a second step of that plan (no copy), and the statistics rule after
 another plan has used the array.
 """
-import numpy as np
 import pytest
 
 from _helpers import KIND_AVG, KIND_ISO
