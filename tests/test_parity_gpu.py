@@ -212,8 +212,11 @@ def test_split_k_gram(iso, precision):
     plan.close()
 
 
-@pytest.mark.parametrize("precision", [0, 2], ids=["mixed", "bf16x3"])
+@pytest.mark.parametrize("precision", [0, 2, 3], ids=["mixed", "bf16x3", "bf16x6"])
 def test_big_tiles_with_remainders(iso, precision):
+    """256 x 256 update tiles beside the 128 x 128 tiles they leave over, in
+    the modes whose updates take the 1024-thread kernel (mixed: bf16x5 and
+    bf16x3; bf16x3) and the 512-thread one (bf16x6)."""
     from workload import custom_layout
     lay, n = custom_layout(BIG_MIXED, align=4)
     _run_and_compare(iso, _cfg(lay, n, K=3), opts=dict(precision=precision))
