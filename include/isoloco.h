@@ -143,7 +143,7 @@ typedef struct {
                         tall matrices on the caller's stream and the others on a second
                         stream of the plan's (forked after the reduction, joined before the
                         scale), so that each fills the other's launch gaps and last waves;
-                        0 (default): 2 when the corrected matrices hold at most 2^28
+                        0 (default): 2 when the corrected matrices hold at most 2^29
                         elements, else 1 (large products compete for the caches instead)  */
   int32_t factored;  /* 1: the tall matrices take the steps from s to the end of their first
                         phase on n x n factors: with A = X_s^T X_s, X_k = X_s M gives

@@ -84,8 +84,10 @@ constexpr float kResolutionBound = 2e-8f;
 // (about 5x the rounding floor of the split-bf16 Gram; the polar factor is then
 // within about half this value of the exact one)
 constexpr float kSwitchTol = 5e-5f;
-// Default streams = 2 for plans whose corrected matrices hold at most this many elements.
-constexpr int64_t kTwoStreamMaxElems = (int64_t)1 << 28;
+// Default streams = 2 for plans whose corrected matrices hold at most this
+// many elements (341M-parameter workload, 3.4e8: two streams 1% faster; 888M,
+// 8.9e8: 5% slower, its large products competing for the caches).
+constexpr int64_t kTwoStreamMaxElems = (int64_t)1 << 29;
 // The tall class iterates on n x n factors from step s to the end of its
 // first phase: X_k = X_s M with A = X_s^T X_s makes X_k^T X_k = M A M, so
 // those steps need n x n products only (M <- M p(M A M)), and X = X_s M is
