@@ -445,7 +445,9 @@ def main():
                    "polar_phase_ends": phase_ends, "tall_factored_steps": list(factored),
                    "alpha": cfg.alpha, "outer_lr": cfg.outer_lr, "mu": cfg.mu},
         "roofline": {"bound": "mfma", "kernel": "batched polar products (gemm_%s: Gram, polynomial, update)" %
-                     ("f32_kernel" if args.precision == "fp32" else "bf16_kernel, gemm_bf16_big_kernel"),
+                     ("f32_kernel" if args.precision == "fp32" else
+                      "bf16_kernel, gemm_bf16_big_kernel" if args.precision == "bf16x6" else
+                      "bf16_kernel, gemm_bf16_big16_kernel"),
                      "achieved": round(gemm_tfs, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(gemm_tfs / peak, 4),
                      "work": "the method's products as fp32 flops (symmetric Gram n(n+1)m, polynomial "
