@@ -55,6 +55,12 @@ def gemm_flops_per_step(layout, stats, check, precision, factored=(0, 0)):
     n (n+1) n each).  Split-bf16 products issue one MFMA product per part
     product (3, 5 or 6)."""
     early, late = PARTS[precision]
+    first, end = factored
+
+    def upd_parts(j):
+        # the update kernel's products of step j (the factored steps' A M too)
+        return early if j < X6_STEPS else late
+
     f = 0
     fm = 0
     for (_, r, c, kind), st in zip(layout, stats):
@@ -65,12 +71,19 @@ def gemm_flops_per_step(layout, stats, check, precision, factored=(0, 0)):
         poly = n * (n + 1) * n
         upd = 2 * m * n * n
         s = st.steps
-        e = min(s, X6_STEPS)
         k = factored_count(m, n, s, factored)
         nn = 2 * n ** 3 + 2 * n * (n + 1) * n
         f += s * (gram + poly + upd) + (gram if check else 0) + k * (nn - gram - upd)
-        fm += (s * (gram + poly) * late + (e * early + (s - e) * late) * upd + (gram * late if check else 0)
-               + k * (nn - gram - upd) * late)
+        # issued: the Grams, polynomials and the factored steps' M B and M P at
+        # the late part count; each update (and A M) at its step's
+        fm += ((s - k + (1 if check else 0)) * gram + s * poly + k * 2 * n * (n + 1) * n) * late
+        for j in range(s):
+            if k and first < j < end:
+                fm += 2 * n ** 3 * upd_parts(j)
+            elif k and j == first:
+                fm += upd * upd_parts(end - 1)  # X = X_first M, launched as step end - 1's update
+            else:
+                fm += upd * upd_parts(j)
     return f, fm
 
 
