@@ -602,21 +602,39 @@ def test_not_converged_flag(iso):
 def test_config3_full_size_sampled(iso):
     """24 blocks d = 1024 / FFN 2816 + 32000 x 1024 (341M parameters), K = 32
     bf16 replicas with per-tensor scales from LogUniform(1e-4, 1e-2): 1-D
-    tensors and one tensor of each shape against the oracle, properties for
-    all 169 matrices."""
+    tensors, one tensor of each shape and the four matrices that took the
+    most steps against the oracle, properties for all 169 matrices."""
     from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
     cfg = WORKLOADS[LLAMA_341M]
-    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=_one_of_each_shape(cfg.layout),
-                                                      return_inputs=True, max_flagged=1)
+    sample = _one_of_each_shape(cfg.layout)
+    theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True,
+                                                      max_flagged=1)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
+    del theta, mom, th_in, workers
+    _deepest_against_oracle(iso, cfg, st, sample, 4)
+
+
+def _deepest_against_oracle(iso, cfg, st, sample, count):
+    """The matrices that took the most polar steps (the deepest phases, the
+    hardest spectra) against the oracle too: a second run of the same step
+    (the same inputs from the same seed, and the step is deterministic: the
+    same step counts), with the oracle on those matrices."""
+    torch.cuda.empty_cache()
+    mats = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_ISO]
+    deep = [i for i in sorted(mats, key=lambda i: (-st[i].steps, i)) if i not in sample][:count]
+    print("deepest matrices:", [(i, st[i].steps) for i in deep], flush=True)
+    # (in this process: the compiled Jacobi loop's threads share one matrix)
+    _, _, st2 = _run_and_compare(iso, cfg, select=deep, max_flagged=1)
+    assert [s.steps for s in st2] == [s.steps for s in st]
 
 
 @pytest.mark.timeout(900)
 def test_config4_full_size_sampled(iso):
     """16 blocks d = 2048 / FFN 5632 + 32000 x 2048 (888M parameters), K = 64
     bf16 replicas (114 GB in HBM): 1-D tensors, one matrix of each shape
-    (square, tall, wide-stored and the 32000 x 2048 embedding) against the
-    oracle, properties for all 113 matrices."""
+    (square, tall, wide-stored and the 32000 x 2048 embedding) and the
+    matrix that took the most steps against the oracle, properties for all
+    113 matrices."""
     from workload import WORKLOADS, SMALL, BLOCK, LLAMA_110M, LLAMA_341M, LLAMA_888M
     cfg = WORKLOADS[LLAMA_888M]
     sample = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_AVG]
@@ -625,6 +643,8 @@ def test_config4_full_size_sampled(iso):
     theta, mom, st, th_in, workers = _run_and_compare(iso, cfg, select=sample, return_inputs=True,
                                                       max_flagged=1)
     _check_polar_properties(cfg.layout, st, mom, th_in, workers)
+    del theta, mom, th_in, workers
+    _deepest_against_oracle(iso, cfg, st, sample, 1)
 
 
 def _planted(rows, cols, smin, rng):
