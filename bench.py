@@ -239,8 +239,8 @@ def _oracle_tensor(job):
 def cpu_full_step(cfg, theta, workers, mom, variant=None):
     """The float64 oracle on every tensor of the step, in a pool of freshly
     started processes (nothing forked after the GPU was used; one thread each,
-    as many as the host's cores up to 16, a one-GPU machine's CPU share), largest
-    tensors first: the step's wall time, with its total CPU time."""
+    as many as the host's cores up to 16), largest tensors first: the step's
+    wall time, with its total CPU time."""
     import multiprocessing as mp
     th = theta.cpu().numpy()
     mo = mom.cpu().numpy()
@@ -302,8 +302,8 @@ def main():
                     help="the same for the other matrices")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build measures one GPU; the IsoLoCo step here runs unsharded on a "
-              "single MI355X (--gpus %d is not supported)" % args.gpus, file=sys.stderr)
+        print("bench.py: the IsoLoCo step runs unsharded on a single MI355X; only --gpus 1 is "
+              "supported (got --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -65,7 +65,7 @@ typedef enum {
   ISOLOCO_ERR_ALIAS = -4,       /* theta, momentum, a worker or the workspace overlap            */
   ISOLOCO_ERR_WORKSPACE = -5,   /* workspace missing, too small or misaligned                    */
   ISOLOCO_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed                    */
-  ISOLOCO_ERR_UNSUPPORTED = -7  /* a valid request this build does not implement                 */
+  ISOLOCO_ERR_UNSUPPORTED = -7  /* a valid request the library does not implement                */
 } isoloco_status;
 
 typedef enum { ISOLOCO_F32 = 0, ISOLOCO_BF16 = 1 } isoloco_dtype;

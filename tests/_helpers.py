@@ -55,8 +55,7 @@ def variant_opts(variant):
 
 
 def oracle_pool_size():
-    """Worker processes for the oracle: the host's cores, at most 16 (the CPU
-    share of a one-GPU machine)."""
+    """Worker processes for the oracle: the host's cores, at most 16."""
     import os
     return max(1, min(16, len(os.sched_getaffinity(0))))
 
