@@ -924,7 +924,7 @@ isoloco_status isoloco_plan(const isoloco_tensor* layout, int32_t n_tensors, int
     if (o.streams == 0) {
       // Two streams fill each other's launch gaps and partial last waves,
       // which matter while launches are short; for large matrices the
-      // concurrent products rather compete for the caches (same-box
+      // concurrent products rather compete for the caches (paired
       // measurements: 109.5M parameters 2% faster, 341M 1%, 888M 4% slower).
       int64_t n2d = 0;
       for (const MatInfo& mi : p->mats) n2d += (int64_t)mi.m * mi.n;
