@@ -561,6 +561,25 @@ def test_config2_embedding_excluded(iso):
     assert st[emb].steps == 0 and st[emb].fro_norm == -1.0
 
 
+@pytest.mark.parametrize("precision", [2, 3, 1], ids=["bf16x3", "bf16x6", "fp32"])
+def test_config2_precision_modes(iso, precision):
+    """The 109.5M workload at full size in the other product arithmetics:
+    every vector, one matrix of each shape and the four matrices that took
+    the most polar steps against the oracle (bf16x3 is within the contract
+    for these spectra, its worst matrix near 4e-4)."""
+    from workload import WORKLOADS, LLAMA_110M
+    cfg = WORKLOADS[LLAMA_110M]
+    sample = _one_of_each_shape(cfg.layout)
+    print("case: precision %d" % precision, flush=True)
+    _, _, st = _run_and_compare(iso, cfg, select=sample, opts=dict(precision=precision), max_flagged=1)
+    torch.cuda.empty_cache()
+    mats = [i for i, t in enumerate(cfg.layout) if t[3] == KIND_ISO]
+    deep = [i for i in sorted(mats, key=lambda i: (-st[i].steps, i)) if i not in sample][:4]
+    print("deepest matrices:", [(i, st[i].steps) for i in deep], flush=True)
+    _, _, st2 = _run_and_compare(iso, cfg, select=deep, opts=dict(precision=precision), max_flagged=1)
+    assert [s.steps for s in st2] == [s.steps for s in st]
+
+
 def test_not_converged_flag(iso):
     """A step cap too short for the spectrum (max_steps = 3 on a 256 x 256
     matrix with singular values spread over [1e-5, 1]): the not-converged
