@@ -177,3 +177,36 @@ def test_worker_order_invariance(iso):
             sl = slice(off, off + rows * cols)
             e = relF(b[sl], ref_b[sl])
             assert e <= 1e-4, (order, rows, cols, e)
+
+
+@pytest.mark.parametrize("precision", [0, 1], ids=["mixed", "fp32"])
+def test_isotropic_fixed_point(iso, precision):
+    """A pseudo-gradient whose singular values are all equal is its own
+    correction: its polar factor is Delta / s and its mean singular value s,
+    so D = Delta (Algorithm 2 with alpha = 1), and with mu = 0 and eta = 1
+    the step moves theta by -Delta and sets B = Delta; the matrices stop at
+    their first check (every singular value is 1 after the normalisation)."""
+    lay, n = _layout()
+    rng = np.random.default_rng(11)
+    d = np.zeros(n)
+    for off, rows, cols, kind in lay:
+        if kind == KIND_ISO:
+            r = min(rows, cols)
+            U, _ = np.linalg.qr(rng.standard_normal((rows, r)))
+            V, _ = np.linalg.qr(rng.standard_normal((cols, r)))
+            d[off:off + rows * cols] = (3e-3 * U @ V.T).reshape(-1)
+        else:
+            d[off:off + rows * cols] = 1e-3 * rng.standard_normal(rows * cols)
+    d = d.astype(np.float32)
+    th, b, st = _step(iso, lay, n, [-d], alpha=1.0, lr=1.0, mu=0.0, opts=dict(precision=precision))
+    for i, (off, rows, cols, kind) in enumerate(lay):
+        sl = slice(off, off + rows * cols)
+        e_b = relF(b[sl], d[sl])
+        e_th = relF(th[sl], -d[sl])
+        print("tensor %d (%dx%d kind %d): B %.2e theta %.2e steps %d" % (i, rows, cols, kind, e_b, e_th,
+                                                                          st[i].steps), flush=True)
+        # 5e-5: the phase-end check's tolerance, about five times the rounding
+        # floor of the split-bf16 products (measured: 1e-5 mixed, 1e-6 fp32)
+        assert e_b <= 5e-5 and e_th <= 5e-5
+        if kind == KIND_ISO:
+            assert abs(st[i].sigma_bar - 3e-3) <= 5e-5 * 3e-3
