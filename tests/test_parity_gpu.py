@@ -297,7 +297,7 @@ def _random_shapes(rng):
     return shapes
 
 
-@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("seed", range(16))
 def test_random_layouts(iso, seed):
     """Seeded random layouts packed without alignment, K from 1 to 6, float32
     or bfloat16 replicas, the mixed, fp32 or bf16x6 products (bf16x3 is
