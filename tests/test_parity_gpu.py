@@ -315,6 +315,28 @@ def test_random_layouts(iso, seed):
                      max_flagged=1)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_random_big_tile_layouts(iso, seed):
+    """Seeded random matrices whose sides are multiples of 4 (short sides 256
+    to about 800, long sides up to about 2800), so that the updates run on
+    256 x 256 tiles with 128 x 128 remainders of every kind (odd strips,
+    ragged edges), tall and square-ish, in the mixed, bf16x3 or bf16x6
+    products; every tensor against the oracle."""
+    from workload import custom_layout
+    rng = np.random.default_rng(2000 + seed)
+    shapes = []
+    for _ in range(int(rng.integers(3, 6))):
+        n = 4 * int(rng.integers(64, 200))
+        m = 4 * int(rng.integers(n // 4, n // 2 + 80)) if rng.random() < 0.6 else 4 * int(rng.integers(n // 2, n))
+        shapes.append((m, n, KIND_ISO) if rng.random() < 0.5 else (n, m, KIND_ISO))
+    shapes.append((int(rng.integers(1, 500)), 1, KIND_AVG))
+    lay, n_el = custom_layout(shapes, align=4)
+    K = int(rng.integers(1, 5))
+    precision = int(rng.choice([0, 2, 3]))
+    print("case: seed %d K %d precision %d shapes %s" % (seed, K, precision, shapes), flush=True)
+    _run_and_compare(iso, _cfg(lay, n_el, K=K), seed=seed, opts=dict(precision=precision), max_flagged=1)
+
+
 def test_single_worker(iso):
     from workload import custom_layout
     lay, n = custom_layout([(96, 80, KIND_ISO), (80, 1, KIND_AVG)], align=4)
